@@ -1,0 +1,515 @@
+"""Pins for the CPU oracle (no GPU).
+
+Each test ties the oracle to something other than itself: numpy's IEEE half
+conversion, exact rational arithmetic, hand-worked fixtures under
+tests/golden/, brute-force fp64 / int64 matrix products in numpy, closed-form
+invariants of Eq. (1)/(4), and Theorem 4.1 checked by exhaustive subset search.
+"""
+from __future__ import annotations
+
+import itertools
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+B = 128
+
+
+# ------------------------------------------------------------ helpers ----
+def f16(bits):
+    return np.asarray(bits, np.uint16).view(np.float16).astype(np.float64)
+
+
+def dense_residual(pw, orc):
+    """Residual codes and dequantised residual scattered into dense [N, K]."""
+    N, K = pw.N, pw.K
+    codes = np.zeros((N, K), np.int64)
+    deq = np.zeros((N, K), np.float64)
+    for nb in range(N // B):
+        for p in range(pw.rowptr[nb], pw.rowptr[nb + 1]):
+            kb = pw.kb[p]
+            c = orc.unpack_codes(pw.Rq[p], B).astype(np.int64)
+            codes[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B] = c
+            deq[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B] = c * f16(pw.s_r[p])[:, None]
+    return codes, deq
+
+
+def dequant_base(pw, orc):
+    codes = orc.unpack_codes(pw.Wq, pw.K).astype(np.float64)
+    return codes * np.repeat(f16(pw.s_w), B, axis=1)
+
+
+def exact_round_half_even(fr: Fraction) -> int:
+    fl = fr.numerator // fr.denominator
+    rem = fr - fl
+    if rem > Fraction(1, 2):
+        return fl + 1
+    if rem < Fraction(1, 2):
+        return fl
+    return fl if fl % 2 == 0 else fl + 1
+
+
+def random_layer(M, N, K, nnzb, seed, orc, dense_codes=False):
+    W = synth.gen_weight(N, K, seed)
+    pw = orc.prepare_weight(W, nnzb)
+    X = synth.gen_act(M, K, seed)
+    if dense_codes:   # spread the activations so that most codes are non-zero
+        X = (np.random.default_rng(seed).standard_normal((M, K)) * 3).astype(np.float16)
+    Xq, s_x = orc.quantize_act(X)
+    return W, X, pw, Xq, s_x
+
+
+# --------------------------------------------------------------- fp16 ----
+def test_f16_to_f32_all_bit_patterns(orc):
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    got = orc.f16_bits_to_f32(bits)
+    ref = bits.view(np.float16).astype(np.float32)
+    finite = np.isfinite(ref)
+    assert np.array_equal(got[finite].view(np.uint32), ref[finite].view(np.uint32))
+    assert np.all(np.isnan(got[np.isnan(ref)]))
+    assert np.array_equal(np.isinf(got), np.isinf(ref))
+
+
+def test_f32_to_f16_matches_numpy(orc):
+    rng = np.random.default_rng(1)
+    # wide exponent range, including subnormal halves and overflow
+    mant = rng.random(200000).astype(np.float32) + np.float32(1)
+    expo = rng.integers(-30, 18, 200000)
+    x = (mant * np.exp2(expo).astype(np.float32)) * rng.choice([-1, 1], 200000).astype(np.float32)
+    # exact ties between adjacent halves: (h_i + h_{i+1}) / 2 is exact in fp32
+    h = np.arange(0, 0x7BFF, dtype=np.uint16)
+    lo = h.view(np.float16).astype(np.float32)
+    hi = (h + 1).view(np.float16).astype(np.float32)
+    ties = (lo + hi) / np.float32(2)
+    edge = np.array([0.0, -0.0, 65504, 65519.99, 65520, 70000, 2**-24, 2**-25,
+                     1.5 * 2**-25, 2**-14, 6e-8, 5.96e-8, 1e-10], np.float32)
+    allx = np.concatenate([x, ties, -ties, edge, -edge])
+    got = orc.f32_to_f16_bits(allx)
+    with np.errstate(over="ignore"):
+        ref = allx.astype(np.float16).view(np.uint16)
+    assert np.array_equal(got, ref)
+
+
+# ------------------------------------------------------- quantiser -------
+def _read_ties():
+    cases, cur = [], {}
+    for line in open(os.path.join(GOLDEN, "quant_ties.txt")):
+        line = line.split("#", 1)[0].strip()
+        if not line:
+            continue
+        key, val = line.split(":", 1)
+        cur[key] = val.split()
+        if key == "q":
+            cases.append(cur)
+            cur = {}
+    return cases
+
+
+@pytest.mark.parametrize("case", _read_ties(), ids=lambda c: " ".join(c["x"])[:24])
+def test_quantizer_golden_ties(orc, case):
+    x = np.array([float(v) for v in case["x"]], np.float16)[None, :]
+    xq, s = orc.quantize_act(x) if x.shape[1] % 2 == 0 else orc.quantize_act(
+        np.concatenate([x, np.zeros((1, 1), np.float16)], axis=1))
+    assert float(f16(s)[0]) == float(case["s"][0])
+    codes = orc.unpack_codes(xq, xq.shape[1] * 2)[0][: len(case["q"])]
+    assert codes.tolist() == [int(v) for v in case["q"]]
+
+
+def test_act_quant_exact_rational(orc):
+    """Every code equals the exactly rounded (Fraction) quotient x / s."""
+    rng = np.random.default_rng(7)
+    X = (rng.standard_normal((6, 256)) * np.array([[1], [30], [1e-3], [200], [1e-6], [5]])).astype(np.float16)
+    X[2, 5] = 0
+    Xq, s_x = orc.quantize_act(X)
+    codes = orc.unpack_codes(Xq, 256)
+    for m in range(6):
+        amax = np.abs(X[m].astype(np.float32)).max()
+        s_ref = np.float16(np.float32(amax) / np.float32(7))
+        assert s_x[m] == s_ref.view(np.uint16)
+        s = Fraction(float(s_ref))
+        for k in range(256):
+            if s == 0:
+                assert codes[m, k] == 0
+                continue
+            q = exact_round_half_even(Fraction(float(X[m, k])) / s)
+            assert codes[m, k] == max(-7, min(7, q)), (m, k)
+
+
+def test_act_quant_zero_row_and_bounds(orc):
+    X = np.zeros((3, 128), np.float16)
+    X[1] = np.linspace(-5, 5, 128).astype(np.float16)
+    X[2, 0] = np.float16(65504)
+    Xq, s_x = orc.quantize_act(X)
+    assert s_x[0] == 0 and not Xq[0].any()
+    codes = orc.unpack_codes(Xq, 128)
+    assert codes.min() >= -7 and codes.max() <= 7
+    # |x - s q| <= s/2 on every element (Eq. 1 rounding bound)
+    s = f16(s_x)
+    err = np.abs(X.astype(np.float64) - s[:, None] * codes)
+    assert np.all(err <= s[:, None] / 2 * (1 + 1e-12) + 0.0)
+
+
+def test_weight_quant_groups(orc):
+    rng = np.random.default_rng(3)
+    N, K = 128, 512
+    W = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    W[5, 130] = 0.9            # an outlier only affects its own (row, group)
+    W[7, 256:384] = 0          # an all-zero group
+    Wq, s_w, R = orc.quantize_weight(W)
+    codes = orc.unpack_codes(Wq, K)
+    for n in range(N):
+        for g in range(K // B):
+            v = W[n, g * B:(g + 1) * B]
+            s_ref = np.float16(np.abs(v).max() / np.float32(7))
+            assert s_w[n, g] == s_ref.view(np.uint16)
+    assert s_w[7, 2] == 0 and not codes[7, 256:384].any()
+    # R = W - s q with one fp32 rounding (s q exact)
+    deq = (codes.astype(np.float32) * np.repeat(f16(s_w), B, axis=1).astype(np.float32))
+    assert np.array_equal(R, W - deq)
+    # exact-rational rounding of a sample of entries
+    s_full = np.repeat(f16(s_w), B, axis=1)
+    for (n, k) in rng.integers(0, [N, K], size=(300, 2)):
+        s = s_full[n, k]
+        if s == 0:
+            continue
+        fr = Fraction(float(W[n, k])) / Fraction(float(s))
+        assert codes[n, k] == max(-7, min(7, exact_round_half_even(fr)))
+
+
+def test_weight_quant_near_ties_exact(orc):
+    """Entries one fp32 ulp either side of every half-integer tie t * s: the
+    codes equal exact-rational rounding (an fp32 quotient by an fp16 scale never
+    lands on a tie unless the exact quotient is one)."""
+    rng = np.random.default_rng(12)
+    rows = []
+    for _ in range(64):
+        s = np.float32(np.float16(rng.uniform(0.003, 0.2)))
+        row = np.zeros(B, np.float32)
+        row[0] = np.float32(7) * s                 # sets the scale back to s
+        if np.float16(row[0] / np.float32(7)) != np.float16(s):
+            continue
+        j = 1
+        for t in np.arange(-6.5, 7, 1.0):
+            ts = np.float32(t) * s                 # exact: <= 15 significant bits
+            for w in (ts, np.nextafter(ts, np.float32(np.inf)), np.nextafter(ts, np.float32(-np.inf))):
+                row[j] = w
+                j += 1
+        rows.append(row)
+    W = np.stack(rows)
+    Wq, s_w, _ = orc.quantize_weight(W)
+    codes = orc.unpack_codes(Wq, B)
+    s_all = f16(s_w)[:, 0]
+    for n in range(W.shape[0]):
+        for k in range(B):
+            fr = Fraction(float(W[n, k])) / Fraction(float(s_all[n]))
+            assert codes[n, k] == max(-7, min(7, exact_round_half_even(fr))), (n, k)
+
+
+# ------------------------------------------------ golden tiny layer ------
+def _read_tiny():
+    d = {}
+    for line in open(os.path.join(GOLDEN, "tiny_layer.txt")):
+        line = line.split("#", 1)[0].strip()
+        if line:
+            k, v = line.split(":", 1)
+            d[k.strip()] = v.strip()
+    return d
+
+
+def _sparse(s):
+    out = {}
+    for tok in s.split():
+        i, v = tok.split(":")
+        out[int(i)] = float(v)
+    return out
+
+
+def test_golden_tiny_layer(orc):
+    d = _read_tiny()
+    X = np.zeros((1, B), np.float16)
+    for i, v in _sparse(d["x_nonzero"]).items():
+        X[0, i] = v
+    W = np.zeros((B, B), np.float32)
+    for i, v in _sparse(d["w_row0_nonzero"]).items():
+        W[0, i] = v
+    pw = orc.prepare_weight(W, 1)
+    Xq, s_x = orc.quantize_act(X)
+    assert f16(s_x)[0] == float(d["s_x"])
+    xc = orc.unpack_codes(Xq, B)[0]
+    assert {i: int(v) for i, v in enumerate(xc) if v} == {i: int(v) for i, v in _sparse(d["xq_nonzero"]).items()}
+    assert f16(pw.s_w)[0, 0] == float(d["s_w_row0"])
+    wc = orc.unpack_codes(pw.Wq, B)[0]
+    assert {i: int(v) for i, v in enumerate(wc) if v} == {i: int(v) for i, v in _sparse(d["wq_row0_nonzero"]).items()}
+    assert pw.score[0, 0] == float(d["score"])
+    assert pw.nnzb == 1 and pw.kb.tolist() == [0]
+    assert f16(pw.s_r)[0, 0] == float(d["s_r_row0"])
+    rc = orc.unpack_codes(pw.Rq[0], B)[0]
+    assert {i: int(v) for i, v in enumerate(rc) if v} == {i: int(v) for i, v in _sparse(d["rq_row0_nonzero"]).items()}
+    Tb, Tr, Y = orc.linear(Xq, s_x, pw)
+    assert Tb[0, 0] == int(d["Tb00"]) and Tr[0, 0] == int(d["Tr00"])
+    assert Y[0, 0] == float(d["Y00"])
+    assert np.all(Y[0, 1:] == 0)
+    pw0 = orc.prepare_weight(W, 0)
+    _, Tr0, Y0 = orc.linear(Xq, s_x, pw0)
+    assert Y0[0, 0] == float(d["Y00_base_only"]) and not Tr0.any()
+
+
+# ------------------------------------------- linear layer vs brute force --
+@pytest.mark.parametrize("M,N,K,pct", [(1, 128, 128, 100), (3, 256, 256, 25),
+                                       (17, 384, 256, 50), (5, 256, 384, 0),
+                                       (2, 128, 512, 100)])
+@pytest.mark.parametrize("dense", [False, True])
+def test_linear_vs_bruteforce(orc, M, N, K, pct, dense):
+    nnzb = synth.budget(N, K, pct)
+    W, X, pw, Xq, s_x = random_layer(M, N, K, nnzb, 11 + M + N + K, orc, dense_codes=dense)
+    Tb, Tr, Y = orc.linear(Xq, s_x, pw)
+    xc = orc.unpack_codes(Xq, K).astype(np.int64)
+    wc = orc.unpack_codes(pw.Wq, K).astype(np.int64)
+    rcodes, rdeq = dense_residual(pw, orc)
+    assert np.array_equal(Tb, xc @ wc.T)
+    assert np.array_equal(Tr, xc @ rcodes.T)
+    # fp64 product of the dequantised operands: Q(X) [Q(W) + M (.) Q(R)]^T
+    Wmq = dequant_base(pw, orc) + rdeq
+    Yref = (xc * f16(s_x)[:, None]) @ Wmq.T
+    scale = max(np.abs(Yref).max(), 1e-300)
+    assert np.abs(Y - Yref).max() <= 1e-12 * scale
+    if pct == 0:
+        assert not Tr.any()
+    if dense:
+        assert np.count_nonzero(xc) > xc.size // 2
+
+
+def test_linear_density0_is_plain_w4a4(orc):
+    W, X, pw0, Xq, s_x = random_layer(4, 256, 256, 0, 5, orc, dense_codes=True)
+    _, _, pw1, _, _ = random_layer(4, 256, 256, 2, 5, orc, dense_codes=True)
+    Tb0, Tr0, Y0 = orc.linear(Xq, s_x, pw0)
+    Tb1, Tr1, Y1 = orc.linear(Xq, s_x, pw1)
+    assert not Tr0.any() and np.array_equal(Tb0, Tb1)   # base is budget-independent
+    # plain W4A4: s_x * sum_g s_w A_b, computed here group by group in numpy
+    xc = orc.unpack_codes(Xq, 256).astype(np.int64)
+    wc = orc.unpack_codes(pw0.Wq, 256).astype(np.int64)
+    ref = np.zeros_like(Y0)
+    for g in range(2):
+        ab = xc[:, g * B:(g + 1) * B] @ wc[:, g * B:(g + 1) * B].T
+        ref += ab * f16(pw0.s_w)[:, g][None, :]
+    ref *= f16(s_x)[:, None]
+    assert np.abs(Y0 - ref).max() <= 1e-12 * np.abs(ref).max()
+    # linearity of Eq. (4): T(rho) = Tb + Tr, and Tr only on selected blocks
+    assert Tr1.any()
+
+
+def test_linear_sampled_matches_full(orc):
+    W, X, pw, Xq, s_x = random_layer(9, 384, 256, 3, 21, orc, dense_codes=True)
+    Tb, Tr, Y = orc.linear(Xq, s_x, pw)
+    rng = np.random.default_rng(0)
+    ms = rng.integers(0, 9, 200)
+    ns = rng.integers(0, 384, 200)
+    tb, tr, y = orc.linear_sampled(Xq, s_x, pw, ms, ns)
+    assert np.array_equal(tb, Tb[ms, ns]) and np.array_equal(tr, Tr[ms, ns])
+    assert np.array_equal(y, Y[ms, ns])
+
+
+def test_int32_range_extremes(orc):
+    """All codes at +-7 over a long K: accumulators stay exact and in int32."""
+    K, N, M = 28672, 128, 2
+    Xq = np.full((M, K // 2), 0x77, np.uint8)                 # +7 everywhere
+    Xq[1] = 0x99                                              # -7 everywhere
+    s_x = np.full(M, np.float16(1).view(np.uint16))
+    W = np.full((N, K), 0.7, np.float32)
+    pw = orc.prepare_weight(W, 0)
+    Tb, Tr, Y = orc.linear(Xq, s_x, pw)
+    assert Tb[0, 0] == 49 * K and Tb[1, 0] == -49 * K and not Tr.any()
+
+
+# ---------------------------------------- residual / reconstruction ------
+def test_reconstruction_improves(orc):
+    N, K = 512, 512
+    W = synth.gen_weight(N, K, 99)
+    for pct in (10, 50, 100):
+        pw = orc.prepare_weight(W, synth.budget(N, K, pct))
+        base = dequant_base(pw, orc)
+        _, rdeq = dense_residual(pw, orc)
+        R = W.astype(np.float64) - base
+        e_base = np.linalg.norm(W - base)
+        e_mq = np.linalg.norm(W - (base + rdeq))
+        assert e_mq < e_base
+        # entrywise on selected blocks: |R - Q(R)| <= |R| (0 is on the grid)
+        sel = np.repeat(np.repeat(pw.mask, B, 0), B, 1)
+        assert np.all(np.abs(R - rdeq)[sel] <= np.abs(R)[sel] + 1e-15)
+        assert np.all(rdeq[~sel] == 0)
+        # memory overhead of the residual = selected fraction of the base bytes
+        assert pw.Rq.nbytes / pw.Wq.nbytes == pytest.approx(pw.nnzb / pw.mask.size)
+
+
+def test_residual_quant_is_eq1_per_block_row(orc):
+    N, K = 256, 384
+    W = synth.gen_weight(N, K, 8)
+    pw = orc.prepare_weight(W, 3)
+    _, _, R = orc.quantize_weight(W)
+    for nb in range(N // B):
+        for p in range(pw.rowptr[nb], pw.rowptr[nb + 1]):
+            kb = pw.kb[p]
+            blk = R[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B]
+            for r in range(0, B, 17):
+                s_ref = np.float16(np.abs(blk[r]).max() / np.float32(7))
+                assert pw.s_r[p, r] == s_ref.view(np.uint16)
+                codes = orc.unpack_codes(pw.Rq[p, r:r + 1], B)[0]
+                qf = np.clip(np.rint(blk[r] / np.float32(s_ref)), -7, 7)
+                assert np.array_equal(codes, qf.astype(np.int8))
+
+
+# ------------------------------------------------------------- selection --
+def test_scores_and_topk_bruteforce(orc):
+    N, K = 640, 768
+    W = synth.gen_weight(N, K, 4)
+    Wq, s_w, R = orc.quantize_weight(W)
+    score = orc.block_scores_frob(R)
+    ref = (R.astype(np.float64) ** 2).reshape(N // B, B, K // B, B).sum(axis=(1, 3))
+    assert np.allclose(score, ref, rtol=1e-12, atol=0)
+    for nnzb in (0, 1, 7, 30):
+        rowptr, kb, mask = orc.select_topk(score, nnzb)
+        order = np.lexsort((np.arange(score.size), -score.ravel()))
+        want = np.zeros(score.size, bool)
+        want[order[:nnzb]] = True
+        assert np.array_equal(mask.ravel(), want)
+        # CSR validity: ascending kb per row, counts match the mask
+        assert rowptr[0] == 0 and rowptr[-1] == nnzb
+        for nb in range(N // B):
+            row = kb[rowptr[nb]:rowptr[nb + 1]]
+            assert np.all(np.diff(row) > 0)
+            assert set(row.tolist()) == set(np.flatnonzero(want.reshape(N // B, -1)[nb]).tolist())
+
+
+def test_topk_ties_lower_index_wins(orc):
+    score = np.array([[1.0, 3.0, 3.0], [3.0, 0.0, 3.0]])
+    rowptr, kb, mask = orc.select_topk(score, 2)
+    assert mask.tolist() == [[False, True, True], [False, False, False]]
+    rowptr, kb, mask = orc.select_topk(score, 3)
+    assert mask.tolist() == [[False, True, True], [True, False, False]]
+    assert rowptr.tolist() == [0, 2, 3] and kb.tolist() == [1, 2, 0]
+    with pytest.raises(ValueError):
+        orc.select_topk(score, 7)
+
+
+def test_skewed_generator_selects_designated(orc):
+    """Residual-norm selection returns exactly the designated skew blocks."""
+    N, K = 2048, 1024
+    nnzb = synth.budget(N, K, 10)
+    des, n_hot = synth.skew_blocks(N, K, nnzb, 1234)
+    W = synth.gen_weight(N, K, 1234, designated=des)
+    pw = orc.prepare_weight(W, nnzb)
+    assert np.array_equal(pw.mask, des)
+    assert n_hot == round(0.8 * nnzb)
+
+
+# ------------------------------------- Algorithm 1 / Theorem 4.1 ---------
+def _surrogate(R, h, rdeq_full, sel_blocks, NB, KB):
+    E = R.copy()
+    for b in sel_blocks:
+        nb, kb = divmod(b, KB)
+        E[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B] -= rdeq_full[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B]
+    return float(np.sum(h[None, :] * E ** 2))
+
+
+def _all_block_qr(R, orc):
+    """Q(R) of every block (Eq. 1 per block row), dense fp64."""
+    N, K = R.shape
+    out = np.zeros((N, K))
+    for nb in range(N // B):
+        for kb in range(K // B):
+            blk = np.ascontiguousarray(R[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B])
+            for r in range(B):
+                s = np.float16(np.abs(blk[r]).max() / np.float32(7))
+                if s == 0:
+                    continue
+                q = np.clip(np.rint(blk[r] / np.float32(s)), -7, 7)
+                out[nb * B + r, kb * B:(kb + 1) * B] = q * float(s)
+    return out
+
+
+def test_dhessian_topk_optimal_for_diagonal_surrogate(orc):
+    """Theorem 4.1: top-K by S_B minimises sum_ij h_j (R - M_S (.) Q(R))^2."""
+    N, K = 384, 384                         # 9 blocks
+    rng = np.random.default_rng(5)
+    W = synth.gen_weight(N, K, 77)
+    X = (rng.standard_normal((64, K)) * rng.uniform(0.1, 3, K)).astype(np.float16)
+    _, _, R = orc.quantize_weight(W)
+    h = orc.hessian_diag(X)
+    # h_j = (2/T) sum_t X_tj^2, checked directly
+    assert np.allclose(h, 2 / 64 * (X.astype(np.float64) ** 2).sum(0), rtol=1e-12)
+    S = orc.block_scores_dhessian(R, h)
+    qr = _all_block_qr(R.astype(np.float64), orc)
+    NB, KB = N // B, K // B
+    for b in range(NB * KB):   # S_B = [L(0) - L({B})]_+ on the surrogate
+        d = _surrogate(R.astype(np.float64), h, qr, [], NB, KB) - _surrogate(R.astype(np.float64), h, qr, [b], NB, KB)
+        assert S.ravel()[b] == pytest.approx(max(d, 0.0), rel=1e-9, abs=1e-18)
+    for Kb in (1, 2, 3, 4):
+        best = min(itertools.combinations(range(NB * KB), Kb),
+                   key=lambda s: _surrogate(R.astype(np.float64), h, qr, s, NB, KB))
+        _, _, mask = orc.select_topk(S, Kb)
+        sel = tuple(np.flatnonzero(mask.ravel()))
+        assert _surrogate(R.astype(np.float64), h, qr, sel, NB, KB) == pytest.approx(
+            _surrogate(R.astype(np.float64), h, qr, best, NB, KB), rel=1e-12)
+
+
+def test_dhessian_exact_when_offdiagonal_zero(orc):
+    """App. A: with orthogonal activation columns (O = 0) the Delta-Hessian
+    top-K equals the exhaustive optimum of the exact output distortion."""
+    N, K = 256, 384                         # 6 blocks
+    rng = np.random.default_rng(9)
+    W = synth.gen_weight(N, K, 31)
+    T = K
+    X = np.zeros((T, K), np.float16)        # token t only touches channel t
+    X[np.arange(K), np.arange(K)] = rng.uniform(0.2, 4.0, K).astype(np.float16)
+    Xd = X.astype(np.float64)
+    assert np.count_nonzero(Xd.T @ Xd - np.diag(np.diag(Xd.T @ Xd))) == 0
+    _, _, R = orc.quantize_weight(W)
+    h = orc.hessian_diag(X)
+    S = orc.block_scores_dhessian(R, h)
+    qr = _all_block_qr(R.astype(np.float64), orc)
+    NB, KB = N // B, K // B
+
+    def exact(sel):
+        E = R.astype(np.float64).copy()
+        for b in sel:
+            nb, kb = divmod(b, KB)
+            E[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B] -= qr[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B]
+        return 2 / T * np.linalg.norm(Xd @ E.T) ** 2
+
+    for Kb in (1, 2, 3):
+        best = min(itertools.combinations(range(NB * KB), Kb), key=exact)
+        _, _, mask = orc.select_topk(S, Kb)
+        sel = tuple(np.flatnonzero(mask.ravel()))
+        assert exact(sel) == pytest.approx(exact(best), rel=1e-12)
+
+
+def test_planted_mistakes_are_caught(orc):
+    """The brute-force pins fail for plausible oracle mistakes (planted here,
+    on the CPU, in numpy restatements of the oracle's output)."""
+    W, X, pw, Xq, s_x = random_layer(3, 256, 256, 2, 17, orc, dense_codes=True)
+    Tb, Tr, Y = orc.linear(Xq, s_x, pw)
+    xc = orc.unpack_codes(Xq, 256).astype(np.int64)
+    wc = orc.unpack_codes(pw.Wq, 256).astype(np.int64)
+    rcodes, rdeq = dense_residual(pw, orc)
+    Yref = (xc * f16(s_x)[:, None]) @ (dequant_base(pw, orc) + rdeq).T
+    tol = 1e-12 * np.abs(Yref).max()
+    # dropped residual term
+    assert np.abs((Y - (xc * f16(s_x)[:, None]) @ rdeq.T) - Yref).max() > tol
+    # transposed residual block (rows <-> columns inside a block)
+    rdeq_t = rdeq.copy()
+    for nb in range(2):
+        for kb in range(2):
+            blk = rdeq_t[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B]
+            rdeq_t[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B] = blk.T
+    assert np.abs((xc * f16(s_x)[:, None]) @ (dequant_base(pw, orc) + rdeq_t).T - Yref).max() > tol
+    # swapped nibble order
+    wsw = np.empty_like(wc)
+    wsw[:, 0::2], wsw[:, 1::2] = wc[:, 1::2], wc[:, 0::2]
+    assert not np.array_equal(xc @ wsw.T, Tb)
+    # sign error on the residual
+    assert not np.array_equal(xc @ (-rcodes).T, Tr)
