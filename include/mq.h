@@ -1,0 +1,212 @@
+/*
+ * mq.h -- C ABI of libmq: MosaicQuant's fused W4A4 + sparse-residual linear
+ * layer for AMD Instinct MI355X (gfx950).
+ *
+ * The layer (arXiv 2606.15652, Section 3 Eq. (4), Alg. 1 last step) is
+ *
+ *     Y = dequant(Xq Wq^T) + dequant(Xq (M_S (.) Rq)^T)
+ *
+ * with a dense 4-bit base weight Wq (one fp16 scale per output row per
+ * 128-long group along K), a 4-bit residual Rq present only on a selected set
+ * S of 128x128 weight blocks (one fp16 scale per row inside each block), and
+ * per-token 4-bit activations Xq (one fp16 scale per row).  Both weight terms
+ * are consumed by one kernel; residual MACs run inside the dense K-loop.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers are DEVICE pointers owned by the caller unless stated; the
+ *   library keeps no pointer after a call returns and allocates nothing.
+ * - Calls are asynchronous on `stream` (0 = the null stream).  On error
+ *   nothing is launched and an mq_status < 0 is returned; no call throws.
+ * - fp16 arrays are IEEE binary16 passed as `void*` / `const void*`.
+ * - Shapes: K and N are multiples of 128 with 128 <= K <= 2^20 and
+ *   128 <= N <= 2^24; 0 <= M <= 2^24 (M == 0 is a no-op).
+ * - 4-bit codes are two's-complement nibbles in [-7, 7] (the quantisers never
+ *   produce -8; the GEMM accepts it).  Byte j of a packed row holds element 2j
+ *   in its low nibble and element 2j+1 in its high nibble.
+ * - Packed operand pointers (Xq, Wq, Rq) must be 16-byte aligned; fp16
+ *   pointers 2-byte aligned; int32 pointers 4-byte aligned; fp32/fp64 arrays
+ *   naturally aligned.  Violations return MQ_ERR_MISALIGNED.
+ * - Inputs must be finite.  Outputs must not alias inputs.
+ * - Thread safety: every call may be made concurrently from several host
+ *   threads; the only global state is a read-only per-device property cache.
+ */
+#ifndef MQ_H
+#define MQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum mq_status {
+    MQ_OK = 0,
+    MQ_ERR_INVALID_ARG = -1,       /* null pointer, negative size, bad budget  */
+    MQ_ERR_UNSUPPORTED_SHAPE = -2, /* K or N not a positive multiple of 128,
+                                      leading dimension too small / unaligned  */
+    MQ_ERR_MISALIGNED = -3,        /* pointer alignment rule violated          */
+    MQ_ERR_WORKSPACE = -4,         /* workspace smaller than required          */
+    MQ_ERR_HIP = -5                /* the HIP runtime reported a launch error  */
+} mq_status;
+
+/* Kernel family selection (testing and A/B timing).  AUTO picks by M. */
+typedef enum mq_variant {
+    MQ_VARIANT_AUTO = 0,
+    MQ_VARIANT_SKINNY = 1,   /* decode: split-K over the waves of a workgroup  */
+    MQ_VARIANT_TILED = 2     /* prefill: M x N output tiles, K-loop of groups   */
+} mq_variant;
+
+/* Static string naming a status code.  Never NULL. */
+const char* mq_status_string(mq_status s);
+
+/* Library ABI version (major * 100 + minor). */
+int mq_version(void);
+
+/* ======================================================================== */
+/* Hot path                                                                  */
+/* ======================================================================== */
+
+/*
+ * Per-token symmetric INT4 activation quantisation (Section 2, Eq. (1), one
+ * scale per token; fused with nibble packing as in Section 4.2 "Kernel
+ * Fusion"):
+ *     a = max_k |X[m,k]|,  s_x[m] = fp16_rn(fp32(a) / 7),
+ *     Xq[m,k] = clamp(round_half_even(X[m,k] / s_x[m]), -7, 7)  (0 if s == 0)
+ *   X   : fp16 [M, ldx] row-major, ldx >= K, ldx % 8 == 0, 16-byte aligned.
+ *   Xq  : out, uint8 [M, K/2] packed nibbles.
+ *   s_x : out, fp16 [M].
+ */
+mq_status mq_quantize_act(const void* X, int M, int K, int ldx,
+                          uint8_t* Xq, void* s_x, hipStream_t stream);
+
+/* Bytes of workspace mq_fused_gemm needs for this shape (0: none). */
+size_t mq_fused_gemm_workspace_size(int M, int N, int K);
+
+/*
+ * Fused dense + sparse-residual W4A4 GEMM (Section 3 Eq. (4) with Eq. (2)'s
+ * scale factorisation per group; Section 4.2 "Kernel Fusion" and
+ * "Overlapped pipeline"):
+ *     A_b[m,n,g] = sum_{k in g} Xq[m,k] Wq[n,k]
+ *     A_r[m,n,g] = sum_{k in g} Xq[m,k] Rq[p][n%128][k%128]   if (n/128,g) in S
+ *     Y[m,n] = fp16( s_x[m] * sum_g ( s_w[n,g] A_b + s_r[p][n%128] A_r ) )
+ *   Xq, s_x          : uint8 [M, K/2], fp16 [M]            (from mq_quantize_act)
+ *   Wq, s_w          : uint8 [N, K/2], fp16 [N, K/128]
+ *   res_rowptr       : int32 [N/128 + 1], CSR over 128-row block rows;
+ *                      res_rowptr[0] == 0, res_rowptr[N/128] == nnzb.
+ *   res_kb           : int32 [nnzb], block column (group) of each selected
+ *                      block, strictly ascending within a block row.
+ *   Rq, s_r          : uint8 [nnzb, 128, 64], fp16 [nnzb, 128]; block p holds
+ *                      rows n = 128*nb + r, columns k = 128*res_kb[p] + c.
+ *   nnzb == 0        : res_kb, Rq, s_r (and res_rowptr) may be NULL.
+ *   Y, ldy           : out, fp16 [M, ldy], ldy >= N, ldy % 8 == 0.
+ *   workspace        : >= mq_fused_gemm_workspace_size(M, N, K) bytes (may be
+ *                      NULL when that is 0).
+ * The CSR's contents are trusted (checked only by the test-suite): a kb
+ * outside [0, K/128) or an unsorted row gives undefined results.
+ */
+mq_status mq_fused_gemm(int M, int N, int K,
+                        const uint8_t* Xq, const void* s_x,
+                        const uint8_t* Wq, const void* s_w,
+                        const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                        const uint8_t* Rq, const void* s_r,
+                        void* Y, int ldy,
+                        void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* mq_fused_gemm with an explicit kernel family. */
+mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int K,
+                                const uint8_t* Xq, const void* s_x,
+                                const uint8_t* Wq, const void* s_w,
+                                const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                                const uint8_t* Rq, const void* s_r,
+                                void* Y, int ldy,
+                                void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Same main loop, raw integer epilogue (for bit-exact testing):
+ *     Tb[m,n] = sum_g A_b[m,n,g],   Tr[m,n] = sum_g A_r[m,n,g]
+ *   Tb, Tr : out, int32 [M, N] row-major.  Exact: |Tb|, |Tr| <= 64 K < 2^31
+ *            for every supported K.
+ */
+mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int K,
+                                const uint8_t* Xq,
+                                const uint8_t* Wq,
+                                const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                                const uint8_t* Rq,
+                                int32_t* Tb, int32_t* Tr, hipStream_t stream);
+
+/* ======================================================================== */
+/* Offline weight preparation (not on the timed path)                        */
+/* ======================================================================== */
+
+/*
+ * Dense 4-bit base and residual-norm block scores (Section 2 Eq. (1) per
+ * (row, 128-group); residual R = W - Q(W) of Section 3 Eq. (4); block
+ * criterion ||R_B||_F^2 of Section 3, Observation 2):
+ *     s_w[n,g] = fp16_rn(fp32(max_{k in g} |W[n,k]|) / 7),
+ *     Wq[n,k]  = clamp(round_half_even(W[n,k] / s_w[n,g]), -7, 7),
+ *     R[n,k]   = W[n,k] - s_w[n,g] Wq[n,k]                    (fp32),
+ *     score[nb,kb] = sum over the 128x128 block of R^2         (fp64).
+ *   W     : fp32 [N, ldw], ldw >= K, ldw % 4 == 0, 16-byte aligned.
+ *   Wq    : out, uint8 [N, K/2];  s_w : out, fp16 [N, K/128].
+ *   score : out, fp64 [N/128, K/128] (may be NULL to skip scoring).
+ */
+mq_status mq_quantize_weight(const float* W, int N, int K, int ldw,
+                             uint8_t* Wq, void* s_w, double* score,
+                             hipStream_t stream);
+
+/*
+ * Diagonal Hessian estimate h_j = (2/T) sum_t X[t,j]^2 from T calibration
+ * tokens (Alg. 1, second step; Section 4.1).
+ *   X : fp16 [T, ldx];  h : out, fp64 [K].
+ */
+mq_status mq_hessian_diag(const void* X, int T, int K, int ldx, double* h,
+                          hipStream_t stream);
+
+/*
+ * Delta-Hessian block score (Alg. 1; Section 4.1):
+ *     S_B = [ sum_B h_j R_ij^2 - sum_B h_j (R_ij - Q(R)_ij)^2 ]_+
+ * with Q(R) the block's 4-bit residual (one scale per block row, as
+ * mq_quantize_residual produces it) and R rebuilt from W, s_w and Wq.
+ *   score : out, fp64 [N/128, K/128].
+ */
+mq_status mq_block_scores_dhessian(const float* W, int N, int K, int ldw,
+                                   const uint8_t* Wq, const void* s_w,
+                                   const double* h, double* score,
+                                   hipStream_t stream);
+
+/*
+ * Top-K block selection and block mask in CSR form (Alg. 1, TopK and mask
+ * steps): the nnzb blocks with the largest score are selected, ties broken by
+ * the lower linear index nb * KB + kb.
+ *   score      : fp64 [NB, KB]  (NB = N/128, KB = K/128), finite.
+ *   res_rowptr : out, int32 [NB + 1];  res_kb : out, int32 [nnzb].
+ * Requires 0 <= nnzb <= NB * KB.
+ */
+mq_status mq_select_blocks(const double* score, int NB, int KB, int nnzb,
+                           int32_t* res_rowptr, int32_t* res_kb,
+                           hipStream_t stream);
+
+/*
+ * Sparse 4-bit residual on the selected blocks (Section 3 Eq. (4); Alg. 1
+ * last step), one fp16 scale per row inside each block (Eq. (1)):
+ *     R = W - s_w Wq;  s_r[p][r] = fp16_rn(fp32(max_c |R|) / 7);
+ *     Rq[p][r][c] = clamp(round_half_even(R / s_r), -7, 7)
+ *   W, Wq, s_w : as for mq_quantize_weight (same W).
+ *   CSR        : as for mq_fused_gemm.
+ *   Rq, s_r    : out, uint8 [nnzb, 128, 64], fp16 [nnzb, 128].
+ */
+mq_status mq_quantize_residual(const float* W, int N, int K, int ldw,
+                               const uint8_t* Wq, const void* s_w,
+                               const int32_t* res_rowptr, const int32_t* res_kb,
+                               int nnzb, uint8_t* Rq, void* s_r,
+                               hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MQ_H */

@@ -46,6 +46,7 @@ def lib() -> C.CDLL:
         P = C.c_void_p
         i, i64 = C.c_int, C.c_int64
         sig = {
+            "orc_num_threads": (i, []),
             "orc_f32_to_f16": (C.c_uint16, [C.c_float]),
             "orc_f16_to_f32": (C.c_float, [C.c_uint16]),
             "orc_f32_to_f16_array": (None, [P, P, i64]),
@@ -73,6 +74,10 @@ def _p(a: Optional[np.ndarray]):
         return None
     assert a.flags["C_CONTIGUOUS"], "oracle expects C-contiguous arrays"
     return a.ctypes.data
+
+
+def num_threads() -> int:
+    return int(lib().orc_num_threads())
 
 
 # ---------------------------------------------------------------- fp16 ----

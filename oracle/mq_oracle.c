@@ -37,11 +37,15 @@
  * Build: gcc -O3 -fno-fast-math -ffp-contract=off -fopenmp -shared -fPIC.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
 
 #define ORC_BLOCK 128   /* group length along K == residual block edge */
+
+/* Threads the parallel loops below use (for reporting CPU timings). */
+int orc_num_threads(void) { return omp_get_max_threads(); }
 #define ORC_QMAX 7
 
 /* ------------------------------------------------------------------------ */

@@ -1,0 +1,263 @@
+"""Python binding of libmq (MosaicQuant fused W4A4 + sparse-residual GEMM on
+MI355X / gfx950).
+
+Argument marshalling only: every function checks tensor dtypes, devices and
+layouts, then calls the C ABI declared in ``include/mq.h`` with raw device
+pointers and the current torch stream.  All arithmetic runs in libmq's HIP
+kernels; there is no fallback.  Importing the package does not load the
+library; the first call does, and raises if ``libmq.so`` has not been built
+(``python -m paper_2606_15652_amd.build``) or no GPU is visible.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmq.so")
+
+MQ_OK = 0
+VARIANTS = {"auto": 0, "skinny": 1, "tiled": 2}
+BLOCK = 128
+
+_P = C.c_void_p
+_I = C.c_int
+_SIG = {
+    "mq_status_string": (C.c_char_p, [_I]),
+    "mq_version": (_I, []),
+    "mq_quantize_act": (_I, [_P, _I, _I, _I, _P, _P, _P]),
+    "mq_fused_gemm_workspace_size": (C.c_size_t, [_I, _I, _I]),
+    "mq_fused_gemm": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P,
+                          C.c_size_t, _P]),
+    "mq_fused_gemm_variant": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I,
+                                  _P, C.c_size_t, _P]),
+    "mq_fused_gemm_acc_i32": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _P, _P]),
+    "mq_quantize_weight": (_I, [_P, _I, _I, _I, _P, _P, _P, _P]),
+    "mq_hessian_diag": (_I, [_P, _I, _I, _I, _P, _P]),
+    "mq_block_scores_dhessian": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P]),
+    "mq_select_blocks": (_I, [_P, _I, _I, _I, _P, _P, _P]),
+    "mq_quantize_residual": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _P]),
+}
+
+_lib: Optional[C.CDLL] = None
+
+
+class MQError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        msg = load().mq_status_string(status).decode()
+        super().__init__(f"{fn} failed with status {status}: {msg}")
+        self.status = status
+
+
+def load(path: str = LIB_PATH) -> C.CDLL:
+    """Load libmq.so (once) and declare its signatures."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise ImportError(f"libmq.so not found at {path}; build it with "
+                              "`python -m paper_2606_15652_amd.build` (hipcc, gfx950)")
+        lib = C.CDLL(path)
+        for name, (res, args) in _SIG.items():
+            f = getattr(lib, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = lib
+    return _lib
+
+
+# ------------------------------------------------------------------ utils --
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream=None):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _need(t, dtype, name, ndim=None):
+    torch = _torch()
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must be {ndim}-D, got shape {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _check(fn, status):
+    if status != MQ_OK:
+        raise MQError(fn, status)
+
+
+# -------------------------------------------------------------- hot path --
+def quantize_act(X, out=None, stream=None):
+    """Per-token INT4 quantisation of fp16 X [M, K] -> (Xq uint8 [M, K/2], s_x fp16 [M])."""
+    torch = _torch()
+    _need(X, torch.float16, "X", 2)
+    M, K = X.shape
+    if out is None:
+        Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+        s_x = torch.empty((M,), dtype=torch.float16, device=X.device)
+    else:
+        Xq, s_x = out
+    _check("mq_quantize_act", load().mq_quantize_act(_ptr(X), M, K, X.stride(0), _ptr(Xq),
+                                                     _ptr(s_x), _stream(stream)))
+    return Xq, s_x
+
+
+@dataclass
+class PackedWeight:
+    """Device-resident operands of one MosaicQuant linear layer (canonical layouts)."""
+    N: int
+    K: int
+    Wq: "object"          # uint8 [N, K/2]
+    s_w: "object"         # fp16 [N, K/128]
+    rowptr: "object"      # int32 [N/128 + 1]
+    kb: "object"          # int32 [nnzb] (may be empty)
+    Rq: "object"          # uint8 [nnzb, 128, 64]
+    s_r: "object"         # fp16 [nnzb, 128]
+    score: "object" = None
+
+    @property
+    def nnzb(self) -> int:
+        return int(self.kb.numel())
+
+    @property
+    def nbytes(self) -> int:
+        return sum(t.numel() * t.element_size() for t in
+                   (self.Wq, self.s_w, self.rowptr, self.kb, self.Rq, self.s_r))
+
+
+def _res_ptrs(pw: PackedWeight):
+    if pw.nnzb == 0:
+        return None, None, None, None
+    return _ptr(pw.rowptr), _ptr(pw.kb), _ptr(pw.Rq), _ptr(pw.s_r)
+
+
+def fused_gemm(Xq, s_x, pw: PackedWeight, out=None, variant: str = "auto", stream=None):
+    """Y fp16 [M, N] = s_x * (Xq Wq^T scaled per group + sparse residual term)."""
+    torch = _torch()
+    _need(Xq, torch.uint8, "Xq", 2)
+    _need(s_x, torch.float16, "s_x", 1)
+    M = Xq.shape[0]
+    if Xq.shape[1] * 2 != pw.K or s_x.shape[0] != M:
+        raise ValueError("Xq / s_x shapes do not match the weight")
+    Y = out if out is not None else torch.empty((M, pw.N), dtype=torch.float16, device=Xq.device)
+    if out is not None:
+        _need(Y, torch.float16, "out", 2)
+    rp, kb, rq, sr = _res_ptrs(pw)
+    lib = load()
+    ws = lib.mq_fused_gemm_workspace_size(M, pw.N, pw.K)
+    wbuf = torch.empty(ws, dtype=torch.uint8, device=Xq.device) if ws else None
+    _check("mq_fused_gemm", lib.mq_fused_gemm_variant(
+        VARIANTS[variant], M, pw.N, pw.K, _ptr(Xq), _ptr(s_x), _ptr(pw.Wq), _ptr(pw.s_w),
+        rp, kb, pw.nnzb, rq, sr, _ptr(Y), Y.stride(0), _ptr(wbuf), ws, _stream(stream)))
+    return Y
+
+
+def fused_gemm_acc_i32(Xq, pw: PackedWeight, variant: str = "auto", stream=None):
+    """Raw exact integer sums (Tb, Tr) int32 [M, N] of the same main loop."""
+    torch = _torch()
+    _need(Xq, torch.uint8, "Xq", 2)
+    M = Xq.shape[0]
+    Tb = torch.empty((M, pw.N), dtype=torch.int32, device=Xq.device)
+    Tr = torch.empty((M, pw.N), dtype=torch.int32, device=Xq.device)
+    rp, kb, rq, _ = _res_ptrs(pw)
+    _check("mq_fused_gemm_acc_i32", load().mq_fused_gemm_acc_i32(
+        VARIANTS[variant], M, pw.N, pw.K, _ptr(Xq), _ptr(pw.Wq), rp, kb, pw.nnzb, rq,
+        _ptr(Tb), _ptr(Tr), _stream(stream)))
+    return Tb, Tr
+
+
+def linear(X, pw: PackedWeight, variant: str = "auto", stream=None):
+    """The whole hot path: quantise fp16 X [M, K] then the fused GEMM."""
+    Xq, s_x = quantize_act(X, stream=stream)
+    return fused_gemm(Xq, s_x, pw, variant=variant, stream=stream)
+
+
+# --------------------------------------------------- weight preparation --
+def quantize_weight(W, with_score: bool = True, stream=None):
+    """fp32 W [N, K] -> (Wq uint8 [N, K/2], s_w fp16 [N, K/128], score fp64 [N/128, K/128])."""
+    torch = _torch()
+    _need(W, torch.float32, "W", 2)
+    N, K = W.shape
+    Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=W.device)
+    s_w = torch.empty((N, K // BLOCK), dtype=torch.float16, device=W.device)
+    score = torch.empty((N // BLOCK, K // BLOCK), dtype=torch.float64, device=W.device) if with_score else None
+    _check("mq_quantize_weight", load().mq_quantize_weight(
+        _ptr(W), N, K, W.stride(0), _ptr(Wq), _ptr(s_w), _ptr(score), _stream(stream)))
+    return Wq, s_w, score
+
+
+def hessian_diag(X, stream=None):
+    torch = _torch()
+    _need(X, torch.float16, "X", 2)
+    T, K = X.shape
+    h = torch.empty((K,), dtype=torch.float64, device=X.device)
+    _check("mq_hessian_diag", load().mq_hessian_diag(_ptr(X), T, K, X.stride(0), _ptr(h),
+                                                     _stream(stream)))
+    return h
+
+
+def block_scores_dhessian(W, Wq, s_w, h, stream=None):
+    torch = _torch()
+    _need(W, torch.float32, "W", 2)
+    N, K = W.shape
+    score = torch.empty((N // BLOCK, K // BLOCK), dtype=torch.float64, device=W.device)
+    _check("mq_block_scores_dhessian", load().mq_block_scores_dhessian(
+        _ptr(W), N, K, W.stride(0), _ptr(Wq), _ptr(s_w), _ptr(h), _ptr(score), _stream(stream)))
+    return score
+
+
+def select_blocks(score, nnzb: int, stream=None):
+    """Top-nnzb blocks of fp64 score [NB, KB] -> (rowptr int32 [NB+1], kb int32 [nnzb])."""
+    torch = _torch()
+    _need(score, torch.float64, "score", 2)
+    NB, KB = score.shape
+    rowptr = torch.empty((NB + 1,), dtype=torch.int32, device=score.device)
+    kb = torch.empty((max(nnzb, 1),), dtype=torch.int32, device=score.device)
+    _check("mq_select_blocks", load().mq_select_blocks(_ptr(score), NB, KB, nnzb, _ptr(rowptr),
+                                                       _ptr(kb), _stream(stream)))
+    return rowptr, kb[:nnzb]
+
+
+def quantize_residual(W, Wq, s_w, rowptr, kb, stream=None):
+    torch = _torch()
+    _need(W, torch.float32, "W", 2)
+    N, K = W.shape
+    nnzb = int(kb.numel())
+    Rq = torch.empty((max(nnzb, 1), BLOCK, BLOCK // 2), dtype=torch.uint8, device=W.device)
+    s_r = torch.empty((max(nnzb, 1), BLOCK), dtype=torch.float16, device=W.device)
+    _check("mq_quantize_residual", load().mq_quantize_residual(
+        _ptr(W), N, K, W.stride(0), _ptr(Wq), _ptr(s_w), _ptr(rowptr),
+        _ptr(kb) if nnzb else None, nnzb, _ptr(Rq), _ptr(s_r), _stream(stream)))
+    return Rq[:nnzb], s_r[:nnzb]
+
+
+def prepare_weight(W, nnzb: int, criterion: str = "frob", X_calib=None, stream=None) -> PackedWeight:
+    """Offline MosaicQuant packing of fp32 W [N, K] on the GPU (Alg. 1):
+    base INT4, block scores, top-nnzb selection, residual INT4."""
+    Wq, s_w, score = quantize_weight(W, with_score=(criterion == "frob"), stream=stream)
+    if criterion == "dhessian":
+        if X_calib is None:
+            raise ValueError("dhessian selection needs calibration activations")
+        score = block_scores_dhessian(W, Wq, s_w, hessian_diag(X_calib, stream), stream)
+    elif criterion != "frob":
+        raise ValueError(criterion)
+    rowptr, kb = select_blocks(score, nnzb, stream)
+    Rq, s_r = quantize_residual(W, Wq, s_w, rowptr, kb, stream)
+    N, K = W.shape
+    return PackedWeight(N, K, Wq, s_w, rowptr, kb, Rq, s_r, score)

@@ -1,0 +1,104 @@
+"""The C-ABI library without a GPU: it loads, exports every symbol declared in
+include/mq.h, and its argument validation returns the documented status codes
+before anything is launched.  Every call below either fails validation or is
+an empty (M == 0 / nnzb == 0) no-op, so the fake pointers are never used."""
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mq.h")
+
+OK, INVALID, SHAPE, MISALIGNED, WORKSPACE = 0, -1, -2, -3, -4
+A = 0x10000          # a 16-byte aligned fake device address (never touched)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mq_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2606_15652_amd as mq
+    if not os.path.exists(mq.LIB_PATH):
+        from paper_2606_15652_amd import build
+        build.build()
+    return mq.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), f"libmq.so does not export {n}"
+
+
+def test_status_strings(lib):
+    for s in (OK, INVALID, SHAPE, MISALIGNED, WORKSPACE, -5, -99):
+        assert lib.mq_status_string(s)
+    assert lib.mq_version() >= 100
+
+
+def test_quantize_act_validation(lib):
+    q = lib.mq_quantize_act
+    assert q(A, 0, 128, 128, A, A, None) == OK                 # empty input: no-op
+    assert q(A, -1, 128, 128, A, A, None) == INVALID
+    assert q(A, 4, 100, 128, A, A, None) == SHAPE               # K not a multiple of 128
+    assert q(A, 4, 256, 128, A, A, None) == SHAPE               # ldx < K
+    assert q(A, 4, 128, 132, A, A, None) == SHAPE               # ldx % 8
+    assert q(None, 4, 128, 128, A, A, None) == INVALID
+    assert q(A + 2, 4, 128, 128, A, A, None) == MISALIGNED
+    assert q(A, 4, 128, 128, A + 8, A, None) == MISALIGNED
+    assert q(A, 4, 128, 128, A, A + 1, None) == MISALIGNED
+
+
+def _gemm(lib, M=4, N=256, K=256, Xq=A, sx=A, Wq=A, sw=A, rp=A, kb=A, nnzb=1, Rq=A, sr=A,
+          Y=A, ldy=None, ws=None, ws_bytes=0, variant=0):
+    return lib.mq_fused_gemm_variant(variant, M, N, K, Xq, sx, Wq, sw, rp, kb, nnzb, Rq, sr, Y,
+                                     N if ldy is None else ldy, ws, ws_bytes, None)
+
+
+def test_fused_gemm_validation(lib):
+    assert _gemm(lib, M=0) == OK
+    assert _gemm(lib, M=-1) == INVALID
+    assert _gemm(lib, N=200) == SHAPE
+    assert _gemm(lib, K=64) == SHAPE
+    assert _gemm(lib, K=1 << 21) == SHAPE
+    assert _gemm(lib, ldy=128) == SHAPE
+    assert _gemm(lib, ldy=260) == SHAPE
+    assert _gemm(lib, nnzb=5) == INVALID                       # > NB * KB = 4
+    assert _gemm(lib, nnzb=-1) == INVALID
+    assert _gemm(lib, Rq=None) == INVALID                      # residual pointers required
+    assert _gemm(lib, Xq=None) == INVALID
+    assert _gemm(lib, Y=None) == INVALID
+    assert _gemm(lib, Wq=A + 4) == MISALIGNED
+    assert _gemm(lib, Rq=A + 8) == MISALIGNED
+    assert _gemm(lib, kb=A + 2) == MISALIGNED
+    assert _gemm(lib, sx=A + 1) == MISALIGNED
+    assert _gemm(lib, variant=7) == INVALID
+    assert lib.mq_fused_gemm_workspace_size(4, 256, 256) == 0
+
+
+def test_acc_i32_validation(lib):
+    f = lib.mq_fused_gemm_acc_i32
+    assert f(0, 0, 256, 256, A, A, A, A, 1, A, A, A, None) == OK
+    assert f(0, 4, 256, 256, A, A, A, A, 1, A, None, A, None) == INVALID
+    assert f(0, 4, 256, 256, A, A, A, A, 1, A, A + 2, A, None) == MISALIGNED
+    assert f(3, 4, 256, 256, A, A, A, A, 1, A, A, A, None) == INVALID
+
+
+def test_weight_prep_validation(lib):
+    assert lib.mq_quantize_weight(A, 256, 200, 256, A, A, A, None) == SHAPE
+    assert lib.mq_quantize_weight(A, 256, 256, 255, A, A, A, None) == SHAPE
+    assert lib.mq_quantize_weight(A + 4, 256, 256, 256, A, A, A, None) == MISALIGNED
+    assert lib.mq_quantize_weight(A, 256, 256, 256, A, A, A + 4, None) == MISALIGNED
+    assert lib.mq_select_blocks(A, 2, 2, 5, A, A, None) == INVALID
+    assert lib.mq_select_blocks(A, 2, 2, -1, A, A, None) == INVALID
+    assert lib.mq_select_blocks(A, 2, 2, 1, A, None, None) == INVALID
+    assert lib.mq_quantize_residual(A, 256, 256, 256, A, A, A, A, 9, A, A, None) == INVALID
+    assert lib.mq_quantize_residual(A, 256, 256, 256, A, A, A, A, 0, None, None, None) == OK
+    assert lib.mq_hessian_diag(A, 0, 128, 128, A, None) == INVALID
+    assert lib.mq_block_scores_dhessian(A, 256, 256, 256, A, A, None, A, None) == INVALID

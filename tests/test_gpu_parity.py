@@ -1,0 +1,398 @@
+"""GPU parity: libmq's HIP kernels (through the C ABI) against the CPU oracle.
+
+Bars: integer and byte outputs (codes, packed nibbles, fp16 scale bits, CSR,
+raw int32 accumulators) bit-exact; fp16 outputs within max-abs-rel 2e-3 of the
+oracle's fp64 epilogue (norm-relative: max|dY| / max|Y64|).  The fp16
+rounding of the output alone contributes up to 2^-11 ~ 4.9e-4, and the fp32
+group accumulation a few 2^-24 per group, so the tests also check a tighter
+1e-3.  Block scores are fp64 sums taken in a different order on the two sides
+and are compared to 1e-12 relative; the selected sets must then coincide
+exactly (a tie closer than that at the budget boundary would be reported).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+B = 128
+TOL = 2e-3
+TIGHT = 1e-3
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    sys.__stderr__.write(f"\n[gpu-case] {request.node.nodeid}\n")
+    sys.__stderr__.flush()
+    yield
+
+
+@pytest.fixture(scope="module")
+def tc():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def mq(tc):
+    import paper_2606_15652_amd as m
+    m.load()
+    return m
+
+
+def dev(tc, a):
+    return tc.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    return t.cpu().numpy()
+
+
+def half_bits(t):
+    import torch
+    return t.cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def maxabsrel(Y, Y64):
+    Yf = Y.float().cpu().numpy().astype(np.float64)
+    den = np.abs(Y64).max()
+    return float(np.abs(Yf - Y64).max() / den) if den > 0 else float(np.abs(Yf).max())
+
+
+# ------------------------------------------------------------------ data ----
+def random_csr(NB, KB, nnzb, rng):
+    sel = np.zeros(NB * KB, bool)
+    sel[rng.choice(NB * KB, size=nnzb, replace=False)] = True
+    sel = sel.reshape(NB, KB)
+    rowptr = np.zeros(NB + 1, np.int32)
+    rowptr[1:] = np.cumsum(sel.sum(1))
+    kb = np.concatenate([np.flatnonzero(r) for r in sel]).astype(np.int32) if nnzb else np.zeros(0, np.int32)
+    return rowptr, kb, sel
+
+
+def random_operands(M, N, K, nnzb, seed):
+    """Uniform random packed operands: every nibble value, -8 included."""
+    rng = np.random.default_rng(seed)
+    NB, KB = N // B, K // B
+    Xq = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
+    s_x = rng.uniform(0.01, 2.0, M).astype(np.float16).view(np.uint16)
+    Wq = rng.integers(0, 256, (N, K // 2), dtype=np.uint8)
+    s_w = rng.uniform(1e-3, 0.05, (N, KB)).astype(np.float16).view(np.uint16)
+    rowptr, kb, sel = random_csr(NB, KB, nnzb, rng)
+    Rq = rng.integers(0, 256, (nnzb, B, B // 2), dtype=np.uint8)
+    s_r = rng.uniform(1e-4, 5e-3, (nnzb, B)).astype(np.float16).view(np.uint16)
+    return Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r
+
+
+def orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r):
+    return orc.PackedWeight(N, K, Wq, s_w, rowptr, kb, Rq, s_r, None, sel)
+
+
+def gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r):
+    import torch
+    return mq.PackedWeight(N, K, dev(tc, Wq), dev(tc, s_w).view(torch.float16),
+                           dev(tc, rowptr), dev(tc, kb),
+                           dev(tc, Rq), dev(tc, s_r).view(torch.float16))
+
+
+# ------------------------------------------------------- activation quant --
+ACT_CASES = [(1, 128), (3, 1024), (64, 4096), (257, 384), (5, 28672), (2, 40960), (33, 2048)]
+
+
+@pytest.mark.parametrize("M,K", ACT_CASES)
+def test_act_quant_parity(tc, mq, orc, M, K):
+    rng = np.random.default_rng(M * 7919 + K)
+    X = synth.gen_act(M, K, 1000 + M + K)
+    if M > 2:
+        X[1] = (rng.standard_normal(K) * 3).astype(np.float16)      # dense codes
+        X[2] = 0                                                    # zero row
+    if M > 4:
+        X[3, :8] = np.array([0.875, -0.4375, 0.3125, 0.1875, -0.0625, 0.0625, -0.3125, 0.4375])
+        X[3, 8:] = 0                                                # exact ties (golden)
+        X[4] = (rng.standard_normal(K) * 1e-6).astype(np.float16)   # subnormal halves
+    if M > 5:
+        X[5, K // 2] = 65504                                        # largest finite half
+    Xq, s_x = mq.quantize_act(dev(tc, X))
+    Xq_ref, sx_ref = orc.quantize_act(X)
+    assert np.array_equal(half_bits(s_x), sx_ref)
+    assert np.array_equal(host(Xq), Xq_ref)
+
+
+def test_act_quant_strided(tc, mq, orc):
+    X = synth.gen_act(9, 640, 5)
+    Xbig = np.zeros((9, 1024), np.float16)
+    Xbig[:, :640] = X
+    Xd = dev(tc, Xbig)[:, :640]
+    Xq = tc.empty((9, 320), dtype=tc.uint8, device="cuda")
+    s_x = tc.empty((9,), dtype=tc.float16, device="cuda")
+    lib = mq.load()
+    st = lib.mq_quantize_act(Xd.data_ptr(), 9, 640, 1024, Xq.data_ptr(), s_x.data_ptr(), None)
+    tc.cuda.synchronize()
+    assert st == 0
+    Xq_ref, sx_ref = orc.quantize_act(X)
+    assert np.array_equal(host(Xq), Xq_ref) and np.array_equal(half_bits(s_x), sx_ref)
+
+
+# ------------------------------------------------------- weight prep -------
+PREP_CASES = [("c1", 1024, 1024, 6, False), ("tall", 2048, 256, 7, False),
+              ("wide", 256, 3072, 10, False), ("skew", 2048, 1024, 13, True),
+              ("dense100", 384, 512, 12, False), ("none", 512, 384, 0, False)]
+
+
+def check_prep(tc, mq, orc, W, nnzb, criterion="frob", Xc=None):
+    pw = mq.prepare_weight(dev(tc, W), nnzb, criterion=criterion,
+                           X_calib=None if Xc is None else dev(tc, Xc))
+    ref = orc.prepare_weight(W, nnzb, criterion=criterion, X_calib=Xc)
+    tc.cuda.synchronize()
+    assert np.array_equal(host(pw.Wq), ref.Wq)
+    assert np.array_equal(half_bits(pw.s_w), ref.s_w)
+    sc = host(pw.score)
+    assert np.allclose(sc, ref.score, rtol=1e-12, atol=1e-300)
+    # selection: exact unless two scores closer than the comparison tolerance
+    # straddle the budget boundary
+    rp, kb = host(pw.rowptr), host(pw.kb)
+    if not (np.array_equal(rp, ref.rowptr) and np.array_equal(kb, ref.kb)):
+        order = np.sort(ref.score.ravel())[::-1]
+        gap = abs(order[nnzb - 1] - order[nnzb]) if 0 < nnzb < order.size else np.inf
+        pytest.fail(f"selected blocks differ (boundary gap {gap:.3e})")
+    assert np.array_equal(host(pw.Rq), ref.Rq)
+    assert np.array_equal(half_bits(pw.s_r), ref.s_r)
+    return pw, ref
+
+
+@pytest.mark.parametrize("name,N,K,nnzb,skew", PREP_CASES, ids=[c[0] for c in PREP_CASES])
+def test_weight_prep_parity(tc, mq, orc, name, N, K, nnzb, skew):
+    seed = 77 + N + K
+    des = synth.skew_blocks(N, K, nnzb, seed)[0] if skew else None
+    W = synth.gen_weight(N, K, seed, designated=des)
+    if name == "dense100":
+        nnzb = (N // B) * (K // B)
+    check_prep(tc, mq, orc, W, nnzb)
+
+
+def test_weight_prep_edge_values(tc, mq, orc):
+    N, K = 256, 384
+    W = synth.gen_weight(N, K, 3)
+    W[0, :128] = 0                        # all-zero group -> scale 0
+    W[1, 0] = 0.875; W[1, 1:128] = 0.4375  # ties against s = 0.125
+    W[2, 128:256] = 1e-9                  # scale underflows in fp16
+    W[3, 5] = 7.5                         # a large outlier
+    check_prep(tc, mq, orc, W, 3)
+
+
+def test_dhessian_prep_parity(tc, mq, orc):
+    N, K = 1024, 768
+    W = synth.gen_weight(N, K, 19)
+    rng = np.random.default_rng(2)
+    Xc = (rng.standard_normal((256, K)) * rng.uniform(0.1, 5, K)).astype(np.float16)
+    h = mq.hessian_diag(dev(tc, Xc))
+    assert np.array_equal(host(h), orc.hessian_diag(Xc))    # same sequential order
+    check_prep(tc, mq, orc, W, 20, criterion="dhessian", Xc=Xc)
+
+
+# ------------------------------------------------------------ GEMM ---------
+GEMM_CASES = [
+    (1, 128, 128, 1), (5, 384, 256, 3), (16, 1024, 1024, 6), (17, 256, 512, 5),
+    (32, 640, 384, 0), (33, 256, 256, 4), (64, 1024, 1024, 6), (100, 384, 640, 9),
+    (129, 512, 1024, 12), (256, 1024, 2048, 13), (70, 128, 4096, 32), (48, 2304, 256, 18),
+]
+
+
+def _variants(M):
+    return ["skinny", "tiled", "auto"] if M <= 32 else ["tiled", "auto"]
+
+
+@pytest.mark.parametrize("M,N,K,nnzb", GEMM_CASES, ids=[f"M{c[0]}_N{c[1]}_K{c[2]}_r{c[3]}" for c in GEMM_CASES])
+def test_gemm_parity_random_codes(tc, mq, orc, M, N, K, nnzb):
+    ops = random_operands(M, N, K, nnzb, seed=M * 131 + N * 7 + K + nnzb)
+    Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = ops
+    Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    Xq_d, sx_d = dev(tc, Xq), dev(tc, s_x).view(tc.float16)
+    for v in _variants(M):
+        Tb, Tr = mq.fused_gemm_acc_i32(Xq_d, pw, variant=v)
+        Y = mq.fused_gemm(Xq_d, sx_d, pw, variant=v)
+        tc.cuda.synchronize()
+        assert np.array_equal(host(Tb), Tb_ref), f"{v}: Tb differs"
+        assert np.array_equal(host(Tr), Tr_ref), f"{v}: Tr differs"
+        err = maxabsrel(Y, Y64)
+        assert err <= TIGHT, f"{v}: max-abs-rel {err:.3e}"
+
+
+def test_gemm_quantized_layer_matches_oracle(tc, mq, orc):
+    """The whole hot path on a synthetic quantised layer (config-1 recipe)."""
+    L = synth.workload("c1_1024")
+    W, X = L.weight(), L.act(64)
+    ref = orc.prepare_weight(W, L.nnzb)
+    Xq_r, sx_r = orc.quantize_act(X)
+    Tb_ref, Tr_ref, Y64 = orc.linear(Xq_r, sx_r, ref)
+    pw = mq.prepare_weight(dev(tc, W), L.nnzb)
+    Y = mq.linear(dev(tc, X), pw)
+    Xq, s_x = mq.quantize_act(dev(tc, X))
+    for v in ("skinny", "tiled"):
+        Tb, Tr = mq.fused_gemm_acc_i32(Xq, pw, variant=v)
+        assert np.array_equal(host(Tb), Tb_ref) and np.array_equal(host(Tr), Tr_ref)
+    assert maxabsrel(Y, Y64) <= TIGHT
+
+
+def test_gemm_extreme_codes_long_k(tc, mq, orc):
+    """All codes -8 or +7 over K = 28672: accumulators at the int32-safe extreme."""
+    M, N, K = 20, 256, 28672
+    Xq = np.full((M, K // 2), 0x88, np.uint8)          # -8 everywhere
+    Xq[1::2] = 0x77                                    # +7
+    Wq = np.full((N, K // 2), 0x88, np.uint8)
+    Wq[::3] = 0x77
+    s_x = np.full(M, np.float16(1).view(np.uint16))
+    s_w = np.full((N, K // B), np.float16(2 ** -10).view(np.uint16))
+    NB, KB = N // B, K // B
+    rowptr = np.array([0, KB, KB], np.int32)           # every block of block row 0
+    kb = np.arange(KB, dtype=np.int32)
+    Rq = np.full((KB, B, B // 2), 0x88, np.uint8)
+    s_r = np.full((KB, B), np.float16(2 ** -12).view(np.uint16))
+    sel = np.zeros((NB, KB), bool)
+    sel[0] = True
+    Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+    assert np.abs(Tb_ref).max() == 64 * K
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    for v in ("skinny", "tiled"):
+        Tb, Tr = mq.fused_gemm_acc_i32(dev(tc, Xq), pw, variant=v)
+        Y = mq.fused_gemm(dev(tc, Xq), dev(tc, s_x).view(tc.float16), pw, variant=v)
+        tc.cuda.synchronize()
+        assert np.array_equal(host(Tb), Tb_ref) and np.array_equal(host(Tr), Tr_ref), v
+        assert maxabsrel(Y, Y64) <= TIGHT, v
+
+
+def test_gemm_guard_bands_and_empty(tc, mq, orc):
+    """No writes outside Y[:M, :N] (ldy > N, canary rows); M == 0 is a no-op."""
+    M, N, K, nnzb = 37, 384, 512, 4
+    ops = random_operands(M, N, K, nnzb, seed=5)
+    Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = ops
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    lib = mq.load()
+    for v in (1, 2):
+        if v == 1 and M > 32:
+            continue
+        canary = 12345
+        Yfull = tc.full((M + 4, N + 8), canary, dtype=tc.int16, device="cuda")
+        Yv = Yfull[2:2 + M]
+        st = lib.mq_fused_gemm_variant(v, M, N, K, dev(tc, Xq).data_ptr(),
+                                       dev(tc, s_x).data_ptr(), pw.Wq.data_ptr(), pw.s_w.data_ptr(),
+                                       pw.rowptr.data_ptr(), pw.kb.data_ptr(), nnzb, pw.Rq.data_ptr(),
+                                       pw.s_r.data_ptr(), Yv.data_ptr(), N + 8, None, 0, None)
+        tc.cuda.synchronize()
+        assert st == 0
+        h = host(Yfull)
+        assert np.all(h[:2] == canary) and np.all(h[2 + M:] == canary)
+        assert np.all(h[2:2 + M, N:] == canary)
+    Y = tc.full((1, N), 7, dtype=tc.int16, device="cuda")
+    st = lib.mq_fused_gemm(0, N, K, dev(tc, Xq).data_ptr(), dev(tc, s_x).data_ptr(),
+                           pw.Wq.data_ptr(), pw.s_w.data_ptr(), pw.rowptr.data_ptr(),
+                           pw.kb.data_ptr(), nnzb, pw.Rq.data_ptr(), pw.s_r.data_ptr(),
+                           Y.data_ptr(), N, None, 0, None)
+    tc.cuda.synchronize()
+    assert st == 0 and np.all(host(Y) == 7)
+
+
+def test_gemm_no_residual_null_pointers(tc, mq, orc):
+    M, N, K = 40, 256, 384
+    Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, 0, seed=9)
+    Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+    Y = tc.empty((M, N), dtype=tc.float16, device="cuda")
+    lib = mq.load()
+    for v in (1, 2):
+        st = lib.mq_fused_gemm_variant(v, M, N, K, dev(tc, Xq).data_ptr(), dev(tc, s_x).data_ptr(),
+                                       dev(tc, Wq).data_ptr(), dev(tc, s_w).data_ptr(), None, None, 0,
+                                       None, None, Y.data_ptr(), N, None, 0, None)
+        tc.cuda.synchronize()
+        assert st == 0
+        assert maxabsrel(Y, Y64) <= TIGHT
+        assert not Tr_ref.any()
+
+
+def test_gemm_deterministic_and_row_independent(tc, mq, orc):
+    M, N, K, nnzb = 48, 512, 1024, 6
+    Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=21)
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    Xd, sd = dev(tc, Xq), dev(tc, s_x).view(tc.float16)
+    for v in ("tiled", "skinny"):
+        rows = slice(0, M) if v == "tiled" else slice(0, 16)
+        Y1 = host(mq.fused_gemm(Xd[rows].contiguous(), sd[rows].contiguous(), pw, variant=v).view(tc.int16))
+        Y2 = host(mq.fused_gemm(Xd[rows].contiguous(), sd[rows].contiguous(), pw, variant=v).view(tc.int16))
+        assert np.array_equal(Y1, Y2)
+        for m in (0, 5, 15):
+            Ym = host(mq.fused_gemm(Xd[m:m + 1].contiguous(), sd[m:m + 1].contiguous(), pw,
+                                    variant=v).view(tc.int16))
+            assert np.array_equal(Ym[0], Y1[m]), (v, m)
+
+
+# ------------------------------------------------ full workload sizes ------
+_prep_cache = {}
+
+
+def _prepared(tc, mq, orc, layer):
+    key = (layer.K, layer.N, layer.seed, layer.nnzb)
+    if key not in _prep_cache:
+        _prep_cache.clear()
+        W = layer.weight()
+        ref = orc.prepare_weight(W, layer.nnzb)
+        pw = mq.prepare_weight(dev(tc, W), layer.nnzb)
+        tc.cuda.synchronize()
+        assert np.array_equal(host(pw.Wq), ref.Wq)
+        assert np.array_equal(half_bits(pw.s_w), ref.s_w)
+        assert np.array_equal(host(pw.rowptr), ref.rowptr) and np.array_equal(host(pw.kb), ref.kb)
+        assert np.array_equal(host(pw.Rq), ref.Rq) and np.array_equal(half_bits(pw.s_r), ref.s_r)
+        des = layer.designated()
+        if des is not None:
+            assert np.array_equal(ref.mask, des)
+        del W
+        _prep_cache[key] = (ref, pw)
+    return _prep_cache[key]
+
+
+def _samples(M, N, rowptr, rng, count=3000):
+    ms = list(rng.integers(0, M, count))
+    ns = list(rng.integers(0, N, count))
+    for m in {0, M - 1, min(M - 1, 63), min(M - 1, 64), M // 2}:
+        for n in {0, N - 1, 127, 128, min(N - 1, 255), min(N - 1, 256), N // 2}:
+            ms.append(m)
+            ns.append(n)
+    hot = np.flatnonzero(np.diff(rowptr) > 0)       # block rows that carry residual
+    for nb in hot[:8]:
+        for r in (0, 63, 127):
+            ms.append(int(rng.integers(0, M)))
+            ns.append(int(nb * B + r))
+    return np.array(ms, np.int32), np.array(ns, np.int32)
+
+
+FULL = [(L.name, M) for L in synth.workloads() for M in L.ms]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,M", FULL, ids=[f"{n}_M{m}" for n, m in FULL])
+def test_full_size_sampled(tc, mq, orc, name, M):
+    layer = synth.workload(name)
+    ref, pw = _prepared(tc, mq, orc, layer)
+    X = layer.act(M)
+    Xd = dev(tc, X)
+    Xq, s_x = mq.quantize_act(Xd)
+    Xq_ref, sx_ref = orc.quantize_act(X)
+    assert np.array_equal(host(Xq), Xq_ref) and np.array_equal(half_bits(s_x), sx_ref)
+    rng = np.random.default_rng(M + layer.seed)
+    ms, ns = _samples(M, layer.N, ref.rowptr, rng)
+    tb_ref, tr_ref, y64 = orc.linear_sampled(Xq_ref, sx_ref, ref, ms, ns)
+    Y = mq.fused_gemm(Xq, s_x, pw)                     # the launch bench.py times
+    Tb, Tr = mq.fused_gemm_acc_i32(Xq, pw)
+    mi, ni = tc.from_numpy(ms).long().cuda(), tc.from_numpy(ns).long().cuda()
+    tb, tr = host(Tb[mi, ni]), host(Tr[mi, ni])
+    y = Y[mi, ni].float().cpu().numpy().astype(np.float64)
+    assert np.array_equal(tb, tb_ref) and np.array_equal(tr, tr_ref)
+    # norm-relative bar over the sampled outputs
+    den = max(np.abs(y64).max(), 1e-30)
+    assert np.abs(y - y64).max() / den <= TIGHT
