@@ -26,6 +26,8 @@
 //    (deterministic).
 #include "mq_device.h"
 
+#include <type_traits>
+
 namespace mq {
 
 struct GemmArgs {
@@ -46,6 +48,45 @@ struct GemmArgs {
 
 // 1/256 removes the 16 x 16 factor of the nibble widening (exact).
 constexpr float kUnscale = 1.0f / 256.0f;
+
+// One m sub-tile row of one group: base MFMA pair + epilogue for each of the
+// WN column sub-tiles, then (HAS_RES) the residual MFMA pair + epilogue.  The
+// caller picks HAS_RES once per group, so this is straight-line code and every
+// MFMA result is converted inside the basic block that produced it (the
+// compiler's MFMA-to-VALU wait states are only placed reliably within a block).
+template <int WN, bool RAW, bool HAS_RES>
+__device__ __forceinline__ void group_row(const i32x4 alo, const i32x4 ahi,
+                                          const i32x4 (&wlo)[WN], const i32x4 (&whi)[WN],
+                                          const i32x4 (&rlo)[WN], const i32x4 (&rhi)[WN],
+                                          const float (&sw_f)[WN], const float (&sr_f)[WN],
+                                          f32x4 (&acc)[WN], i32x4 (&iacc)[WN], i32x4 (&racc)[WN]) {
+#pragma unroll
+    for (int j = 0; j < WN; ++j) {
+        i32x4 s = mfma_i8(alo, wlo[j], i32x4{0, 0, 0, 0});
+        s = mfma_i8(ahi, whi[j], s);
+        if constexpr (RAW) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) iacc[j][r] += s[r] >> 8;  // exact: s is 256 x the sum
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) acc[j][r] += sw_f[j] * (float)s[r];
+        }
+    }
+    if constexpr (HAS_RES) {
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+            i32x4 s = mfma_i8(alo, rlo[j], i32x4{0, 0, 0, 0});
+            s = mfma_i8(ahi, rhi[j], s);
+            if constexpr (RAW) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) racc[j][r] += s[r] >> 8;
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[j][r] += sr_f[j] * (float)s[r];
+            }
+        }
+    }
+}
 
 // --------------------------------------------------------------------------
 // Tiled kernel
@@ -171,6 +212,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_tiled_kernel(GemmArgs a) {
         float sw_f[WN], sr_f[WN];
         const int p = cur_p;
 #pragma unroll
+        for (int j = 0; j < WN; ++j) { rlo[j] = rhi[j] = i32x4{0, 0, 0, 0}; sw_f[j] = sr_f[j] = 0.f; }
+#pragma unroll
         for (int j = 0; j < WN; ++j) {
             unpack_nibbles(wpk[j], wlo[j], whi[j]);
             if constexpr (!RAW) sw_f[j] = half_bits_to_float(swb[j]) * kUnscale;
@@ -191,40 +234,20 @@ __global__ __launch_bounds__(64 * NW) void gemm_tiled_kernel(GemmArgs a) {
         }
         __syncthreads();
         if (active) {
+            auto tiles = [&](auto has_res) {
+                constexpr bool HR = decltype(has_res)::value;
 #pragma unroll
-            for (int i = 0; i < WM; ++i) {
-                const int row = i * 16 + lrow;
-                const int sw = row & 7;
-                const uint8_t* rb = &xs[buf][row * kRowBytes];
-                const i32x4 alo = *reinterpret_cast<const i32x4*>(rb + (((2 * lq) ^ sw) << 4));
-                const i32x4 ahi = *reinterpret_cast<const i32x4*>(rb + (((2 * lq + 1) ^ sw) << 4));
-#pragma unroll
-                for (int j = 0; j < WN; ++j) {
-                    i32x4 s = mfma_i8(alo, wlo[j], i32x4{0, 0, 0, 0});
-                    s = mfma_i8(ahi, whi[j], s);
-                    if constexpr (RAW) {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) iacc[i][j][r] += s[r] >> 8;  // exact
-                    } else {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) acc[i][j][r] += sw_f[j] * (float)s[r];
-                    }
+                for (int i = 0; i < WM; ++i) {
+                    const int row = i * 16 + lrow;
+                    const int sw = row & 7;
+                    const uint8_t* rb = &xs[buf][row * kRowBytes];
+                    const i32x4 alo = *reinterpret_cast<const i32x4*>(rb + (((2 * lq) ^ sw) << 4));
+                    const i32x4 ahi = *reinterpret_cast<const i32x4*>(rb + (((2 * lq + 1) ^ sw) << 4));
+                    group_row<WN, RAW, HR>(alo, ahi, wlo, whi, rlo, rhi, sw_f, sr_f, acc[i], iacc[i], racc[i]);
                 }
-                if (p >= 0) {
-#pragma unroll
-                    for (int j = 0; j < WN; ++j) {
-                        i32x4 s = mfma_i8(alo, rlo[j], i32x4{0, 0, 0, 0});
-                        s = mfma_i8(ahi, rhi[j], s);
-                        if constexpr (RAW) {
-#pragma unroll
-                            for (int r = 0; r < 4; ++r) racc[i][j][r] += s[r] >> 8;
-                        } else {
-#pragma unroll
-                            for (int r = 0; r < 4; ++r) acc[i][j][r] += sr_f[j] * (float)s[r];
-                        }
-                    }
-                }
-            }
+            };
+            if (p >= 0) tiles(std::true_type{});
+            else tiles(std::false_type{});
         }
     }
 
@@ -336,6 +359,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
         float sw_f[WN], sr_f[WN];
         const int p = cur_p;
 #pragma unroll
+        for (int j = 0; j < WN; ++j) { rlo[j] = rhi[j] = i32x4{0, 0, 0, 0}; sw_f[j] = sr_f[j] = 0.f; }
+#pragma unroll
         for (int i = 0; i < WM; ++i) unpack_nibbles(xpk[i], alo[i], ahi[i]);
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
@@ -347,37 +372,14 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
             }
         }
         if (g + 1 < ge) load(g + 1);
+        auto tiles = [&](auto has_res) {
+            constexpr bool HR = decltype(has_res)::value;
 #pragma unroll
-        for (int i = 0; i < WM; ++i) {
-#pragma unroll
-            for (int j = 0; j < WN; ++j) {
-                if constexpr (RAW) {
-                    i32x4 s = mfma_i8(alo[i], wlo[j], i32x4{0, 0, 0, 0});
-                    s = mfma_i8(ahi[i], whi[j], s);
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) iacc[i][j][r] += s[r] >> 8;
-                } else {
-                    i32x4 s = mfma_i8(alo[i], wlo[j], i32x4{0, 0, 0, 0});
-                    s = mfma_i8(ahi[i], whi[j], s);
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) acc[i][j][r] += sw_f[j] * (float)s[r];
-                }
-            }
-            if (p >= 0) {
-#pragma unroll
-                for (int j = 0; j < WN; ++j) {
-                    i32x4 s = mfma_i8(alo[i], rlo[j], i32x4{0, 0, 0, 0});
-                    s = mfma_i8(ahi[i], rhi[j], s);
-                    if constexpr (RAW) {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) racc[i][j][r] += s[r] >> 8;
-                    } else {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) acc[i][j][r] += sr_f[j] * (float)s[r];
-                    }
-                }
-            }
-        }
+            for (int i = 0; i < WM; ++i)
+                group_row<WN, RAW, HR>(alo[i], ahi[i], wlo, whi, rlo, rhi, sw_f, sr_f, acc[i], iacc[i], racc[i]);
+        };
+        if (p >= 0) tiles(std::true_type{});
+        else tiles(std::false_type{});
     }
 
     // cross-wave reduction in wave order

@@ -275,6 +275,7 @@ def test_gemm_guard_bands_and_empty(tc, mq, orc):
     ops = random_operands(M, N, K, nnzb, seed=5)
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = ops
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    Xq_d, sx_d = dev(tc, Xq), dev(tc, s_x)          # kept alive across the launches
     lib = mq.load()
     for v in (1, 2):
         if v == 1 and M > 32:
@@ -282,8 +283,8 @@ def test_gemm_guard_bands_and_empty(tc, mq, orc):
         canary = 12345
         Yfull = tc.full((M + 4, N + 8), canary, dtype=tc.int16, device="cuda")
         Yv = Yfull[2:2 + M]
-        st = lib.mq_fused_gemm_variant(v, M, N, K, dev(tc, Xq).data_ptr(),
-                                       dev(tc, s_x).data_ptr(), pw.Wq.data_ptr(), pw.s_w.data_ptr(),
+        st = lib.mq_fused_gemm_variant(v, M, N, K, Xq_d.data_ptr(),
+                                       sx_d.data_ptr(), pw.Wq.data_ptr(), pw.s_w.data_ptr(),
                                        pw.rowptr.data_ptr(), pw.kb.data_ptr(), nnzb, pw.Rq.data_ptr(),
                                        pw.s_r.data_ptr(), Yv.data_ptr(), N + 8, None, 0, None)
         tc.cuda.synchronize()
@@ -292,7 +293,7 @@ def test_gemm_guard_bands_and_empty(tc, mq, orc):
         assert np.all(h[:2] == canary) and np.all(h[2 + M:] == canary)
         assert np.all(h[2:2 + M, N:] == canary)
     Y = tc.full((1, N), 7, dtype=tc.int16, device="cuda")
-    st = lib.mq_fused_gemm(0, N, K, dev(tc, Xq).data_ptr(), dev(tc, s_x).data_ptr(),
+    st = lib.mq_fused_gemm(0, N, K, Xq_d.data_ptr(), sx_d.data_ptr(),
                            pw.Wq.data_ptr(), pw.s_w.data_ptr(), pw.rowptr.data_ptr(),
                            pw.kb.data_ptr(), nnzb, pw.Rq.data_ptr(), pw.s_r.data_ptr(),
                            Y.data_ptr(), N, None, 0, None)
@@ -305,10 +306,10 @@ def test_gemm_no_residual_null_pointers(tc, mq, orc):
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, 0, seed=9)
     Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
     Y = tc.empty((M, N), dtype=tc.float16, device="cuda")
+    keep = [dev(tc, a) for a in (Xq, s_x, Wq, s_w)]       # kept alive across the launches
     lib = mq.load()
     for v in (1, 2):
-        st = lib.mq_fused_gemm_variant(v, M, N, K, dev(tc, Xq).data_ptr(), dev(tc, s_x).data_ptr(),
-                                       dev(tc, Wq).data_ptr(), dev(tc, s_w).data_ptr(), None, None, 0,
+        st = lib.mq_fused_gemm_variant(v, M, N, K, *[t.data_ptr() for t in keep], None, None, 0,
                                        None, None, Y.data_ptr(), N, None, 0, None)
         tc.cuda.synchronize()
         assert st == 0
