@@ -20,9 +20,11 @@ microseconds per call, effective TOPS, the fraction of the INT8 MFMA peak
 bytes), and hipBLASLt W16A16 (torch.nn.functional.linear, fp16) timed the
 same way on the same shapes with rotating weights.
 
-roofline: the dominant kernel is the fused GEMM at M = 4096; its average
-launch duration is measured with HIP events around back-to-back launches on
-the stream it runs on.  cpu_baseline: the CPU oracle (C, OpenMP) on the full
+All timing replays HIP graphs (captured with torch.cuda.graph, which the
+binding follows because it launches on torch's current stream), so host-side
+launch overhead is outside the timed region; HIP events are recorded on the
+replay stream.  roofline: the dominant kernel is the fused GEMM at M = 4096;
+its average launch duration is the graph-replayed per-call time.  cpu_baseline: the CPU oracle (C, OpenMP) on the full
 step (all four M), timed once on the host cores.
 """
 from __future__ import annotations
@@ -94,7 +96,6 @@ def main():
         raise SystemExit("bench.py needs a GPU")
     mq.load()
     dev = torch.device("cuda:0")
-    stream = torch.cuda.current_stream()
     layer = synth.workload("c2_4096")
     K, N, nnzb = layer.K, layer.N, layer.nnzb
     ms = [int(m) for m in args.ms.split(",")]
@@ -126,28 +127,43 @@ def main():
             mq.quantize_act(Xs[m], out=(Xqs[m], sxs[m]))
             mq.fused_gemm(Xqs[m], sxs[m], next_pw(), out=Ys[m])
 
+    def graph_of(fn, calls):
+        """Capture `calls` back-to-back invocations of fn in one HIP graph."""
+        fn()                                   # warm the libraries outside capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(calls):
+                fn()
+        torch.cuda.synchronize()
+        return g
+
     def timed(fn, reps):
-        """Average microseconds per call of fn over reps back-to-back calls."""
-        fn()
+        """Average microseconds per call of fn: reps calls replayed from a HIP
+        graph (no host launch overhead in the timed region), HIP events on the
+        replay stream."""
+        g = graph_of(fn, reps)
+        g.replay()
         torch.cuda.synchronize()
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0.record(stream)
-        for _ in range(reps):
-            fn()
-        t1.record(stream)
+        t0.record()
+        g.replay()
+        t1.record()
         t1.synchronize()
         return t0.elapsed_time(t1) * 1e3 / reps
 
     # ------------------------------------------------------------ timed steps
-    for _ in range(args.warmup):
-        step()
+    # one graph replay = `steps` steps; warm-up replays of a separate graph
+    warm = graph_of(step, max(1, args.warmup))
+    warm.replay()
+    torch.cuda.synchronize()
+    main_graph = graph_of(step, args.steps)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
+    e0.record()
+    main_graph.replay()
+    e1.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     ms_per_step = e0.elapsed_time(e1) / args.steps

@@ -30,6 +30,10 @@
 
 namespace mq {
 
+// Kernel arguments.  Pointer use by mode: the fp16 path (mq_fused_gemm*) reads
+// s_x, s_w, s_r and writes Y; the raw-sum path (mq_fused_gemm_acc_i32) passes
+// s_x = s_w = s_r = Y = nullptr and writes Tb, Tr.  rowptr is null when there
+// are no residual blocks; res_kb, Rq (and s_r) are only read for entries of it.
 struct GemmArgs {
     int M, N, K;
     const uint8_t* Xq;
@@ -48,6 +52,14 @@ struct GemmArgs {
 
 // 1/256 removes the 16 x 16 factor of the nibble widening (exact).
 constexpr float kUnscale = 1.0f / 256.0f;
+
+// Keeps a value in registers at this point of the program: an empty volatile
+// asm that reads and writes it, so everything producing it (MFMA results and
+// their epilogue) must complete before the asm, inside the current block.
+template <typename T>
+__device__ __forceinline__ void pin(T& v) {
+    asm volatile("" : "+v"(v));
+}
 
 // One m sub-tile row of one group: base MFMA pair + epilogue for each of the
 // WN column sub-tiles, then (HAS_RES) the residual MFMA pair + epilogue.  The
@@ -91,86 +103,137 @@ __device__ __forceinline__ void group_row(const i32x4 alo, const i32x4 ahi,
 // --------------------------------------------------------------------------
 // Tiled kernel
 // --------------------------------------------------------------------------
-// WM: 16-row sub-tiles per wave along M; WN: 16-column sub-tiles per wave
-// along N; NW: waves per workgroup, all along N (they share the X tile).
-template <int WM, int WN, int NW, bool RAW>
-__global__ __launch_bounds__(64 * NW) void gemm_tiled_kernel(GemmArgs a) {
-    constexpr int BM = 16 * WM;
-    constexpr int BN = 16 * WN * NW;
-    constexpr int kThreads = 64 * NW;
-    constexpr int kXChunks = BM * 4;                       // 16-byte packed chunks per group
-    constexpr int kXPerThread = (kXChunks + kThreads - 1) / kThreads;
-    constexpr int kRowBytes = 128;                         // widened int8 row of one group
-    static_assert(WN * 16 <= 128 && 128 % (WN * 16) == 0, "wave columns must sit in one block row");
+// Workgroup: 4 waves (2 along M x 2 along N) owning a 128 x 128 output tile,
+// i.e. exactly one 128-row block row of the residual; each wave owns 64 x 64
+// (4 x 4 sub-tiles of 16 x 16, 64 fp32 accumulators).  Two workgroups share a
+// CU, so one can compute while the other waits at its barrier.
+//
+// Per 128-K group the packed X tile (128 x 64 B), W tile (128 x 64 B), the
+// group's 128 weight scales and, when the block row has a residual block at
+// this group, the R tile and its 128 scales are staged once per workgroup into
+// an LDS double buffer.  Each thread holds the next group's chunks in
+// registers: at the top of iteration g it stores group g+1 into the idle
+// buffer and issues the loads of group g+2, then the waves compute group g;
+// one barrier per group separates the two buffers' lifetimes.
+//
+// Loads use per-tile buffer resources (scalar base at the tile's first row,
+// 32-bit offsets; rows past M read as zero).  16-byte chunks are XOR-swizzled
+// by (row >> 1) & 3 inside 64-byte rows, which makes the 16-lane fragment
+// reads conflict-free (LDS serves 8 lanes of 16 B per 128-byte bank window).
+//
+// The residual runs as a second straight-line phase of the same group: the
+// wave re-reads the staged X fragments and accumulates into the same
+// registers.  With split-K (SPLIT), workgroup z handles a contiguous run of
+// groups and writes fp32 partial sums; reduce_splits_kernel adds them in split
+// order (deterministic) and applies s_x.
+constexpr int kTB = 128, kTThreads = 256;
 
-    __shared__ __attribute__((aligned(16))) uint8_t xs[2][BM * kRowBytes];
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
+
+// Linear tile order: blocks are dealt to the 8 XCDs round-robin, so give each
+// XCD a contiguous range of tiles, ordered with M fastest (the CUs of one XCD
+// then share weight strips in their L2).
+__device__ __forceinline__ void tile_coords(int b, int tiles_m, int tiles_n, int& tm, int& tn) {
+    const int nt = tiles_m * tiles_n;
+    const int xcd = b % 8, k = b / 8;
+    const int per = nt / 8, rem = nt % 8;
+    const int t = xcd < rem ? xcd * (per + 1) + k : rem * (per + 1) + (xcd - rem) * per + k;
+    tm = t % tiles_m;
+    tn = t / tiles_m;
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    const i32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
+}
+
+template <bool RAW, bool SPLIT>
+__global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, int groups_per_split,
+                                                                 float* __restrict__ part) {
+    constexpr int WM = 4, WN = 4;
+    constexpr int kRow = kGroupBytes;                       // 64 packed bytes per row per group
+    constexpr int kTile = kTB * kRow;                       // 8 KB
+    __shared__ __attribute__((aligned(16))) uint8_t xs[2][kTile];
+    __shared__ __attribute__((aligned(16))) uint8_t ws[2][kTile];
+    __shared__ __attribute__((aligned(16))) uint8_t rs[2][kTile];
+    __shared__ uint16_t sws[2][kTB], srs[2][kTB];
+    __shared__ int pres[2];
 
     const int M = a.M, N = a.N, K = a.K;
     const int G = K / kGroup;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int tiles_n = (N + BN - 1) / BN;
-    const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
-    const int m0 = tm * BM;
-    const int wn0 = tn * BN + wave * 16 * WN;
-    const bool active = wn0 < N;                            // N % 128 == 0: whole wave in or out
-    const int64_t ldk = K / 2;
-
-    // residual walk for this wave's block row
-    int rp = 0, rend = 0;
-    if (active && a.rowptr) {
-        const int nb = wn0 / 128;
-        rp = a.rowptr[nb];
-        rend = a.rowptr[nb + 1];
-    }
-    const int rrow0 = (wn0 % 128);                          // first row of this wave inside the block
-
-    // per-lane pointers
+    const uint32_t ldk = (uint32_t)(K / 2);
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
     const int lrow = lane & 15, lq = lane >> 4;
-    const uint8_t* wbase = a.Wq + (int64_t)(wn0 + lrow) * ldk + lq * 16;
-    const uint16_t* swbase = a.s_w + (int64_t)(wn0 + lrow) * G;
+    const int tiles_m = (M + kTB - 1) / kTB, tiles_n = N / kTB;
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * kTB, n0 = tn * kTB;
+    const int gb = SPLIT ? blockIdx.y * groups_per_split : 0;
+    const int ge = SPLIT ? min(G, gb + groups_per_split) : G;
 
-    // --- prefetch state (group g) ---
-    uint4 xpk[kXPerThread];
-    uint4 wpk[WN], rpk[WN];
-    uint16_t swb[WN], srb[WN];
-#pragma unroll
-    for (int j = 0; j < WN; ++j) {
-        wpk[j] = rpk[j] = make_uint4(0, 0, 0, 0);
-        swb[j] = srb[j] = 0;
+    // per-tile buffer resources
+    const uint32_t xrows = (uint32_t)min(kTB, M - m0);
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.Xq + (int64_t)m0 * ldk, xrows * ldk);
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.Wq + (int64_t)n0 * ldk, (uint32_t)kTB * ldk);
+
+    // residual walk of the tile's block row, from the first entry at or after gb
+    int rp = 0, re = 0;
+    if (a.rowptr) {
+        rp = a.rowptr[tn];
+        re = a.rowptr[tn + 1];
+        while (rp < re && a.res_kb[rp] < gb) ++rp;
     }
-    int cur_p = -1;
 
-    auto load_x = [&](int g, uint4* dst) {
-#pragma unroll
-        for (int i = 0; i < kXPerThread; ++i) {
-            const int c = threadIdx.x + i * kThreads;
-            const int row = c >> 2, q = c & 3;
-            dst[i] = make_uint4(0, 0, 0, 0);
-            if (c < kXChunks && m0 + row < M)
-                dst[i] = ldg16(a.Xq + (int64_t)(m0 + row) * ldk + (int64_t)g * kGroupBytes + q * 16);
+    // staging: chunks c = t and t + 256 -> row c / 4, 16-byte chunk c % 4
+    const int r0 = t >> 2, r1 = 64 + (t >> 2), sq = t & 3;
+    const uint32_t voff0 = (uint32_t)r0 * ldk + sq * 16, voff1 = (uint32_t)r1 * ldk + sq * 16;
+    const int dst0 = r0 * kRow + (swz(r0, sq) << 4), dst1 = r1 * kRow + (swz(r1, sq) << 4);
+    const uint32_t roff0 = (uint32_t)r0 * kRow + sq * 16, roff1 = (uint32_t)r1 * kRow + sq * 16;
+
+    uint4 x0, x1, w0, w1, q0, q1;
+    uint16_t swv = 0, srv = 0;
+    int pv = -1;
+    auto fetch = [&](int g) {
+        const uint32_t so = (uint32_t)g * kGroupBytes;
+        x0 = bload16(xr, voff0, so);
+        x1 = bload16(xr, voff1, so);
+        w0 = bload16(wr, voff0, so);
+        w1 = bload16(wr, voff1, so);
+        // scales exist only for the fp16 output path (the raw-sum entry point
+        // passes no scale pointers)
+        if constexpr (!RAW) {
+            if (t < kTB) swv = a.s_w[(int64_t)(n0 + t) * G + g];
+        }
+        pv = -1;
+        if (rp < re && a.res_kb[rp] == g) {
+            pv = rp++;
+            const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.Rq + (int64_t)pv * kTile, (uint32_t)kTile);
+            q0 = bload16(rr, roff0, 0);
+            q1 = bload16(rr, roff1, 0);
+            if constexpr (!RAW) {
+                if (t < kTB) srv = a.s_r[(int64_t)pv * kTB + t];
+            }
         }
     };
-    auto load_w = [&](int g) {
-        if (!active) return;
-#pragma unroll
-        for (int j = 0; j < WN; ++j) {
-            wpk[j] = ldg16(wbase + (int64_t)j * 16 * ldk + (int64_t)g * kGroupBytes);
-            if constexpr (!RAW) swb[j] = swbase[(int64_t)j * 16 * G + g];
+    auto stage = [&](int buf) {
+        *reinterpret_cast<uint4*>(&xs[buf][dst0]) = x0;
+        *reinterpret_cast<uint4*>(&xs[buf][dst1]) = x1;
+        *reinterpret_cast<uint4*>(&ws[buf][dst0]) = w0;
+        *reinterpret_cast<uint4*>(&ws[buf][dst1]) = w1;
+        if (t < kTB) sws[buf][t] = swv;
+        if (pv >= 0) {
+            *reinterpret_cast<uint4*>(&rs[buf][dst0]) = q0;
+            *reinterpret_cast<uint4*>(&rs[buf][dst1]) = q1;
+            if (t < kTB) srs[buf][t] = srv;
         }
-    };
-    auto load_r = [&](int p) {
-        const uint8_t* rb = a.Rq + ((int64_t)p * 128 + rrow0 + lrow) * kGroupBytes + lq * 16;
-#pragma unroll
-        for (int j = 0; j < WN; ++j) {
-            rpk[j] = ldg16(rb + j * 16 * kGroupBytes);
-            if constexpr (!RAW) srb[j] = a.s_r[(int64_t)p * 128 + rrow0 + j * 16 + lrow];
-        }
-    };
-    // residual entry for group g (advances the walk)
-    auto res_for = [&](int g) -> int {
-        if (rp < rend && a.res_kb[rp] == g) return rp++;
-        return -1;
+        if (t == 0) pres[buf] = pv;
     };
 
     f32x4 acc[WM][WN];
@@ -184,98 +247,105 @@ __global__ __launch_bounds__(64 * NW) void gemm_tiled_kernel(GemmArgs a) {
             racc[i][j] = i32x4{0, 0, 0, 0};
         }
 
-    load_x(0, xpk);
-    load_w(0);
-    if (active) {
-        cur_p = res_for(0);
-        if (cur_p >= 0) load_r(cur_p);
-    }
-
-    for (int g = 0; g < G; ++g) {
-        const int buf = g & 1;
-        // widen this group's activation chunks into LDS
-#pragma unroll
-        for (int i = 0; i < kXPerThread; ++i) {
-            const int c = threadIdx.x + i * kThreads;
-            if (c < kXChunks) {
-                const int row = c >> 2, q = c & 3;
-                i32x4 lo, hi;
-                unpack_nibbles(xpk[i], lo, hi);
-                const int sw = row & 7;
-                uint8_t* rb = &xs[buf][row * kRowBytes];
-                *reinterpret_cast<i32x4*>(rb + (((2 * q) ^ sw) << 4)) = lo;
-                *reinterpret_cast<i32x4*>(rb + (((2 * q + 1) ^ sw) << 4)) = hi;
-            }
-        }
-        // widen this group's weight (and residual) fragments
-        i32x4 wlo[WN], whi[WN], rlo[WN], rhi[WN];
-        float sw_f[WN], sr_f[WN];
-        const int p = cur_p;
-#pragma unroll
-        for (int j = 0; j < WN; ++j) { rlo[j] = rhi[j] = i32x4{0, 0, 0, 0}; sw_f[j] = sr_f[j] = 0.f; }
+    const int wrow = 64 * wm, wcol = 64 * wn;
+    // one phase of a group: B fragments from `bt` (scales `sc`), A from xs
+    auto phase = [&](const uint8_t* xt, const uint8_t* bt, const uint16_t* sc, auto is_res) {
+        constexpr bool R = decltype(is_res)::value;
+        i32x4 blo[WN], bhi[WN], dummy[WN];
+        float bs[WN], dscale[WN];
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
-            unpack_nibbles(wpk[j], wlo[j], whi[j]);
-            if constexpr (!RAW) sw_f[j] = half_bits_to_float(swb[j]) * kUnscale;
-            if (p >= 0) {
-                unpack_nibbles(rpk[j], rlo[j], rhi[j]);
-                if constexpr (!RAW) sr_f[j] = half_bits_to_float(srb[j]) * kUnscale;
-            }
+            const int row = wcol + 16 * j + lrow;
+            unpack_nibbles(*reinterpret_cast<const uint4*>(&bt[row * kRow + (swz(row, lq) << 4)]), blo[j], bhi[j]);
+            bs[j] = RAW ? 0.f : half_bits_to_float(sc[wcol + 16 * j + lrow]) * kUnscale;
+            dummy[j] = i32x4{0, 0, 0, 0};
+            dscale[j] = 0.f;
         }
-        // prefetch group g+1
-        if (g + 1 < G) {
-            load_x(g + 1, xpk);
-            load_w(g + 1);
-            cur_p = -1;
-            if (active) {
-                cur_p = res_for(g + 1);
-                if (cur_p >= 0) load_r(cur_p);
-            }
-        }
-        __syncthreads();
-        if (active) {
-            auto tiles = [&](auto has_res) {
-                constexpr bool HR = decltype(has_res)::value;
 #pragma unroll
-                for (int i = 0; i < WM; ++i) {
-                    const int row = i * 16 + lrow;
-                    const int sw = row & 7;
-                    const uint8_t* rb = &xs[buf][row * kRowBytes];
-                    const i32x4 alo = *reinterpret_cast<const i32x4*>(rb + (((2 * lq) ^ sw) << 4));
-                    const i32x4 ahi = *reinterpret_cast<const i32x4*>(rb + (((2 * lq + 1) ^ sw) << 4));
-                    group_row<WN, RAW, HR>(alo, ahi, wlo, whi, rlo, rhi, sw_f, sr_f, acc[i], iacc[i], racc[i]);
-                }
-            };
-            if (p >= 0) tiles(std::true_type{});
-            else tiles(std::false_type{});
+        for (int i = 0; i < WM; ++i) {
+            const int row = wrow + 16 * i + lrow;
+            i32x4 alo, ahi;
+            unpack_nibbles(*reinterpret_cast<const uint4*>(&xt[row * kRow + (swz(row, lq) << 4)]), alo, ahi);
+            // the residual phase feeds its fragments as the "base" operands of
+            // group_row and accumulates into racc in raw mode
+            if constexpr (R)
+                group_row<WN, RAW, false>(alo, ahi, blo, bhi, dummy, dummy, bs, dscale, acc[i], racc[i], racc[i]);
+            else
+                group_row<WN, RAW, false>(alo, ahi, blo, bhi, dummy, dummy, bs, dscale, acc[i], iacc[i], racc[i]);
         }
+        // the phase's epilogue completes inside this block (see pin)
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+            for (int j = 0; j < WN; ++j) {
+                if constexpr (!RAW) pin(acc[i][j]);
+                else if constexpr (R) pin(racc[i][j]);
+                else pin(iacc[i][j]);
+            }
+    };
+
+    if (gb < ge) {
+        fetch(gb);
+        stage(0);
+        if (gb + 1 < ge) fetch(gb + 1);
+    }
+    __syncthreads();
+    for (int g = gb; g < ge; ++g) {
+        const int buf = (g - gb) & 1;
+        if (g + 1 < ge) {
+            stage(buf ^ 1);
+            if (g + 2 < ge) fetch(g + 2);
+        }
+        phase(xs[buf], ws[buf], sws[buf], std::false_type{});
+        if (pres[buf] >= 0) phase(xs[buf], rs[buf], srs[buf], std::true_type{});
+        __syncthreads();
     }
 
-    if (!active) return;
-    // epilogue: lane holds rows 4*(lane/16)+r of each sub-tile, column lane%16
+    // epilogue: lane holds rows 4 * (lane / 16) + r of each sub-tile, column lane % 16
 #pragma unroll
     for (int i = 0; i < WM; ++i) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const int m = m0 + i * 16 + 4 * lq + r;
+            const int m = m0 + wrow + 16 * i + 4 * lq + r;
             if (m >= M) continue;
-            if constexpr (RAW) {
+            const float sx = (RAW || SPLIT) ? 0.f : half_bits_to_float(a.s_x[m]);
 #pragma unroll
-                for (int j = 0; j < WN; ++j) {
-                    const int n = wn0 + j * 16 + lrow;
+            for (int j = 0; j < WN; ++j) {
+                const int n = n0 + wcol + 16 * j + lrow;
+                if constexpr (RAW) {
                     a.Tb[(int64_t)m * N + n] = iacc[i][j][r];
                     a.Tr[(int64_t)m * N + n] = racc[i][j][r];
-                }
-            } else {
-                const float sx = half_bits_to_float(a.s_x[m]);
-#pragma unroll
-                for (int j = 0; j < WN; ++j) {
-                    const int n = wn0 + j * 16 + lrow;
+                } else if constexpr (SPLIT) {
+                    part[((int64_t)blockIdx.y * M + m) * N + n] = acc[i][j][r];
+                } else {
                     a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(sx * acc[i][j][r]);
                 }
             }
         }
     }
+}
+
+// Y[m, n] = fp16(s_x[m] * sum_{s < splits} part[s, m, n]), summed in split order.
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, int splits,
+                                                            int M, int N, const uint16_t* __restrict__ s_x,
+                                                            uint16_t* __restrict__ Y, int ldy) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t total = (int64_t)M * N;
+    if (idx >= total) return;
+    const int m = (int)(idx / N), n = (int)(idx % N);
+    float v = 0.f;
+    for (int s = 0; s < splits; ++s) v += part[s * total + idx];
+    Y[(int64_t)m * ldy + n] = float_to_half_bits(half_bits_to_float(s_x[m]) * v);
+}
+
+// Split-K factor for the tiled kernel: enough workgroups to give every CU two,
+// with at least 8 groups per split.
+static int tiled_splits(int M, int N, int K) {
+    const int tiles = ((M + kTB - 1) / kTB) * (N / kTB);
+    const int G = K / kGroup;
+    int s = 1;
+    while (tiles * s < 512 && G / (s * 2) >= 8) s *= 2;
+    return s;
 }
 
 // --------------------------------------------------------------------------
@@ -432,10 +502,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
 // Host dispatch
 // --------------------------------------------------------------------------
 constexpr int kSkinnyMaxM = 32;
+constexpr int kSkinnyAutoM = 32;   // AUTO picks the skinny kernel up to this M
 
 template <bool RAW>
-static mq_status launch(mq_variant variant, const GemmArgs& a, hipStream_t stream) {
-    if (variant == MQ_VARIANT_AUTO) variant = a.M <= 32 ? MQ_VARIANT_SKINNY : MQ_VARIANT_TILED;
+static mq_status launch(mq_variant variant, const GemmArgs& a, void* workspace, size_t ws_bytes,
+                        hipStream_t stream) {
+    if (variant == MQ_VARIANT_AUTO) variant = a.M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY : MQ_VARIANT_TILED;
     if (variant == MQ_VARIANT_SKINNY && a.M > kSkinnyMaxM) variant = MQ_VARIANT_TILED;
     if (variant == MQ_VARIANT_SKINNY) {
         constexpr int NW = 8;
@@ -445,12 +517,25 @@ static mq_status launch(mq_variant variant, const GemmArgs& a, hipStream_t strea
         else
             hipLaunchKernelGGL((gemm_skinny_kernel<2, 1, NW, RAW>), grid, block, 0, stream, a);
     } else {
-        constexpr int WM = 4, WN = 4, NW = 4;
-        constexpr int BM = 16 * WM, BN = 16 * WN * NW;
-        const int64_t tiles = (int64_t)((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+        const int64_t tiles = (int64_t)((a.M + kTB - 1) / kTB) * (a.N / kTB);
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
-        hipLaunchKernelGGL((gemm_tiled_kernel<WM, WN, NW, RAW>), dim3((unsigned)tiles), dim3(64 * NW),
-                           0, stream, a);
+        const int splits = RAW ? 1 : tiled_splits(a.M, a.N, a.K);
+        if (splits == 1) {
+            hipLaunchKernelGGL((gemm_tiled_kernel<RAW, false>), dim3((unsigned)tiles), dim3(kTThreads), 0, stream,
+                               a, 0, (float*)nullptr);
+        } else {
+            if (!workspace || ws_bytes < (size_t)splits * a.M * a.N * sizeof(float)) return MQ_ERR_WORKSPACE;
+            const int G = a.K / kGroup;
+            const int gps = (G + splits - 1) / splits;
+            float* part = static_cast<float*>(workspace);
+            hipLaunchKernelGGL((gemm_tiled_kernel<RAW, true>), dim3((unsigned)tiles, splits), dim3(kTThreads), 0,
+                               stream, a, gps, part);
+            mq_status st = mq_host::launch_status();
+            if (st != MQ_OK) return st;
+            const int64_t total = (int64_t)a.M * a.N;
+            hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                               part, splits, a.M, a.N, a.s_x, a.Y, a.ldy);
+        }
     }
     return mq_host::launch_status();
 }
@@ -475,8 +560,9 @@ static mq_status check_common(int M, int N, int K, const uint8_t* Xq, const uint
 using namespace mq;
 
 extern "C" size_t mq_fused_gemm_workspace_size(int M, int N, int K) {
-    (void)M; (void)N; (void)K;
-    return 0;
+    if (M <= 0 || !mq_host::shape_ok(N, K)) return 0;
+    const int splits = tiled_splits(M, N, K);
+    return splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
 }
 
 extern "C" mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int K,
@@ -500,7 +586,7 @@ extern "C" mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int
     GemmArgs a{M, N, K, Xq, static_cast<const uint16_t*>(s_x), Wq, static_cast<const uint16_t*>(s_w),
                nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq, static_cast<const uint16_t*>(s_r),
                static_cast<uint16_t*>(Y), ldy, nullptr, nullptr};
-    return launch<false>(variant, a, stream);
+    return launch<false>(variant, a, workspace, ws_bytes, stream);
 }
 
 extern "C" mq_status mq_fused_gemm(int M, int N, int K,
@@ -528,5 +614,5 @@ extern "C" mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int
     if (!mq_host::aligned(Tb, 4) || !mq_host::aligned(Tr, 4)) return MQ_ERR_MISALIGNED;
     GemmArgs a{M, N, K, Xq, nullptr, Wq, nullptr, nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq,
                nullptr, nullptr, 0, Tb, Tr};
-    return launch<true>(variant, a, stream);
+    return launch<true>(variant, a, nullptr, 0, stream);
 }

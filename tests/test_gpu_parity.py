@@ -397,3 +397,41 @@ def test_full_size_sampled(tc, mq, orc, name, M):
     # norm-relative bar over the sampled outputs
     den = max(np.abs(y64).max(), 1e-30)
     assert np.abs(y - y64).max() / den <= TIGHT
+
+
+def test_graph_replay_matches_eager(tc, mq, orc):
+    """The hot path captured in a HIP graph: every replay (with eager work and
+    synchronisation in between) equals the eager result bit for bit."""
+    L = synth.workload("c1_1024")
+    pw = mq.prepare_weight(dev(tc, L.weight()), L.nnzb)
+    X = dev(tc, L.act(64))
+    Xq = tc.empty((64, L.K // 2), dtype=tc.uint8, device="cuda")
+    s_x = tc.empty((64,), dtype=tc.float16, device="cuda")
+    Y = tc.empty((64, L.N), dtype=tc.float16, device="cuda")
+    Y_eager = mq.linear(X, pw).clone()
+    Ys = tc.empty((16, L.N), dtype=tc.float16, device="cuda")
+    Xs = X[:16].contiguous()
+    Xqs = tc.empty((16, L.K // 2), dtype=tc.uint8, device="cuda")
+    sxs = tc.empty((16,), dtype=tc.float16, device="cuda")
+    Ys_eager = mq.linear(Xs, pw).clone()
+
+    def body():
+        mq.quantize_act(X, out=(Xq, s_x))
+        mq.fused_gemm(Xq, s_x, pw, out=Y)
+        mq.quantize_act(Xs, out=(Xqs, sxs))
+        mq.fused_gemm(Xqs, sxs, pw, out=Ys)
+
+    body()
+    tc.cuda.synchronize()
+    g = tc.cuda.CUDAGraph()
+    with tc.cuda.graph(g):
+        body()
+    for rep in range(3):
+        Y.zero_()
+        Ys.zero_()
+        mq.linear(X[:5].contiguous(), pw)            # unrelated eager work in between
+        tc.cuda.synchronize()
+        g.replay()
+        tc.cuda.synchronize()
+        assert tc.equal(Y.view(tc.int16), Y_eager.view(tc.int16)), rep
+        assert tc.equal(Ys.view(tc.int16), Ys_eager.view(tc.int16)), rep
