@@ -127,6 +127,9 @@ __device__ __forceinline__ void group_row(const i32x4 alo, const i32x4 ahi,
 // groups and writes fp32 partial sums; reduce_splits_kernel adds them in split
 // order (deterministic) and applies s_x.
 constexpr int kTB = 128, kTThreads = 256;
+// Extra dynamic LDS per workgroup (none needed: the 3-stage ring already
+// limits a CU to two workgroups).
+constexpr int kTOccPadLds = 0;
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
 
@@ -151,17 +154,32 @@ __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t voff
     return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
 }
 
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(4))) int32_t cint32_t;   // read-only (scalar-loadable) int32
+
+// 16 bytes per lane, buffer -> LDS: lane l's bytes land at dst + 16 l.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 16, voff, soff, 0, 0);
+}
+// 2 bytes per lane, buffer -> LDS: lane l's value lands zero-extended in the
+// dword at dst + 4 l.
+__device__ __forceinline__ void dma2(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t voff, uint32_t soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 2, voff, soff, 0, 0);
+}
+
 template <bool RAW, bool SPLIT>
 __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, int groups_per_split,
                                                                  float* __restrict__ part) {
     constexpr int WM = 4, WN = 4;
     constexpr int kRow = kGroupBytes;                       // 64 packed bytes per row per group
     constexpr int kTile = kTB * kRow;                       // 8 KB
-    __shared__ __attribute__((aligned(16))) uint8_t xs[2][kTile];
-    __shared__ __attribute__((aligned(16))) uint8_t ws[2][kTile];
-    __shared__ __attribute__((aligned(16))) uint8_t rs[2][kTile];
-    __shared__ uint16_t sws[2][kTB], srs[2][kTB];
-    __shared__ int pres[2];
+    constexpr int kStages = 3;
+    struct Slot {
+        uint8_t x[kTile], w[kTile], r[kTile];
+        uint32_t sw[kTB], sr[kTB];                          // fp16 scales, zero-extended
+    };
+    __shared__ __attribute__((aligned(16))) Slot ring[kStages];
+    __shared__ int pres[kStages];
 
     const int M = a.M, N = a.N, K = a.K;
     const int G = K / kGroup;
@@ -178,62 +196,75 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
     const int gb = SPLIT ? blockIdx.y * groups_per_split : 0;
     const int ge = SPLIT ? min(G, gb + groups_per_split) : G;
 
-    // per-tile buffer resources
+    // per-tile buffer resources (rows past M read as zero)
     const uint32_t xrows = (uint32_t)min(kTB, M - m0);
     const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.Xq + (int64_t)m0 * ldk, xrows * ldk);
     const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.Wq + (int64_t)n0 * ldk, (uint32_t)kTB * ldk);
+    // zero-length resource on a valid base: every load through it returns
+    // zero without touching memory (absent residual blocks)
+    const __amdgpu_buffer_rsrc_t nullr = make_rsrc(a.Wq, 0);
 
-    // residual walk of the tile's block row, from the first entry at or after gb
+    // residual walk of the tile's block row, from the first entry at or after
+    // gb.  The CSR is read through the constant address space so the walk stays
+    // in scalar registers (scalar loads do not count against the vector-memory
+    // counter the pipeline waits on).
+    const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
     int rp = 0, re = 0;
     if (a.rowptr) {
-        rp = a.rowptr[tn];
-        re = a.rowptr[tn + 1];
-        while (rp < re && a.res_kb[rp] < gb) ++rp;
+        const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
+        rp = rowptr[tn];
+        re = rowptr[tn + 1];
+        while (rp < re && res_kb[rp] < gb) ++rp;
     }
 
-    // staging: chunks c = t and t + 256 -> row c / 4, 16-byte chunk c % 4
-    const int r0 = t >> 2, r1 = 64 + (t >> 2), sq = t & 3;
-    const uint32_t voff0 = (uint32_t)r0 * ldk + sq * 16, voff1 = (uint32_t)r1 * ldk + sq * 16;
-    const int dst0 = r0 * kRow + (swz(r0, sq) << 4), dst1 = r1 * kRow + (swz(r1, sq) << 4);
-    const uint32_t roff0 = (uint32_t)r0 * kRow + sq * 16, roff1 = (uint32_t)r1 * kRow + sq * 16;
+    // DMA lane mapping: wave w fills 1 KB blocks 2w and 2w + 1 of each 8 KB
+    // tile (16 rows each); lane l takes row 16 b + l / 4 and physical chunk
+    // l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row.
+    uint32_t vrow[2], vres[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int row = 16 * (2 * wave + i) + (lane >> 2);
+        const int c = (lane & 3) ^ ((row >> 1) & 3);
+        vrow[i] = (uint32_t)row * ldk + c * 16;
+        vres[i] = (uint32_t)row * kRow + c * 16;
+    }
+    // scales: waves 0, 1 fetch s_w of rows 64 w + lane; waves 2, 3 fetch s_r
+    const __amdgpu_buffer_rsrc_t swr = make_rsrc(a.s_w, RAW ? 0u : (uint32_t)((int64_t)N * G * 2));
+    const uint32_t vsw = (uint32_t)(n0 + 64 * (wave & 1) + lane) * (uint32_t)G * 2;
+    constexpr int kLoadsPerStage = RAW ? 6 : 7;             // DMA instructions per wave per group
 
-    uint4 x0, x1, w0, w1, q0, q1;
-    uint16_t swv = 0, srv = 0;
-    int pv = -1;
-    auto fetch = [&](int g) {
+    auto issue = [&](int g, int slot) {
+        Slot& S = ring[slot];
         const uint32_t so = (uint32_t)g * kGroupBytes;
-        x0 = bload16(xr, voff0, so);
-        x1 = bload16(xr, voff1, so);
-        w0 = bload16(wr, voff0, so);
-        w1 = bload16(wr, voff1, so);
-        // scales exist only for the fp16 output path (the raw-sum entry point
-        // passes no scale pointers)
+        dma16(xr, &S.x[(2 * wave) * 1024], vrow[0], so);
+        dma16(xr, &S.x[(2 * wave + 1) * 1024], vrow[1], so);
+        dma16(wr, &S.w[(2 * wave) * 1024], vrow[0], so);
+        dma16(wr, &S.w[(2 * wave + 1) * 1024], vrow[1], so);
+        int p = -1;
+        if (rp < re && res_kb[rp] == g) p = rp++;
+        const __amdgpu_buffer_rsrc_t rr = p >= 0 ? make_rsrc(a.Rq + (int64_t)p * kTile, (uint32_t)kTile) : nullr;
+        dma16(rr, &S.r[(2 * wave) * 1024], vres[0], 0);
+        dma16(rr, &S.r[(2 * wave + 1) * 1024], vres[1], 0);
         if constexpr (!RAW) {
-            if (t < kTB) swv = a.s_w[(int64_t)(n0 + t) * G + g];
-        }
-        pv = -1;
-        if (rp < re && a.res_kb[rp] == g) {
-            pv = rp++;
-            const __amdgpu_buffer_rsrc_t rr = make_rsrc(a.Rq + (int64_t)pv * kTile, (uint32_t)kTile);
-            q0 = bload16(rr, roff0, 0);
-            q1 = bload16(rr, roff1, 0);
-            if constexpr (!RAW) {
-                if (t < kTB) srv = a.s_r[(int64_t)pv * kTB + t];
+            if (wave < 2) {
+                dma2(swr, &S.sw[64 * wave], vsw, (uint32_t)g * 2);
+            } else {
+                const __amdgpu_buffer_rsrc_t srr =
+                    p >= 0 ? make_rsrc(a.s_r + (int64_t)p * kTB, (uint32_t)kTB * 2) : nullr;
+                dma2(srr, &S.sr[64 * (wave - 2)], (uint32_t)(64 * (wave - 2) + lane) * 2, 0);
             }
         }
+        if (t == 0) pres[slot] = p;
     };
-    auto stage = [&](int buf) {
-        *reinterpret_cast<uint4*>(&xs[buf][dst0]) = x0;
-        *reinterpret_cast<uint4*>(&xs[buf][dst1]) = x1;
-        *reinterpret_cast<uint4*>(&ws[buf][dst0]) = w0;
-        *reinterpret_cast<uint4*>(&ws[buf][dst1]) = w1;
-        if (t < kTB) sws[buf][t] = swv;
-        if (pv >= 0) {
-            *reinterpret_cast<uint4*>(&rs[buf][dst0]) = q0;
-            *reinterpret_cast<uint4*>(&rs[buf][dst1]) = q1;
-            if (t < kTB) srs[buf][t] = srv;
+    // wait until this wave's loads of the group about to be computed have
+    // landed (the next group's may stay in flight), then synchronise
+    auto sync_group = [&](bool next_in_flight) {
+        if (next_in_flight) {
+            if constexpr (kLoadsPerStage == 7) asm volatile("s_waitcnt vmcnt(7) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        } else {
+            asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
         }
-        if (t == 0) pres[buf] = pv;
     };
 
     f32x4 acc[WM][WN];
@@ -248,8 +279,8 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
         }
 
     const int wrow = 64 * wm, wcol = 64 * wn;
-    // one phase of a group: B fragments from `bt` (scales `sc`), A from xs
-    auto phase = [&](const uint8_t* xt, const uint8_t* bt, const uint16_t* sc, auto is_res) {
+    // one phase of a group: B fragments from `bt` (scales `sc`), A from xt
+    auto phase = [&](const uint8_t* xt, const uint8_t* bt, const uint32_t* sc, auto is_res) {
         constexpr bool R = decltype(is_res)::value;
         i32x4 blo[WN], bhi[WN], dummy[WN];
         float bs[WN], dscale[WN];
@@ -257,7 +288,7 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
         for (int j = 0; j < WN; ++j) {
             const int row = wcol + 16 * j + lrow;
             unpack_nibbles(*reinterpret_cast<const uint4*>(&bt[row * kRow + (swz(row, lq) << 4)]), blo[j], bhi[j]);
-            bs[j] = RAW ? 0.f : half_bits_to_float(sc[wcol + 16 * j + lrow]) * kUnscale;
+            bs[j] = RAW ? 0.f : half_bits_to_float((uint16_t)sc[wcol + 16 * j + lrow]) * kUnscale;
             dummy[j] = i32x4{0, 0, 0, 0};
             dscale[j] = 0.f;
         }
@@ -284,21 +315,17 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
             }
     };
 
-    if (gb < ge) {
-        fetch(gb);
-        stage(0);
-        if (gb + 1 < ge) fetch(gb + 1);
-    }
-    __syncthreads();
+    if (gb < ge) issue(gb, 0);
+    if (gb + 1 < ge) issue(gb + 1, 1);
     for (int g = gb; g < ge; ++g) {
-        const int buf = (g - gb) & 1;
-        if (g + 1 < ge) {
-            stage(buf ^ 1);
-            if (g + 2 < ge) fetch(g + 2);
-        }
-        phase(xs[buf], ws[buf], sws[buf], std::false_type{});
-        if (pres[buf] >= 0) phase(xs[buf], rs[buf], srs[buf], std::true_type{});
-        __syncthreads();
+        const int slot = (g - gb) % kStages;
+        // group g landed for everyone; everyone finished group g - 1, whose
+        // slot (g + 2) % 3 is refilled next
+        sync_group(g + 1 < ge);
+        if (g + 2 < ge) issue(g + 2, (g + 2 - gb) % kStages);
+        const Slot& S = ring[slot];
+        phase(S.x, S.w, S.sw, std::false_type{});
+        if (pres[slot] >= 0) phase(S.x, S.r, S.sr, std::true_type{});
     }
 
     // epilogue: lane holds rows 4 * (lane / 16) + r of each sub-tile, column lane % 16
@@ -521,15 +548,15 @@ static mq_status launch(mq_variant variant, const GemmArgs& a, void* workspace, 
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
         const int splits = RAW ? 1 : tiled_splits(a.M, a.N, a.K);
         if (splits == 1) {
-            hipLaunchKernelGGL((gemm_tiled_kernel<RAW, false>), dim3((unsigned)tiles), dim3(kTThreads), 0, stream,
-                               a, 0, (float*)nullptr);
+            hipLaunchKernelGGL((gemm_tiled_kernel<RAW, false>), dim3((unsigned)tiles), dim3(kTThreads), kTOccPadLds,
+                               stream, a, 0, (float*)nullptr);
         } else {
             if (!workspace || ws_bytes < (size_t)splits * a.M * a.N * sizeof(float)) return MQ_ERR_WORKSPACE;
             const int G = a.K / kGroup;
             const int gps = (G + splits - 1) / splits;
             float* part = static_cast<float*>(workspace);
-            hipLaunchKernelGGL((gemm_tiled_kernel<RAW, true>), dim3((unsigned)tiles, splits), dim3(kTThreads), 0,
-                               stream, a, gps, part);
+            hipLaunchKernelGGL((gemm_tiled_kernel<RAW, true>), dim3((unsigned)tiles, splits), dim3(kTThreads),
+                               kTOccPadLds, stream, a, gps, part);
             mq_status st = mq_host::launch_status();
             if (st != MQ_OK) return st;
             const int64_t total = (int64_t)a.M * a.N;
