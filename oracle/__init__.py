@@ -51,6 +51,8 @@ def lib() -> C.CDLL:
             "orc_f16_to_f32": (C.c_float, [C.c_uint16]),
             "orc_f32_to_f16_array": (None, [P, P, i64]),
             "orc_f16_to_f32_array": (None, [P, P, i64]),
+            "orc_pack_codes": (None, [P, i, i, P]),
+            "orc_unpack_code": (i, [P, i]),
             "orc_quantize_act": (None, [P, i, i, i, P, P]),
             "orc_quantize_weight": (None, [P, i, i, P, P, P]),
             "orc_block_scores_frob": (None, [P, i, i, P]),
@@ -95,18 +97,54 @@ def f16_bits_to_f32(h: np.ndarray) -> np.ndarray:
     return out
 
 
+def _zero_bits(w: int) -> int:
+    """Always-zero bits of 32-bit word w of a chunk's 96-bit field word (the
+    two middle bits, 6e+3 and 6e+4, of every 6-bit field e)."""
+    z = 0
+    for e in range(16):
+        for b in (3, 4):
+            bit = 6 * e + b
+            if bit // 32 == w:
+                z |= 1 << (bit % 32)
+    return z
+
+
 def unpack_codes(packed: np.ndarray, K: int) -> np.ndarray:
-    """Signed int8 codes [rows, K] from packed nibbles [rows, K/2] (pure numpy
-    restatement of the packing convention; used by tests only)."""
+    """Signed int8 codes [rows, K] from packed rows [rows, K/2] (pure numpy
+    restatement of the chunk layout documented in mq_oracle.c; tests only).
+    Chunk c of a row (bytes 8c..8c+7, little-endian words P0, P1) holds codes
+    16c..16c+15; the 96-bit field word is (P0 & ~ZA, P1 & ~ZB,
+    (P0 & ZA) | (P1 & ZB)) and code e is the sign-magnitude field at bit 6e."""
     p = np.ascontiguousarray(packed, dtype=np.uint8).reshape(-1, K // 2)
-    lo = (p & 0xF).astype(np.int8)
-    hi = (p >> 4).astype(np.int8)
-    lo = np.where(lo >= 8, lo - 16, lo).astype(np.int8)
-    hi = np.where(hi >= 8, hi - 16, hi).astype(np.int8)
-    out = np.empty((p.shape[0], K), np.int8)
-    out[:, 0::2] = lo
-    out[:, 1::2] = hi
-    return out
+    words = p.reshape(p.shape[0], K // 16, 2, 4).astype(np.uint64)
+    w = words[..., 0] | (words[..., 1] << 8) | (words[..., 2] << 16) | (words[..., 3] << 24)
+    p0, p1 = w[..., 0], w[..., 1]
+    za, zb = np.uint64(_zero_bits(0)), np.uint64(_zero_bits(1))
+    full = np.uint64(0xFFFFFFFF)
+    o = [p0 & (full ^ za), p1 & (full ^ zb), (p0 & za) | (p1 & zb)]
+    big = o[0] | (o[1] << np.uint64(32))          # bits 0..63 of the field word
+    out = np.empty((p.shape[0], K // 16, 16), np.int8)
+    for e in range(16):
+        lo = 6 * e
+        if lo + 6 <= 64:
+            f = (big >> np.uint64(lo)) & np.uint64(63)
+        else:                                     # fields 11..15 start in word 2 or straddle
+            f = ((o[1] >> np.uint64(lo - 32)) | (o[2] << np.uint64(64 - lo))) & np.uint64(63) \
+                if lo < 64 else (o[2] >> np.uint64(lo - 64)) & np.uint64(63)
+        mag = (f & np.uint64(7)).astype(np.int8)
+        out[..., e] = np.where((f & np.uint64(32)) != 0, -mag, mag)
+    return out.reshape(p.shape[0], K)
+
+
+def pack_codes(codes: np.ndarray) -> np.ndarray:
+    """Packed rows [rows, K/2] of int codes [rows, K] in [-7, 7] (oracle C)."""
+    q = np.ascontiguousarray(codes, dtype=np.int8)
+    q2 = q.reshape(-1, q.shape[-1])
+    if np.abs(q2.astype(np.int16)).max(initial=0) > 7:
+        raise ValueError("codes must lie in [-7, 7]")
+    out = np.empty((q2.shape[0], q2.shape[1] // 2), np.uint8)
+    lib().orc_pack_codes(_p(q2), q2.shape[0], q2.shape[1], _p(out))
+    return out.reshape(*q.shape[:-1], q.shape[-1] // 2)
 
 
 # ------------------------------------------------------- quantisation ----

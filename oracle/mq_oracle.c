@@ -28,8 +28,9 @@
  *   residual: 128x128 blocks aligned with the groups, one fp16 scale per row
  *   inside each selected block;
  *   top-K ties: lower linear block index (nb * KB + kb) wins;
- *   nibble packing: q & 0xF (two's complement), byte j of a row holds k = 2j
- *   in its low nibble and k = 2j + 1 in its high nibble.
+ *   packed layout (the paper fixes no bit layout; its Section 4.2 fuses the
+ *   layout packing with quantisation): 4 bits per code in 8-byte chunks of
+ *   16 codes, sign-magnitude, folded as described at pack_chunk() below.
  *
  * Floating point: quantisation decisions are taken in fp32 (the precision the
  * GPU kernels use, so both sides decide every code identically); scores and
@@ -124,17 +125,103 @@ static void quant_sym4(const float* v, int n, uint16_t* s_bits, int8_t* q)
     }
 }
 
-static uint8_t nib(int8_t q) { return (uint8_t)(q & 0xF); }
+/* ------------------------------------------------------------------------ */
+/* Packed layout of 4-bit codes.                                             */
+/*                                                                           */
+/* A row of K codes is K/16 chunks of 8 bytes; chunk c holds codes           */
+/* k = 16c .. 16c + 15.  Code e of a chunk (|q| <= 7) becomes the 6-bit field */
+/*     f_e = 32 * [q < 0] + |q|                                              */
+/* at bit 6e of a 96-bit word O (bits 6e+3 and 6e+4 stay zero).  Writing     */
+/* O = o0 + 2^32 o1 + 2^64 o2, let ZA (ZB) be the always-zero bits of o0     */
+/* (o1); ZA and ZB are disjoint and together cover every bit of o2 that can  */
+/* be non-zero, so the chunk stores the two little-endian 32-bit words       */
+/*     P0 = o0 | (o2 & ZA),   P1 = o1 | (o2 & ZB)                            */
+/* and o2 = (P0 & ZA) | (P1 & ZB) comes back from them.  Every 8-byte        */
+/* pattern decodes to 16 codes in [-7, 7] (a set sign bit with magnitude 0   */
+/* is the code 0).                                                           */
+/* ------------------------------------------------------------------------ */
 
-/* signed value of nibble k of a packed row */
+/* always-zero bits of word w (0, 1, 2) of O, derived from the field layout */
+static uint32_t zero_bits(int w)
+{
+    uint32_t z = 0;
+    for (int e = 0; e < 16; ++e)
+        for (int b = 3; b <= 4; ++b) {
+            int bit = 6 * e + b;
+            if (bit / 32 == w) z |= 1u << (bit % 32);
+        }
+    return z;
+}
+
+static uint32_t rd32(const uint8_t* p)
+{
+    return (uint32_t)p[0] | ((uint32_t)p[1] << 8) | ((uint32_t)p[2] << 16) | ((uint32_t)p[3] << 24);
+}
+
+static void wr32(uint8_t* p, uint32_t v)
+{
+    p[0] = (uint8_t)v; p[1] = (uint8_t)(v >> 8); p[2] = (uint8_t)(v >> 16); p[3] = (uint8_t)(v >> 24);
+}
+
+/* 16 codes -> 8 bytes */
+static void pack_chunk(const int8_t* q, uint8_t* out)
+{
+    uint32_t o[3] = {0, 0, 0};
+    for (int e = 0; e < 16; ++e) {
+        int mag = q[e] < 0 ? -q[e] : q[e];
+        uint32_t f = (uint32_t)((q[e] < 0 ? 32 : 0) + mag);
+        for (int b = 0; b < 6; ++b)
+            if (f & (1u << b)) {
+                int bit = 6 * e + b;
+                o[bit / 32] |= 1u << (bit % 32);
+            }
+    }
+    wr32(out, o[0] | (o[2] & zero_bits(0)));
+    wr32(out + 4, o[1] | (o[2] & zero_bits(1)));
+}
+
+/* 8 bytes -> 16 codes */
+static void unpack_chunk(const uint8_t* ch, int8_t* q)
+{
+    uint32_t p0 = rd32(ch), p1 = rd32(ch + 4);
+    uint32_t za = zero_bits(0), zb = zero_bits(1);
+    uint32_t o[3] = {p0 & ~za, p1 & ~zb, (p0 & za) | (p1 & zb)};
+    for (int e = 0; e < 16; ++e) {
+        uint32_t f = 0;
+        for (int b = 0; b < 6; ++b) {
+            int bit = 6 * e + b;
+            if (o[bit / 32] & (1u << (bit % 32))) f |= 1u << b;
+        }
+        int mag = (int)(f & 7u);
+        q[e] = (int8_t)((f & 32u) ? -mag : mag);
+    }
+}
+
+/* signed value of code k of a packed row */
 static int unpack_code(const uint8_t* row, int k)
 {
-    int b = row[k >> 1];
-    int n = (k & 1) ? (b >> 4) : (b & 0xF);
-    return n >= 8 ? n - 16 : n;
+    int8_t q[16];
+    unpack_chunk(row + (k / 16) * 8, q);
+    return q[k % 16];
+}
+
+/* packed bytes (K/2) -> codes of a row */
+static void unpack_row(const uint8_t* packed, int K, int8_t* out)
+{
+    for (int c = 0; c < K / 16; ++c) unpack_chunk(packed + 8 * c, out + 16 * c);
+}
+
+/* codes of a row (K a multiple of 16) -> packed bytes (K/2) */
+static void pack_row(const int8_t* q, int K, uint8_t* out)
+{
+    for (int c = 0; c < K / 16; ++c) pack_chunk(q + 16 * c, out + 8 * c);
 }
 
 int orc_unpack_code(const uint8_t* row, int k) { return unpack_code(row, k); }
+void orc_pack_codes(const int8_t* q, int rows, int K, uint8_t* out)
+{
+    for (int r = 0; r < rows; ++r) pack_row(q + (int64_t)r * K, K, out + (int64_t)r * (K / 2));
+}
 
 /* ------------------------------------------------------------------------ */
 /* Per-token activation quantisation (Eq. 1 applied row by row).             */
@@ -148,9 +235,7 @@ void orc_quantize_act(const uint16_t* X, int M, int K, int ldx,
         int8_t* q = (int8_t*)malloc((size_t)K);
         for (int k = 0; k < K; ++k) v[k] = orc_f16_to_f32(X[(int64_t)m * ldx + k]);
         quant_sym4(v, K, &s_x[m], q);
-        uint8_t* out = Xq + (int64_t)m * (K / 2);
-        for (int j = 0; j < K / 2; ++j)
-            out[j] = (uint8_t)(nib(q[2 * j]) | (nib(q[2 * j + 1]) << 4));
+        pack_row(q, K, Xq + (int64_t)m * (K / 2));
         free(v);
         free(q);
     }
@@ -173,9 +258,7 @@ void orc_quantize_weight(const float* W, int N, int K,
             quant_sym4(v, ORC_BLOCK, &sb, q);
             s_w[(int64_t)n * G + g] = sb;
             float s = orc_f16_to_f32(sb);
-            uint8_t* out = Wq + (int64_t)n * (K / 2) + (int64_t)g * (ORC_BLOCK / 2);
-            for (int j = 0; j < ORC_BLOCK / 2; ++j)
-                out[j] = (uint8_t)(nib(q[2 * j]) | (nib(q[2 * j + 1]) << 4));
+            pack_row(q, ORC_BLOCK, Wq + (int64_t)n * (K / 2) + (int64_t)g * (ORC_BLOCK / 2));
             if (R) {
                 float* r = R + (int64_t)n * K + (int64_t)g * ORC_BLOCK;
                 for (int i = 0; i < ORC_BLOCK; ++i) {
@@ -311,9 +394,7 @@ void orc_quantize_residual(const float* R, int N, int K,
             for (int r = 0; r < ORC_BLOCK; ++r) {
                 const float* v = R + (int64_t)(nb * ORC_BLOCK + r) * K + kb * ORC_BLOCK;
                 quant_sym4(v, ORC_BLOCK, &s_r[(int64_t)p * ORC_BLOCK + r], q);
-                uint8_t* out = Rq + ((int64_t)p * ORC_BLOCK + r) * (ORC_BLOCK / 2);
-                for (int j = 0; j < ORC_BLOCK / 2; ++j)
-                    out[j] = (uint8_t)(nib(q[2 * j]) | (nib(q[2 * j + 1]) << 4));
+                pack_row(q, ORC_BLOCK, Rq + ((int64_t)p * ORC_BLOCK + r) * (ORC_BLOCK / 2));
             }
         }
     }
@@ -380,9 +461,11 @@ static void layer_elem(const orc_layer* L, const int8_t* xrow, const int8_t* wro
         int p = L->pmap[(n / ORC_BLOCK) * L->G + g];
         if (p >= 0) {
             const uint8_t* rrow = L->Rq + ((int64_t)p * ORC_BLOCK + n % ORC_BLOCK) * (ORC_BLOCK / 2);
+            int8_t rc[ORC_BLOCK];
+            unpack_row(rrow, ORC_BLOCK, rc);
             int64_t ar = 0;
             for (int c = 0; c < ORC_BLOCK; ++c)
-                ar += (int64_t)xrow[g * ORC_BLOCK + c] * unpack_code(rrow, c);
+                ar += (int64_t)xrow[g * ORC_BLOCK + c] * rc[c];
             Tr += ar;
             acc += L->sr[(int64_t)p * ORC_BLOCK + n % ORC_BLOCK] * (double)ar;
         }
@@ -393,10 +476,6 @@ static void layer_elem(const orc_layer* L, const int8_t* xrow, const int8_t* wro
     *y = L->sx[m] * acc;
 }
 
-static void unpack_row(const uint8_t* packed, int K, int8_t* out)
-{
-    for (int k = 0; k < K; ++k) out[k] = (int8_t)unpack_code(packed, k);
-}
 
 /* Full layer: Tb, Tr, Y64 are [M, N] row-major (any may be NULL).
  * Returns the number of entries of Tb or Tr outside the int32 range. */

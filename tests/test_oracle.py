@@ -95,6 +95,63 @@ def test_f32_to_f16_matches_numpy(orc):
     assert np.array_equal(got, ref)
 
 
+# ------------------------------------------------------ packed layout ----
+def _read_layout():
+    cases, cur = [], {}
+    for line in open(os.path.join(GOLDEN, "pack_layout.txt")):
+        line = line.split("#", 1)[0].strip()
+        if not line:
+            continue
+        key, val = line.split(":", 1)
+        cur[key] = val.split()
+        if key == "bytes":
+            cases.append(cur)
+            cur = {}
+    return cases
+
+
+@pytest.mark.parametrize("case", _read_layout(), ids=lambda c: " ".join(c["codes"])[:20])
+def test_pack_layout_golden(orc, case):
+    """Hand-worked chunks: packing gives the fixture's bytes, both decoders
+    (C and numpy) give the codes back."""
+    codes = np.array([int(v) for v in case["codes"]], np.int8)[None, :]
+    want = bytes(int(b, 16) for b in case["bytes"])
+    packed = orc.pack_codes(codes)
+    assert packed.tobytes() == want
+    buf = np.frombuffer(want, np.uint8)[None, :]
+    assert orc.unpack_codes(buf, 16)[0].tolist() == codes[0].tolist()
+    import ctypes
+    ptr = buf.ctypes.data_as(ctypes.c_void_p)
+    assert [orc.lib().orc_unpack_code(ptr, k) for k in range(16)] == codes[0].tolist()
+
+
+def test_pack_layout_invariants(orc):
+    """Round trip of random codes; every byte pattern decodes to [-7, 7] with
+    the C and numpy decoders agreeing; the fold masks partition the third
+    word's data bits."""
+    rng = np.random.default_rng(11)
+    codes = rng.integers(-7, 8, (9, 512)).astype(np.int8)
+    assert np.array_equal(orc.unpack_codes(orc.pack_codes(codes), 512), codes)
+    raw = rng.integers(0, 256, (4, 64), dtype=np.uint8)
+    dec = orc.unpack_codes(raw, 128)
+    assert dec.min() >= -7 and dec.max() <= 7
+    import ctypes
+    for r in range(4):
+        ptr = raw[r].ctypes.data_as(ctypes.c_void_p)
+        assert [orc.lib().orc_unpack_code(ptr, k) for k in range(128)] == dec[r].tolist()
+    # re-packing a decoded random pattern reproduces it except for sign bits
+    # of zero codes (the only redundancy of the encoding)
+    assert np.array_equal(orc.unpack_codes(orc.pack_codes(dec), 128), dec)
+    za, zb, z2 = orc._zero_bits(0), orc._zero_bits(1), orc._zero_bits(2)
+    assert za & zb == 0 and (za | zb) == (~z2 & 0xFFFFFFFF)
+    # each code lands in its own chunk position: a single non-zero code moves
+    # exactly one decoded position
+    for k in (0, 5, 10, 15, 16, 31, 127):
+        one = np.zeros((1, 128), np.int8)
+        one[0, k] = -5
+        assert np.flatnonzero(orc.unpack_codes(orc.pack_codes(one), 128)[0]).tolist() == [k]
+
+
 # ------------------------------------------------------- quantiser -------
 def _read_ties():
     cases, cur = [], {}
@@ -113,8 +170,8 @@ def _read_ties():
 @pytest.mark.parametrize("case", _read_ties(), ids=lambda c: " ".join(c["x"])[:24])
 def test_quantizer_golden_ties(orc, case):
     x = np.array([float(v) for v in case["x"]], np.float16)[None, :]
-    xq, s = orc.quantize_act(x) if x.shape[1] % 2 == 0 else orc.quantize_act(
-        np.concatenate([x, np.zeros((1, 1), np.float16)], axis=1))
+    pad = -x.shape[1] % 16                      # the packed layout holds chunks of 16 codes
+    xq, s = orc.quantize_act(np.concatenate([x, np.zeros((1, pad), np.float16)], axis=1))
     assert float(f16(s)[0]) == float(case["s"][0])
     codes = orc.unpack_codes(xq, xq.shape[1] * 2)[0][: len(case["q"])]
     assert codes.tolist() == [int(v) for v in case["q"]]
@@ -317,8 +374,9 @@ def test_linear_sampled_matches_full(orc):
 def test_int32_range_extremes(orc):
     """All codes at +-7 over a long K: accumulators stay exact and in int32."""
     K, N, M = 28672, 128, 2
-    Xq = np.full((M, K // 2), 0x77, np.uint8)                 # +7 everywhere
-    Xq[1] = 0x99                                              # -7 everywhere
+    codes = np.full((M, K), 7, np.int8)
+    codes[1] = -7
+    Xq = orc.pack_codes(codes)
     s_x = np.full(M, np.float16(1).view(np.uint16))
     W = np.full((N, K), 0.7, np.float32)
     pw = orc.prepare_weight(W, 0)
@@ -507,7 +565,7 @@ def test_planted_mistakes_are_caught(orc):
             blk = rdeq_t[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B]
             rdeq_t[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B] = blk.T
     assert np.abs((xc * f16(s_x)[:, None]) @ (dequant_base(pw, orc) + rdeq_t).T - Yref).max() > tol
-    # swapped nibble order
+    # swapped element order
     wsw = np.empty_like(wc)
     wsw[:, 0::2], wsw[:, 1::2] = wc[:, 1::2], wc[:, 0::2]
     assert not np.array_equal(xc @ wsw.T, Tb)
