@@ -42,6 +42,10 @@ sys.path.insert(0, ROOT)
 PEAK_I8_TOPS = 5000.0          # MI355X dense INT8 MFMA, TOP/s
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
 ROTATE_BYTES = 600 << 20       # > 512 MB of distinct weight copies
+TRAFFIC_CALLS = 8              # dispatches per kernel in a --traffic counter run
+COPY_BYTES = 256 << 20         # size of the reference copy in a --traffic run
+CPU_MIN_S = 10.0               # cpu_baseline repeats whole steps for at least this long
+CPU_MAX_STEPS = 8
 GEMM_SRC = os.path.join(ROOT, "paper_2606_15652_amd", "csrc", "fused_gemm.hip")
 
 
@@ -55,6 +59,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-blas", action="store_true")
     ap.add_argument("--quick", action="store_true", help="short run for profilers")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="fold the counter_collection.csv files of two --traffic runs (FETCH_SIZE, "
+                         "WRITE_SIZE) into profiles/fused_gemm_traffic.json; needs no GPU")
+    ap.add_argument("--traffic", action="store_true",
+                    help="counter run: eager fused GEMM launches at the largest M, then a plain "
+                         "256 MiB device copy as the scale reference for FETCH_SIZE / WRITE_SIZE")
     return ap.parse_args()
 
 
@@ -77,8 +87,52 @@ def quant_bytes(M, K):
     return M * K * 2 + M * K / 2 + M * 2
 
 
+def summarize_traffic(fetch_csv, write_csv, m):
+    """HBM bytes per fused GEMM dispatch from two rocprofv3 --pmc runs of
+    `bench.py --traffic`.  Each counter (KiB per dispatch) is scaled by
+    known bytes / counter reading of the reference copy, the last
+    TRAFFIC_CALLS dispatches of the run."""
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        by_disp = {}
+        for r in rows:       # one value per dispatch (summed over any per-XCD rows)
+            d = int(r["Dispatch_Id"])
+            name, v = by_disp.get(d, (r["Kernel_Name"], 0.0))
+            by_disp[d] = (name, v + float(r["Counter_Value"]))
+        disp = sorted(by_disp.items())
+        gemm = [v for _, (name, v) in disp if "gemm_tiled_kernel" in name]
+        copy = [v for _, (_, v) in disp[-TRAFFIC_CALLS:]]
+        if not gemm or len(copy) < TRAFFIC_CALLS:
+            raise SystemExit(f"{path}: no gemm_tiled_kernel or reference copy dispatches for {counter}")
+        return statistics.median(gemm), statistics.median(copy)
+
+    g_f, c_f = per_kernel(fetch_csv, "FETCH_SIZE")
+    g_w, c_w = per_kernel(write_csv, "WRITE_SIZE")
+    kib = COPY_BYTES / 1024.0
+    f_scale, w_scale = kib / c_f, kib / c_w
+    fetch_b = g_f * f_scale * 1024.0
+    write_b = g_w * w_scale * 1024.0
+    out = {"kernel": "gemm_tiled_kernel", "M": m, "src_hash": src_hash(GEMM_SRC),
+           "fetch_kib_raw": g_f, "write_kib_raw": g_w,
+           "copy_fetch_kib_raw": c_f, "copy_write_kib_raw": c_w, "copy_bytes": COPY_BYTES,
+           "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+           "fetch_bytes": round(fetch_b), "write_bytes": round(write_b),
+           "bytes_per_launch": round(fetch_b + write_b)}
+    path = os.path.join(ROOT, "profiles", "fused_gemm_traffic.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out))
+
+
 def main():
     args = parse()
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic, m=max(int(x) for x in args.ms.split(",")))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
@@ -151,6 +205,24 @@ def main():
         t1.record()
         t1.synchronize()
         return t0.elapsed_time(t1) * 1e3 / reps
+
+    if args.traffic:
+        # For rocprofv3 --pmc: TRAFFIC_CALLS GEMM dispatches at the largest M,
+        # each on its own weight copy, then TRAFFIC_CALLS copies of 256 MiB.
+        mdom = max(ms)
+        mq.quantize_act(Xs[mdom], out=(Xqs[mdom], sxs[mdom]))
+        for _ in range(TRAFFIC_CALLS):
+            mq.fused_gemm(Xqs[mdom], sxs[mdom], next_pw(), out=Ys[mdom])
+        # an elementwise kernel that reads and writes COPY_BYTES each (a
+        # same-dtype copy_ could be served by a DMA engine, invisible to the counters)
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(TRAFFIC_CALLS):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(json.dumps({"traffic_run": True, "M": mdom, "calls": TRAFFIC_CALLS,
+                          "copy_bytes": COPY_BYTES}), flush=True)
+        return
 
     # ------------------------------------------------------------ timed steps
     # one graph replay = `steps` steps; warm-up replays of a separate graph
@@ -233,14 +305,19 @@ def main():
         ref = oracle.prepare_weight(Wn, nnzb)
         xs_np = {m: layer.act(m) for m in ms}
         oracle.linear(*oracle.quantize_act(xs_np[1]), ref)        # warm-up
+        nsteps = 0
         c0 = time.perf_counter()
-        for m in ms:
-            xq, sx = oracle.quantize_act(xs_np[m])
-            oracle.linear(xq, sx, ref)
-        cs = time.perf_counter() - c0
+        while nsteps < CPU_MAX_STEPS and (nsteps == 0 or time.perf_counter() - c0 < CPU_MIN_S):
+            for m in ms:
+                xq, sx = oracle.quantize_act(xs_np[m])
+                oracle.linear(xq, sx, ref)
+            nsteps += 1
+        cs = (time.perf_counter() - c0) / nsteps
         cpu = {"value": round(eff_ops / cs / 1e12, 6), "unit": "TOPS", "cores": oracle.num_threads(),
-               "kind": "oracle", "seconds": round(cs, 3),
-               "sample": f"one full step (M={','.join(map(str, ms))}; quantise + int64 GEMM + fp64 epilogue)"}
+               "kind": "oracle", "seconds_per_step": round(cs, 3), "steps": nsteps,
+               "sample": f"{nsteps} full step(s) of the same workload (M={','.join(map(str, ms))}: "
+                         "activation quantisation + int64 GEMM + fp64 epilogue), weight "
+                         "preparation excluded"}
 
     out = {
         "metric": "effective TOPS of fused W4A4+residual GEMM (with act quant) over M=1..4096",

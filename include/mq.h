@@ -21,9 +21,19 @@
  * - fp16 arrays are IEEE binary16 passed as `void*` / `const void*`.
  * - Shapes: K and N are multiples of 128 with 128 <= K <= 2^20 and
  *   128 <= N <= 2^24; 0 <= M <= 2^24 (M == 0 is a no-op).
- * - 4-bit codes are two's-complement nibbles in [-7, 7] (the quantisers never
- *   produce -8; the GEMM accepts it).  Byte j of a packed row holds element 2j
- *   in its low nibble and element 2j+1 in its high nibble.
+ * - Packed 4-bit codes (Xq, Wq, Rq): codes q in [-7, 7], 4 bits each, a row
+ *   of K codes taking K/2 bytes as K/16 chunks of 8 bytes; chunk c holds codes
+ *   16c .. 16c+15.  Code e of a chunk is the 6-bit sign-magnitude field
+ *   f_e = 32 [q < 0] + |q| at bit 6e of a 96-bit word O = (o0, o1, o2) of
+ *   32-bit words; bits 6e+3 and 6e+4 of every field are zero.  The zero bits
+ *   of o0 (ZA = 0x18618618) and of o1 (ZB = 0x86186186) together cover every
+ *   bit o2 can use, and the chunk stores the little-endian words
+ *       P0 = o0 | (o2 & ZA),   P1 = o1 | (o2 & ZB).
+ *   Every byte pattern is a valid chunk (a sign bit with magnitude 0 is the
+ *   code 0).  The layout lets the GEMM feed the codes, unchanged in value, to
+ *   the fp6 (e2m3) matrix instruction of CDNA4 with four bit operations per
+ *   chunk; the paper fixes no bit layout (Section 4.2 fuses layout packing
+ *   with quantisation).
  * - Packed operand pointers (Xq, Wq, Rq) must be 16-byte aligned; fp16
  *   pointers 2-byte aligned; int32 pointers 4-byte aligned; fp32/fp64 arrays
  *   naturally aligned.  Violations return MQ_ERR_MISALIGNED.
@@ -72,12 +82,12 @@ int mq_version(void);
 
 /*
  * Per-token symmetric INT4 activation quantisation (Section 2, Eq. (1), one
- * scale per token; fused with nibble packing as in Section 4.2 "Kernel
+ * scale per token; fused with code packing as in Section 4.2 "Kernel
  * Fusion"):
  *     a = max_k |X[m,k]|,  s_x[m] = fp16_rn(fp32(a) / 7),
  *     Xq[m,k] = clamp(round_half_even(X[m,k] / s_x[m]), -7, 7)  (0 if s == 0)
  *   X   : fp16 [M, ldx] row-major, ldx >= K, ldx % 8 == 0, 16-byte aligned.
- *   Xq  : out, uint8 [M, K/2] packed nibbles.
+ *   Xq  : out, uint8 [M, K/2] packed codes (layout above).
  *   s_x : out, fp16 [M].
  */
 mq_status mq_quantize_act(const void* X, int M, int K, int ldx,
@@ -128,7 +138,7 @@ mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int K,
 /*
  * Same main loop, raw integer epilogue (for bit-exact testing):
  *     Tb[m,n] = sum_g A_b[m,n,g],   Tr[m,n] = sum_g A_r[m,n,g]
- *   Tb, Tr : out, int32 [M, N] row-major.  Exact: |Tb|, |Tr| <= 64 K < 2^31
+ *   Tb, Tr : out, int32 [M, N] row-major.  Exact: |Tb|, |Tr| <= 49 K < 2^31
  *            for every supported K.
  */
 mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int K,

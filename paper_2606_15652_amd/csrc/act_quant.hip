@@ -1,14 +1,15 @@
-// Per-token symmetric INT4 activation quantisation fused with nibble packing
+// Per-token symmetric INT4 activation quantisation fused with code packing
 // (Section 2, Eq. (1) applied per row; Section 4.2 "Kernel Fusion": layout
 // packing is fused with quantisation).
 //
-// One workgroup of 256 threads per token row.  Each thread owns 16-byte
-// chunks (8 fp16) of the row; the row maximum of |x| is taken on the fp16 bit
+// One workgroup of 256 threads per token row.  Each thread owns 32-byte
+// chunks (16 fp16) of the row; the row maximum of |x| is taken on the fp16 bit
 // patterns with the sign cleared (an order-preserving integer max for finite
 // values), reduced across the wave with xor-shuffles and across the four waves
 // through LDS.  Codes are then formed from the registers (rows up to
-// CPT * 2048 elements) or by re-reading the row (longer rows), and written as
-// 4 packed bytes per chunk: fully coalesced 16-byte loads, 4-byte stores.
+// CPT * 4096 elements) or by re-reading the row (longer rows), and written as
+// one folded 8-byte chunk per 16 codes (fold_codes): coalesced 16-byte loads,
+// 8-byte stores.
 #include "mq_device.h"
 
 namespace mq {
@@ -27,19 +28,17 @@ __device__ __forceinline__ uint32_t chunk_absmax_bits(const uint4 v) {
     return m;
 }
 
-// 8 fp16 -> 8 codes -> 4 packed bytes (element 2j low nibble, 2j+1 high).
-__device__ __forceinline__ uint32_t quant_chunk(const uint4 v, float s) {
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t out = 0;
-    if (s == 0.0f) return 0u;
+// 16 fp16 -> 16 codes -> one folded chunk.
+__device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, float s) {
+    if (s == 0.0f) return make_uint2(0u, 0u);
+    const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    int q[16];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        int q0 = quant_code(half_bits_to_float((uint16_t)(w[i] & 0xFFFFu)), s);
-        int q1 = quant_code(half_bits_to_float((uint16_t)(w[i] >> 16)), s);
-        uint32_t byte = ((uint32_t)q0 & 0xFu) | (((uint32_t)q1 & 0xFu) << 4);
-        out |= byte << (8 * i);
+    for (int i = 0; i < 8; ++i) {
+        q[2 * i] = quant_code(half_bits_to_float((uint16_t)(w[i] & 0xFFFFu)), s);
+        q[2 * i + 1] = quant_code(half_bits_to_float((uint16_t)(w[i] >> 16)), s);
     }
-    return out;
+    return fold_codes(q);
 }
 
 // CPT > 0: the row stays in registers (CPT chunks per thread); CPT == 0: the
@@ -52,25 +51,29 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
     const int m = blockIdx.x;
     const int t = threadIdx.x;
     const uint16_t* row = X + (int64_t)m * ldx;
-    uint32_t* out = reinterpret_cast<uint32_t*>(Xq + (int64_t)m * (K / 2));
-    const int nchunks = K / 8;
+    uint2* out = reinterpret_cast<uint2*>(Xq + (int64_t)m * (K / 2));
+    const int nchunks = K / 16;
 
     uint32_t amax = 0;
-    uint4 v[CPT > 0 ? CPT : 1];
+    uint4 v[CPT > 0 ? CPT : 1][2];
     if constexpr (CPT > 0) {
 #pragma unroll
         for (int i = 0; i < CPT; ++i) {
             const int c = t + i * kActThreads;
             if (c < nchunks) {
-                v[i] = *reinterpret_cast<const uint4*>(row + 8 * c);
-                const uint32_t cm = chunk_absmax_bits(v[i]);
-                amax = cm > amax ? cm : amax;
+                v[i][0] = *reinterpret_cast<const uint4*>(row + 16 * c);
+                v[i][1] = *reinterpret_cast<const uint4*>(row + 16 * c + 8);
+                const uint32_t cm0 = chunk_absmax_bits(v[i][0]), cm1 = chunk_absmax_bits(v[i][1]);
+                amax = cm0 > amax ? cm0 : amax;
+                amax = cm1 > amax ? cm1 : amax;
             }
         }
     } else {
         for (int c = t; c < nchunks; c += kActThreads) {
-            const uint32_t cm = chunk_absmax_bits(*reinterpret_cast<const uint4*>(row + 8 * c));
-            amax = cm > amax ? cm : amax;
+            const uint32_t cm0 = chunk_absmax_bits(*reinterpret_cast<const uint4*>(row + 16 * c));
+            const uint32_t cm1 = chunk_absmax_bits(*reinterpret_cast<const uint4*>(row + 16 * c + 8));
+            amax = cm0 > amax ? cm0 : amax;
+            amax = cm1 > amax ? cm1 : amax;
         }
     }
     amax = wave_max_u32(amax);
@@ -88,11 +91,12 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
 #pragma unroll
         for (int i = 0; i < CPT; ++i) {
             const int c = t + i * kActThreads;
-            if (c < nchunks) out[c] = quant_chunk(v[i], s);
+            if (c < nchunks) out[c] = quant_chunk(v[i][0], v[i][1], s);
         }
     } else {
         for (int c = t; c < nchunks; c += kActThreads)
-            out[c] = quant_chunk(*reinterpret_cast<const uint4*>(row + 8 * c), s);
+            out[c] = quant_chunk(*reinterpret_cast<const uint4*>(row + 16 * c),
+                                 *reinterpret_cast<const uint4*>(row + 16 * c + 8), s);
     }
 }
 
@@ -111,7 +115,7 @@ extern "C" mq_status mq_quantize_act(const void* X, int M, int K, int ldx,
         return MQ_ERR_MISALIGNED;
     const auto* x = static_cast<const uint16_t*>(X);
     auto* s = static_cast<uint16_t*>(s_x);
-    const int chunks_per_thread = (K / 8 + kActThreads - 1) / kActThreads;
+    const int chunks_per_thread = (K / 16 + kActThreads - 1) / kActThreads;
     dim3 grid(M), block(kActThreads);
     if (chunks_per_thread <= 1)
         hipLaunchKernelGGL(act_quant_kernel<1>, grid, block, 0, stream, x, K, ldx, Xq, s);

@@ -4,22 +4,22 @@
 //
 //   Y[m,n] = s_x[m] * sum_g ( s_w[n,g] A_b[m,n,g] + s_r[p,n%128] A_r[m,n,g] )
 //
-// CDNA4 has no 4-bit matrix instruction, so packed nibbles are widened in
-// registers to int8 (16 * code, see unpack_nibbles) and fed to
-// v_mfma_i32_16x16x64_i8.  One MFMA pair covers one 128-long group of a 16x16
-// output sub-tile; its int32 result is the exact group sum (times 256), which
-// the epilogue converts and scales into an fp32 accumulator.  The residual
-// blocks of the tile's 128-row block row are walked in the same K-loop: when
-// the CSR's next column equals the current group, the residual fragments are
-// multiplied with the activation fragments already staged for the dense term
-// and accumulated into the same output registers.
+// CDNA4 has no 4-bit integer matrix instruction.  The packed codes are stored
+// so that a 16-byte pair of chunks expands with four bit operations per chunk
+// into the operand of v_mfma_f32_16x16x128_f8f6f4 read as fp6 e2m3, where each
+// code q is the exact subnormal q/8 (unfold_codes).  One instruction covers
+// one whole 128-long group of a 16x16 output sub-tile, its fp32 result is the
+// exact group sum / 64, and the epilogue is one fma per element and group with
+// the scale times 64.  The residual blocks of the tile's 128-row block row are
+// walked in the same K-loop: when the CSR's next column equals the current
+// group, the residual fragments are multiplied with the activation fragments
+// already staged for the dense term and accumulated into the same output
+// registers.
 //
 // Two kernel families share that inner step:
-//  * tiled  (prefill):  a workgroup owns a BM x BN output tile; the packed
-//    activation tile of each group is widened once per workgroup into an LDS
-//    double buffer (XOR-swizzled 16-byte chunks) and shared by all waves, each
-//    wave streams its own weight rows straight from global memory into
-//    registers, one group ahead of the MFMAs.
+//  * tiled  (prefill):  a workgroup owns a 128 x 128 output tile; the packed X,
+//    W and (when present) R tiles of each group are copied by the LDS DMA into
+//    a 3-stage ring shared by its four waves.
 //  * skinny (decode, small M): a workgroup owns 16 output columns and all M
 //    rows; its waves split the K-loop, each streaming a contiguous run of
 //    groups, and the fp32 partial tiles are reduced through LDS in wave order
@@ -50,9 +50,6 @@ struct GemmArgs {
     int32_t* Tr;
 };
 
-// 1/256 removes the 16 x 16 factor of the nibble widening (exact).
-constexpr float kUnscale = 1.0f / 256.0f;
-
 // Keeps a value in registers at this point of the program: an empty volatile
 // asm that reads and writes it, so everything producing it (MFMA results and
 // their epilogue) must complete before the asm, inside the current block.
@@ -61,40 +58,39 @@ __device__ __forceinline__ void pin(T& v) {
     asm volatile("" : "+v"(v));
 }
 
-// One m sub-tile row of one group: base MFMA pair + epilogue for each of the
-// WN column sub-tiles, then (HAS_RES) the residual MFMA pair + epilogue.  The
-// caller picks HAS_RES once per group, so this is straight-line code and every
-// MFMA result is converted inside the basic block that produced it (the
-// compiler's MFMA-to-VALU wait states are only placed reliably within a block).
+// One m sub-tile row of one group: base MFMA + epilogue for each of the WN
+// column sub-tiles, then (HAS_RES) the residual MFMA + epilogue.  sw / sr carry
+// the scales times kCodeScale.  The caller picks HAS_RES once per group, so
+// this is straight-line code and every MFMA result is consumed inside the
+// basic block that produced it (the compiler's MFMA-to-VALU wait states are
+// only placed reliably within a block).  Raw mode adds the exact integer group
+// sums instead.
 template <int WN, bool RAW, bool HAS_RES>
-__device__ __forceinline__ void group_row(const i32x4 alo, const i32x4 ahi,
-                                          const i32x4 (&wlo)[WN], const i32x4 (&whi)[WN],
-                                          const i32x4 (&rlo)[WN], const i32x4 (&rhi)[WN],
-                                          const float (&sw_f)[WN], const float (&sr_f)[WN],
+__device__ __forceinline__ void group_row(const i32x8 a, const i32x8 (&w)[WN], const i32x8 (&rr)[WN],
+                                          const float (&sw)[WN], const float (&sr)[WN],
                                           f32x4 (&acc)[WN], i32x4 (&iacc)[WN], i32x4 (&racc)[WN]) {
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < WN; ++j) {
-        i32x4 s = mfma_i8(alo, wlo[j], i32x4{0, 0, 0, 0});
-        s = mfma_i8(ahi, whi[j], s);
+        const f32x4 t = mfma_codes(a, w[j], zero);
         if constexpr (RAW) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) iacc[j][r] += s[r] >> 8;  // exact: s is 256 x the sum
+            for (int r = 0; r < 4; ++r) iacc[j][r] += (int)(t[r] * kCodeScale);   // exact integer
         } else {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) acc[j][r] += sw_f[j] * (float)s[r];
+            for (int r = 0; r < 4; ++r) acc[j][r] = __builtin_fmaf(sw[j], t[r], acc[j][r]);
         }
     }
     if constexpr (HAS_RES) {
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
-            i32x4 s = mfma_i8(alo, rlo[j], i32x4{0, 0, 0, 0});
-            s = mfma_i8(ahi, rhi[j], s);
+            const f32x4 t = mfma_codes(a, rr[j], zero);
             if constexpr (RAW) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) racc[j][r] += s[r] >> 8;
+                for (int r = 0; r < 4; ++r) racc[j][r] += (int)(t[r] * kCodeScale);
             } else {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) acc[j][r] += sr_f[j] * (float)s[r];
+                for (int r = 0; r < 4; ++r) acc[j][r] = __builtin_fmaf(sr[j], t[r], acc[j][r]);
             }
         }
     }
@@ -110,11 +106,12 @@ __device__ __forceinline__ void group_row(const i32x4 alo, const i32x4 ahi,
 //
 // Per 128-K group the packed X tile (128 x 64 B), W tile (128 x 64 B), the
 // group's 128 weight scales and, when the block row has a residual block at
-// this group, the R tile and its 128 scales are staged once per workgroup into
-// an LDS double buffer.  Each thread holds the next group's chunks in
-// registers: at the top of iteration g it stores group g+1 into the idle
-// buffer and issues the loads of group g+2, then the waves compute group g;
-// one barrier per group separates the two buffers' lifetimes.
+// this group, the R tile and its 128 scales go by LDS DMA (buffer loads that
+// write LDS directly, no staging registers) into one slot of a 3-stage ring:
+// at iteration g the waves wait for group g's loads, meet at the barrier that
+// also frees the slot of group g-1, issue group g+2 into it and compute g.
+// The DMA does not raise the compiler's wait counters, so the kernel waits on
+// the vector-memory counter itself (sync_group).
 //
 // Loads use per-tile buffer resources (scalar base at the tile's first row,
 // 32-bit offsets; rows past M read as zero).  16-byte chunks are XOR-swizzled
@@ -133,16 +130,24 @@ constexpr int kTOccPadLds = 0;
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
 
-// Linear tile order: blocks are dealt to the 8 XCDs round-robin, so give each
-// XCD a contiguous range of tiles, ordered with M fastest (the CUs of one XCD
-// then share weight strips in their L2).
+// Tile order: blocks are dealt to the 8 XCDs round-robin, so give each XCD a
+// contiguous range of a grouped tile order (the CUs of one XCD then share
+// operand strips in their L2).
+constexpr int kGroupM = 8;
 __device__ __forceinline__ void tile_coords(int b, int tiles_m, int tiles_n, int& tm, int& tn) {
     const int nt = tiles_m * tiles_n;
     const int xcd = b % 8, k = b / 8;
     const int per = nt / 8, rem = nt % 8;
     const int t = xcd < rem ? xcd * (per + 1) + k : rem * (per + 1) + (xcd - rem) * per + k;
-    tm = t % tiles_m;
-    tn = t / tiles_m;
+    // grouped order inside the range: bands of kGroupM tile rows, M fastest
+    // within a band, so the tiles an XCD holds at once form a near-square
+    // patch and share its L2 for both operands
+    const int band = t / (kGroupM * tiles_n);
+    const int first = band * kGroupM;
+    const int h = min(tiles_m - first, kGroupM);
+    const int r = t - band * kGroupM * tiles_n;
+    tm = first + r % h;
+    tn = r / h;
 }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
@@ -282,27 +287,26 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
     // one phase of a group: B fragments from `bt` (scales `sc`), A from xt
     auto phase = [&](const uint8_t* xt, const uint8_t* bt, const uint32_t* sc, auto is_res) {
         constexpr bool R = decltype(is_res)::value;
-        i32x4 blo[WN], bhi[WN], dummy[WN];
+        i32x8 b[WN], dummy[WN];
         float bs[WN], dscale[WN];
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
             const int row = wcol + 16 * j + lrow;
-            unpack_nibbles(*reinterpret_cast<const uint4*>(&bt[row * kRow + (swz(row, lq) << 4)]), blo[j], bhi[j]);
-            bs[j] = RAW ? 0.f : half_bits_to_float((uint16_t)sc[wcol + 16 * j + lrow]) * kUnscale;
-            dummy[j] = i32x4{0, 0, 0, 0};
+            b[j] = unfold_codes(*reinterpret_cast<const uint4*>(&bt[row * kRow + (swz(row, lq) << 4)]));
+            bs[j] = RAW ? 0.f : half_bits_to_float((uint16_t)sc[wcol + 16 * j + lrow]) * kCodeScale;
+            dummy[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0};
             dscale[j] = 0.f;
         }
 #pragma unroll
         for (int i = 0; i < WM; ++i) {
             const int row = wrow + 16 * i + lrow;
-            i32x4 alo, ahi;
-            unpack_nibbles(*reinterpret_cast<const uint4*>(&xt[row * kRow + (swz(row, lq) << 4)]), alo, ahi);
+            const i32x8 av = unfold_codes(*reinterpret_cast<const uint4*>(&xt[row * kRow + (swz(row, lq) << 4)]));
             // the residual phase feeds its fragments as the "base" operands of
             // group_row and accumulates into racc in raw mode
             if constexpr (R)
-                group_row<WN, RAW, false>(alo, ahi, blo, bhi, dummy, dummy, bs, dscale, acc[i], racc[i], racc[i]);
+                group_row<WN, RAW, false>(av, b, dummy, bs, dscale, acc[i], racc[i], racc[i]);
             else
-                group_row<WN, RAW, false>(alo, ahi, blo, bhi, dummy, dummy, bs, dscale, acc[i], iacc[i], racc[i]);
+                group_row<WN, RAW, false>(av, b, dummy, bs, dscale, acc[i], iacc[i], racc[i]);
         }
         // the phase's epilogue completes inside this block (see pin)
 #pragma unroll
@@ -452,20 +456,20 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
 
     if (gb < ge) load(gb);
     for (int g = gb; g < ge; ++g) {
-        i32x4 alo[WM], ahi[WM], wlo[WN], whi[WN], rlo[WN], rhi[WN];
+        i32x8 av[WM], wv[WN], rv[WN];
         float sw_f[WN], sr_f[WN];
         const int p = cur_p;
 #pragma unroll
-        for (int j = 0; j < WN; ++j) { rlo[j] = rhi[j] = i32x4{0, 0, 0, 0}; sw_f[j] = sr_f[j] = 0.f; }
+        for (int j = 0; j < WN; ++j) { rv[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0}; sw_f[j] = sr_f[j] = 0.f; }
 #pragma unroll
-        for (int i = 0; i < WM; ++i) unpack_nibbles(xpk[i], alo[i], ahi[i]);
+        for (int i = 0; i < WM; ++i) av[i] = unfold_codes(xpk[i]);
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
-            unpack_nibbles(wpk[j], wlo[j], whi[j]);
-            if constexpr (!RAW) sw_f[j] = half_bits_to_float(swb[j]) * kUnscale;
+            wv[j] = unfold_codes(wpk[j]);
+            if constexpr (!RAW) sw_f[j] = half_bits_to_float(swb[j]) * kCodeScale;
             if (p >= 0) {
-                unpack_nibbles(rpk[j], rlo[j], rhi[j]);
-                if constexpr (!RAW) sr_f[j] = half_bits_to_float(srb[j]) * kUnscale;
+                rv[j] = unfold_codes(rpk[j]);
+                if constexpr (!RAW) sr_f[j] = half_bits_to_float(srb[j]) * kCodeScale;
             }
         }
         if (g + 1 < ge) load(g + 1);
@@ -473,7 +477,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
             constexpr bool HR = decltype(has_res)::value;
 #pragma unroll
             for (int i = 0; i < WM; ++i)
-                group_row<WN, RAW, HR>(alo[i], ahi[i], wlo, whi, rlo, rhi, sw_f, sr_f, acc[i], iacc[i], racc[i]);
+                group_row<WN, RAW, HR>(av[i], wv, rv, sw_f, sr_f, acc[i], iacc[i], racc[i]);
         };
         if (p >= 0) tiles(std::true_type{});
         else tiles(std::false_type{});

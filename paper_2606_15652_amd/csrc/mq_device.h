@@ -42,26 +42,60 @@ __device__ __forceinline__ int quant_code(float x, float s) {
     return (int)r;
 }
 
-// ------------------------------------------------------------------ unpack --
-// 16 packed bytes (32 nibbles, elements 2j in low and 2j+1 in high nibbles)
-// -> two MFMA operands of 16 int8 each, holding 16 * code:
-//   lo = the even elements, hi = the odd elements (same byte positions).
-// Masking the high nibble in place yields 16 * (signed code) as an int8, and
-// shifting the low nibble up by 4 does the same for the even element, so the
-// integer products are 256x the code products; callers remove the factor.
-__device__ __forceinline__ void unpack_nibbles(const uint4 p, i32x4& lo, i32x4& hi) {
-    const uint32_t m = 0xF0F0F0F0u;
-    hi = i32x4{(int)(p.x & m), (int)(p.y & m), (int)(p.z & m), (int)(p.w & m)};
-    lo = i32x4{(int)((p.x << 4) & m), (int)((p.y << 4) & m),
-               (int)((p.z << 4) & m), (int)((p.w << 4) & m)};
+// ---------------------------------------------------------- packed codes --
+// Storage of 4-bit codes (q in [-7, 7]): a row of K codes is K/16 chunks of
+// 8 bytes, chunk c holding codes 16c .. 16c + 15.  Code e of a chunk is the
+// 6-bit field f = 32 [q < 0] + |q| at bit 6e of a 96-bit word (o0, o1, o2);
+// read as an fp6 e2m3 value a field with zero exponent is the subnormal
+// sign * |q| / 8, so a chunk expands into MFMA operand dwords with a mask per
+// word.  The two exponent bits of every field are zero, and those of o0 (kFoldA)
+// and of o1 (kFoldB) together are exactly the bits o2 can use, so the chunk is
+// stored folded as  P0 = o0 | (o2 & kFoldA),  P1 = o1 | (o2 & kFoldB).
+constexpr uint32_t kFoldA = 0x18618618u;   // bits 6e+3, 6e+4 inside word 0
+constexpr uint32_t kFoldB = 0x86186186u;   // bits 6e+3, 6e+4 inside word 1
+
+typedef int32_t i32x8 __attribute__((ext_vector_type(8)));
+
+// 16 codes -> one folded chunk (quantisers)
+__device__ __forceinline__ uint2 fold_codes(const int (&q)[16]) {
+    uint32_t o[3] = {0u, 0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const uint32_t f = (q[e] < 0 ? 32u : 0u) | (uint32_t)(q[e] < 0 ? -q[e] : q[e]);
+        const int bit = 6 * e, w = bit >> 5, off = bit & 31;
+        o[w] |= f << off;
+        if (off > 26) o[w + 1] |= f >> (32 - off);
+    }
+    return make_uint2(o[0] | (o[2] & kFoldA), o[1] | (o[2] & kFoldB));
 }
 
-// D = A(16x64 int8) * B(64x16 int8) + C, int32.  Lane l supplies row l%16 of A
-// and column l%16 of B for its quarter (l/16) of K; it receives
-// D[4*(l/16) + r][l%16], r = 0..3.
-__device__ __forceinline__ i32x4 mfma_i8(const i32x4 a, const i32x4 b, const i32x4 c) {
-    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+// code e (0..15) of a folded chunk
+__device__ __forceinline__ int chunk_code(uint32_t p0, uint32_t p1, int e) {
+    const uint32_t o[3] = {p0 & ~kFoldA, p1 & ~kFoldB, (p0 & kFoldA) | (p1 & kFoldB)};
+    const int bit = 6 * e, w = bit >> 5, off = bit & 31;
+    uint32_t f = o[w] >> off;
+    if (off > 26) f |= o[w + 1] << (32 - off);
+    const int mag = (int)(f & 7u);
+    return (f & 32u) ? -mag : mag;
 }
+
+// 16 bytes = two chunks (32 codes) -> the six e2m3 dwords of one MFMA lane
+// operand (dwords 6, 7 unused): 4 bit operations per chunk.
+__device__ __forceinline__ i32x8 unfold_codes(const uint4 p) {
+    return i32x8{(int)(p.x & ~kFoldA), (int)(p.y & ~kFoldB), (int)((p.x & kFoldA) | (p.y & kFoldB)),
+                 (int)(p.z & ~kFoldA), (int)(p.w & ~kFoldB), (int)((p.z & kFoldA) | (p.w & kFoldB)),
+                 0, 0};
+}
+
+// D = A (16 x 128) B^T + C in fp32 on e2m3 operands: lane l supplies row l%16
+// of A and of B for its quarter l/16 of K (32 codes, one 16-byte pair of
+// chunks) and receives D[4 * (l/16) + r][l%16], r = 0..3.  Products of codes
+// are exact and so is their sum: D = (sum of code products) / 64.
+__device__ __forceinline__ f32x4 mfma_codes(const i32x8 a, const i32x8 b, const f32x4 c) {
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 2, 2, 0, 0, 0, 0);
+}
+// removes the 1/64 of the e2m3 encoding (exact)
+constexpr float kCodeScale = 64.0f;
 
 __device__ __forceinline__ uint4 ldg16(const uint8_t* p) {
     return *reinterpret_cast<const uint4*>(p);

@@ -13,4 +13,4 @@ extern "C" const char* mq_status_string(mq_status s) {
     return "MQ_ERR_UNKNOWN";
 }
 
-extern "C" int mq_version(void) { return 100; }
+extern "C" int mq_version(void) { return 200; }

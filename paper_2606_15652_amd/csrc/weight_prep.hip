@@ -27,29 +27,23 @@ __global__ __launch_bounds__(256) void quant_base_kernel(
     const uint16_t sb = scale_bits_from_amax(amax);
     const float s = half_bits_to_float(sb);
     s_w[(int64_t)n * G + g] = sb;
-    uint4* dst = reinterpret_cast<uint4*>(Wq + (int64_t)n * (K / 2) + (int64_t)g * kGroupBytes);
-    for (int c = 0; c < kGroupBytes / 16; ++c) {   // 16 bytes = 32 elements
-        uint32_t words[4];
-        for (int w = 0; w < 4; ++w) {
-            uint32_t word = 0;
-            for (int b = 0; b < 4; ++b) {
-                const float4 v = src[c * 8 + w * 2 + b / 2];
-                const float e0 = (b & 1) ? v.z : v.x;
-                const float e1 = (b & 1) ? v.w : v.y;
-                const int q0 = s == 0.0f ? 0 : quant_code(e0, s);
-                const int q1 = s == 0.0f ? 0 : quant_code(e1, s);
-                word |= (((uint32_t)q0 & 0xFu) | (((uint32_t)q1 & 0xFu) << 4)) << (8 * b);
-            }
-            words[w] = word;
+    uint2* dst = reinterpret_cast<uint2*>(Wq + (int64_t)n * (K / 2) + (int64_t)g * kGroupBytes);
+    for (int c = 0; c < kGroup / 16; ++c) {   // one folded chunk per 16 elements
+        int q[16];
+        for (int i = 0; i < 4; ++i) {
+            const float4 v = src[c * 4 + i];
+            q[4 * i + 0] = s == 0.0f ? 0 : quant_code(v.x, s);
+            q[4 * i + 1] = s == 0.0f ? 0 : quant_code(v.y, s);
+            q[4 * i + 2] = s == 0.0f ? 0 : quant_code(v.z, s);
+            q[4 * i + 3] = s == 0.0f ? 0 : quant_code(v.w, s);
         }
-        dst[c] = make_uint4(words[0], words[1], words[2], words[3]);
+        dst[c] = fold_codes(q);
     }
 }
 
 __device__ __forceinline__ int code_at(const uint8_t* packed_row, int k) {
-    const int b = packed_row[k >> 1];
-    const int v = (k & 1) ? (b >> 4) : (b & 0xF);
-    return v >= 8 ? v - 16 : v;
+    const uint2 ch = reinterpret_cast<const uint2*>(packed_row)[k >> 4];
+    return chunk_code(ch.x, ch.y, k & 15);
 }
 
 // R = W - s q in fp32: s * q is exact (11-bit significand times |q| <= 8), so
@@ -245,13 +239,15 @@ __global__ __launch_bounds__(128) void quant_residual_kernel(
     const uint16_t srb = residual_row_scale(w, q, s);
     const float sr = half_bits_to_float(srb);
     s_r[(int64_t)p * kGroup + r] = srb;
-    uint8_t* dst = Rq + ((int64_t)p * kGroup + r) * kGroupBytes;
-    for (int j = 0; j < kGroupBytes; ++j) {
-        const float r0 = residual_at(w[2 * j], s, code_at(q, 2 * j));
-        const float r1 = residual_at(w[2 * j + 1], s, code_at(q, 2 * j + 1));
-        const int q0 = sr == 0.0f ? 0 : quant_code(r0, sr);
-        const int q1 = sr == 0.0f ? 0 : quant_code(r1, sr);
-        dst[j] = (uint8_t)(((uint32_t)q0 & 0xFu) | (((uint32_t)q1 & 0xFu) << 4));
+    uint2* dst = reinterpret_cast<uint2*>(Rq + ((int64_t)p * kGroup + r) * kGroupBytes);
+    for (int c = 0; c < kGroup / 16; ++c) {
+        int rq[16];
+        for (int e = 0; e < 16; ++e) {
+            const int k = 16 * c + e;
+            const float rv = residual_at(w[k], s, code_at(q, k));
+            rq[e] = sr == 0.0f ? 0 : quant_code(rv, sr);
+        }
+        dst[c] = fold_codes(rq);
     }
 }
 
