@@ -34,6 +34,13 @@
  *   the fp6 (e2m3) matrix instruction of CDNA4 with four bit operations per
  *   chunk; the paper fixes no bit layout (Section 4.2 fuses layout packing
  *   with quantisation).
+ * - Group order of packed rows (Xq [M rows], Wq [N rows]): a row's K/2 bytes
+ *   are K/128 pieces of 64 bytes (one 128-code group each), stored
+ *   group-major: piece (row r, group g) of a matrix of R rows sits at byte
+ *   (g R + r) 64.  Every 128-row x 128-code tile is then one contiguous run
+ *   of bytes, and the tiles of neighbouring row blocks are neighbours.
+ * - Weight scales s_w are stored [K/128][N]: s_w of (row n, group g) at
+ *   element g N + n.
  * - Packed operand pointers (Xq, Wq, Rq) must be 16-byte aligned; fp16
  *   pointers 2-byte aligned; int32 pointers 4-byte aligned; fp32/fp64 arrays
  *   naturally aligned.  Violations return MQ_ERR_MISALIGNED.
@@ -87,7 +94,7 @@ int mq_version(void);
  *     a = max_k |X[m,k]|,  s_x[m] = fp16_rn(fp32(a) / 7),
  *     Xq[m,k] = clamp(round_half_even(X[m,k] / s_x[m]), -7, 7)  (0 if s == 0)
  *   X   : fp16 [M, ldx] row-major, ldx >= K, ldx % 8 == 0, 16-byte aligned.
- *   Xq  : out, uint8 [M, K/2] packed codes (layout above).
+ *   Xq  : out, uint8 [M, K/2] packed codes in group order (layout above).
  *   s_x : out, fp16 [M].
  */
 mq_status mq_quantize_act(const void* X, int M, int K, int ldx,
@@ -103,8 +110,8 @@ size_t mq_fused_gemm_workspace_size(int M, int N, int K);
  *     A_b[m,n,g] = sum_{k in g} Xq[m,k] Wq[n,k]
  *     A_r[m,n,g] = sum_{k in g} Xq[m,k] Rq[p][n%128][k%128]   if (n/128,g) in S
  *     Y[m,n] = fp16( s_x[m] * sum_g ( s_w[n,g] A_b + s_r[p][n%128] A_r ) )
- *   Xq, s_x          : uint8 [M, K/2], fp16 [M]            (from mq_quantize_act)
- *   Wq, s_w          : uint8 [N, K/2], fp16 [N, K/128]
+ *   Xq, s_x          : uint8 [M, K/2] group order, fp16 [M] (from mq_quantize_act)
+ *   Wq, s_w          : uint8 [N, K/2] group order, fp16 [K/128, N]
  *   res_rowptr       : int32 [N/128 + 1], CSR over 128-row block rows;
  *                      res_rowptr[0] == 0, res_rowptr[N/128] == nnzb.
  *   res_kb           : int32 [nnzb], block column (group) of each selected
@@ -161,7 +168,7 @@ mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int K,
  *     R[n,k]   = W[n,k] - s_w[n,g] Wq[n,k]                    (fp32),
  *     score[nb,kb] = sum over the 128x128 block of R^2         (fp64).
  *   W     : fp32 [N, ldw], ldw >= K, ldw % 4 == 0, 16-byte aligned.
- *   Wq    : out, uint8 [N, K/2];  s_w : out, fp16 [N, K/128].
+ *   Wq    : out, uint8 [N, K/2] group order;  s_w : out, fp16 [K/128, N].
  *   score : out, fp64 [N/128, K/128] (may be NULL to skip scoring).
  */
 mq_status mq_quantize_weight(const float* W, int N, int K, int ldw,

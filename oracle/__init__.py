@@ -147,6 +147,43 @@ def pack_codes(codes: np.ndarray) -> np.ndarray:
     return out.reshape(*q.shape[:-1], q.shape[-1] // 2)
 
 
+# ------------------------------------------------------- device layout ----
+# The oracle works on row-major packed rows ([rows, K/2], row r's 64-byte
+# group pieces in K order) and row-major scales ([N, K/128]).  The GPU library
+# stores the same bytes group-major, so that every 128-row x 128-code tile is
+# one contiguous 8 KB run and the tiles of neighbouring row blocks are
+# neighbours in memory:
+#   packed rows: piece (row r, group g) at byte (g rows + r) 64;
+#   weight scales: s_w[n, g] at element g N + n.
+# These helpers are that permutation and its inverse (tests only).
+def block_rows(packed: np.ndarray, K: int) -> np.ndarray:
+    """Row-major packed rows [rows, K/2] -> device group-major order (same shape)."""
+    p = np.ascontiguousarray(packed, np.uint8).reshape(-1, K // 2)
+    rows, G = p.shape[0], K // BLOCK
+    return np.ascontiguousarray(p.reshape(rows, G, 64).transpose(1, 0, 2)).reshape(rows, K // 2)
+
+
+def unblock_rows(dev: np.ndarray, K: int) -> np.ndarray:
+    """Device group-major order -> row-major packed rows [rows, K/2]."""
+    d = np.ascontiguousarray(dev, np.uint8).reshape(-1, K // 2)
+    rows, G = d.shape[0], K // BLOCK
+    return np.ascontiguousarray(d.reshape(G, rows, 64).transpose(1, 0, 2)).reshape(rows, K // 2)
+
+
+def block_scales(s_w: np.ndarray) -> np.ndarray:
+    """Row-major weight scales [N, K/128] -> device order [K/128, N]
+    (returned with shape [N, K/128])."""
+    s = np.ascontiguousarray(s_w)
+    N, G = s.shape
+    return np.ascontiguousarray(s.T).reshape(N, G)
+
+
+def unblock_scales(dev: np.ndarray) -> np.ndarray:
+    d = np.ascontiguousarray(dev)
+    N, G = d.shape
+    return np.ascontiguousarray(d.reshape(G, N).T)
+
+
 # ------------------------------------------------------- quantisation ----
 def quantize_act(X: np.ndarray):
     """Per-token INT4 of fp16 X [M, K] -> (Xq uint8 [M, K/2], s_x bits [M])."""

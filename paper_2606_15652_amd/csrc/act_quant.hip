@@ -8,8 +8,8 @@
 // values), reduced across the wave with xor-shuffles and across the four waves
 // through LDS.  Codes are then formed from the registers (rows up to
 // CPT * 4096 elements) or by re-reading the row (longer rows), and written as
-// one folded 8-byte chunk per 16 codes (fold_codes): coalesced 16-byte loads,
-// 8-byte stores.
+// one folded 8-byte chunk per 16 codes (fold_codes) in the device group order
+// (piece_offset): coalesced 16-byte loads, 8-byte stores.
 #include "mq_device.h"
 
 namespace mq {
@@ -45,14 +45,17 @@ __device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, flo
 // row is read twice.
 template <int CPT>
 __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
-    const uint16_t* __restrict__ X, int K, int ldx,
+    const uint16_t* __restrict__ X, int M, int K, int ldx,
     uint8_t* __restrict__ Xq, uint16_t* __restrict__ s_x) {
     __shared__ uint32_t red[kActThreads / 64];
     const int m = blockIdx.x;
     const int t = threadIdx.x;
     const uint16_t* row = X + (int64_t)m * ldx;
-    uint2* out = reinterpret_cast<uint2*>(Xq + (int64_t)m * (K / 2));
     const int nchunks = K / 16;
+    // chunk c (codes 16c .. 16c+15) is chunk c % 8 of the piece of group c / 8
+    auto out = [&](int c) -> uint2& {
+        return *reinterpret_cast<uint2*>(Xq + piece_offset(M, m, c >> 3) + (c & 7) * 8);
+    };
 
     uint32_t amax = 0;
     uint4 v[CPT > 0 ? CPT : 1][2];
@@ -91,11 +94,11 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
 #pragma unroll
         for (int i = 0; i < CPT; ++i) {
             const int c = t + i * kActThreads;
-            if (c < nchunks) out[c] = quant_chunk(v[i][0], v[i][1], s);
+            if (c < nchunks) out(c) = quant_chunk(v[i][0], v[i][1], s);
         }
     } else {
         for (int c = t; c < nchunks; c += kActThreads)
-            out[c] = quant_chunk(*reinterpret_cast<const uint4*>(row + 16 * c),
+            out(c) = quant_chunk(*reinterpret_cast<const uint4*>(row + 16 * c),
                                  *reinterpret_cast<const uint4*>(row + 16 * c + 8), s);
     }
 }
@@ -118,16 +121,16 @@ extern "C" mq_status mq_quantize_act(const void* X, int M, int K, int ldx,
     const int chunks_per_thread = (K / 16 + kActThreads - 1) / kActThreads;
     dim3 grid(M), block(kActThreads);
     if (chunks_per_thread <= 1)
-        hipLaunchKernelGGL(act_quant_kernel<1>, grid, block, 0, stream, x, K, ldx, Xq, s);
+        hipLaunchKernelGGL(act_quant_kernel<1>, grid, block, 0, stream, x, M, K, ldx, Xq, s);
     else if (chunks_per_thread <= 2)
-        hipLaunchKernelGGL(act_quant_kernel<2>, grid, block, 0, stream, x, K, ldx, Xq, s);
+        hipLaunchKernelGGL(act_quant_kernel<2>, grid, block, 0, stream, x, M, K, ldx, Xq, s);
     else if (chunks_per_thread <= 4)
-        hipLaunchKernelGGL(act_quant_kernel<4>, grid, block, 0, stream, x, K, ldx, Xq, s);
+        hipLaunchKernelGGL(act_quant_kernel<4>, grid, block, 0, stream, x, M, K, ldx, Xq, s);
     else if (chunks_per_thread <= 8)
-        hipLaunchKernelGGL(act_quant_kernel<8>, grid, block, 0, stream, x, K, ldx, Xq, s);
+        hipLaunchKernelGGL(act_quant_kernel<8>, grid, block, 0, stream, x, M, K, ldx, Xq, s);
     else if (chunks_per_thread <= 16)
-        hipLaunchKernelGGL(act_quant_kernel<16>, grid, block, 0, stream, x, K, ldx, Xq, s);
+        hipLaunchKernelGGL(act_quant_kernel<16>, grid, block, 0, stream, x, M, K, ldx, Xq, s);
     else
-        hipLaunchKernelGGL(act_quant_kernel<0>, grid, block, 0, stream, x, K, ldx, Xq, s);
+        hipLaunchKernelGGL(act_quant_kernel<0>, grid, block, 0, stream, x, M, K, ldx, Xq, s);
     return mq_host::launch_status();
 }

@@ -111,10 +111,10 @@ __device__ __forceinline__ void group_row(const i32x8 a, const i32x8 (&w)[WN], c
 // at iteration g the waves wait for group g's loads, meet at the barrier that
 // also frees the slot of group g-1, issue group g+2 into it and compute g.
 // The DMA does not raise the compiler's wait counters, so the kernel waits on
-// the vector-memory counter itself (sync_group).
+// the vector-memory counter itself (wait_loads_and_sync).
 //
-// Loads use per-tile buffer resources (scalar base at the tile's first row,
-// 32-bit offsets; rows past M read as zero).  16-byte chunks are XOR-swizzled
+// Loads use per-tile buffer resources over operands in device group order, so
+// each load instruction reads 1 KB of whole 64-byte rows, contiguous.  16-byte chunks are XOR-swizzled
 // by (row >> 1) & 3 inside 64-byte rows, which makes the 16-lane fragment
 // reads conflict-free (LDS serves 8 lanes of 16 B per 128-byte bank window).
 //
@@ -162,14 +162,43 @@ __device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t voff
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef __attribute__((address_space(4))) int32_t cint32_t;   // read-only (scalar-loadable) int32
 
-// 16 bytes per lane, buffer -> LDS: lane l's bytes land at dst + 16 l.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t voff, uint32_t soff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 16, voff, soff, 0, 0);
+// LDS DMA (buffer loads that write LDS, lane l's bytes at dst + size * l),
+// issued from inline assembly so that the compiler does not track them: its
+// wait-count pass would otherwise make every later LDS read wait for all of
+// them, including the prefetches of later groups.  The kernel waits for them
+// itself (wait_loads_and_sync), before the barrier that publishes a stage.
+// The compiler's own vector-memory waits stay correct: loads return in order,
+// so loads it does not know of can only make its waits longer.
+// Buffer descriptor words: base[31:0]; base[47:32] (stride 0); byte size;
+// raw-buffer flags.
+__device__ __forceinline__ i32x4 buf_desc(const void* base, uint32_t bytes) {
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    return i32x4{(int)(uint32_t)b, (int)((uint32_t)(b >> 32) & 0xFFFFu), (int)bytes, 0x00020000};
 }
-// 2 bytes per lane, buffer -> LDS: lane l's value lands zero-extended in the
-// dword at dst + 4 l.
-__device__ __forceinline__ void dma2(__amdgpu_buffer_rsrc_t r, void* dst, uint32_t voff, uint32_t soff) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 2, voff, soff, 0, 0);
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return (uint32_t)(uintptr_t)(lds_ptr_t)p;
+}
+__device__ __forceinline__ void dma16(const i32x4 desc, const void* dst, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(lds_addr(dst)), "v"(voff), "s"(desc) : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const i32x4 desc, const void* dst, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :: "s"(lds_addr(dst)), "v"(voff), "s"(desc) : "memory", "m0");
+}
+
+// Waits until at most n of this wave's vector-memory loads are in flight (the
+// LDS DMA does not raise the compiler's own waits), then meets the other waves
+// of the workgroup.  s_waitcnt takes an immediate, hence one case per count a
+// wave can leave in flight; any other n waits for everything.
+__device__ __forceinline__ void wait_loads_and_sync(int n) {
+    switch (n) {
+        case 4: asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
+        case 5: asm volatile("s_waitcnt vmcnt(5) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
+        case 6: asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
+        case 7: asm volatile("s_waitcnt vmcnt(7) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
+    }
 }
 
 template <bool RAW, bool SPLIT>
@@ -181,14 +210,12 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
     constexpr int kStages = 3;
     struct Slot {
         uint8_t x[kTile], w[kTile], r[kTile];
-        uint32_t sw[kTB], sr[kTB];                          // fp16 scales, zero-extended
+        uint32_t sw[kTB / 2], sr[kTB / 2];                  // fp16 scales, two per dword
     };
     __shared__ __attribute__((aligned(16))) Slot ring[kStages];
-    __shared__ int pres[kStages];
 
     const int M = a.M, N = a.N, K = a.K;
     const int G = K / kGroup;
-    const uint32_t ldk = (uint32_t)(K / 2);
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -201,13 +228,13 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
     const int gb = SPLIT ? blockIdx.y * groups_per_split : 0;
     const int ge = SPLIT ? min(G, gb + groups_per_split) : G;
 
-    // per-tile buffer resources (rows past M read as zero)
+    // Operands in device group order: the group-g tile of X rows m0.. is
+    // xrows * 64 contiguous bytes at (g M + m0) 64, that of W rows n0.. 8 KB at
+    // (g N + n0) 64, and R block p is 8 KB.  Every tile load goes through a
+    // resource spanning exactly that tile (offsets in the vector operand
+    // only), so X rows past xrows fail the range check and read zero.
     const uint32_t xrows = (uint32_t)min(kTB, M - m0);
-    const __amdgpu_buffer_rsrc_t xr = make_rsrc(a.Xq + (int64_t)m0 * ldk, xrows * ldk);
-    const __amdgpu_buffer_rsrc_t wr = make_rsrc(a.Wq + (int64_t)n0 * ldk, (uint32_t)kTB * ldk);
-    // zero-length resource on a valid base: every load through it returns
-    // zero without touching memory (absent residual blocks)
-    const __amdgpu_buffer_rsrc_t nullr = make_rsrc(a.Wq, 0);
+    const uint32_t xbytes = xrows * (uint32_t)kRow;
 
     // residual walk of the tile's block row, from the first entry at or after
     // gb.  The CSR is read through the constant address space so the walk stays
@@ -224,52 +251,50 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
 
     // DMA lane mapping: wave w fills 1 KB blocks 2w and 2w + 1 of each 8 KB
     // tile (16 rows each); lane l takes row 16 b + l / 4 and physical chunk
-    // l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row.
-    uint32_t vrow[2], vres[2];
+    // l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row.  Each load
+    // instruction reads 1 KB of whole 64-byte rows, contiguous in memory.
+    uint32_t vt[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int row = 16 * (2 * wave + i) + (lane >> 2);
         const int c = (lane & 3) ^ ((row >> 1) & 3);
-        vrow[i] = (uint32_t)row * ldk + c * 16;
-        vres[i] = (uint32_t)row * kRow + c * 16;
+        vt[i] = (uint32_t)row * kRow + c * 16;
     }
-    // scales: waves 0, 1 fetch s_w of rows 64 w + lane; waves 2, 3 fetch s_r
-    const __amdgpu_buffer_rsrc_t swr = make_rsrc(a.s_w, RAW ? 0u : (uint32_t)((int64_t)N * G * 2));
-    const uint32_t vsw = (uint32_t)(n0 + 64 * (wave & 1) + lane) * (uint32_t)G * 2;
-    constexpr int kLoadsPerStage = RAW ? 6 : 7;             // DMA instructions per wave per group
 
-    auto issue = [&](int g, int slot) {
+    // Loads of group g into `slot`; returns the number of vector-memory loads
+    // this wave issued and sets p to the group's residual block (or -1).
+    // Wave 0 also fetches the tile's 128 weight scales (256 B), wave 1 the
+    // residual block's 128 scales.
+    auto issue = [&](int g, int slot, int& p) -> int {
         Slot& S = ring[slot];
-        const uint32_t so = (uint32_t)g * kGroupBytes;
-        dma16(xr, &S.x[(2 * wave) * 1024], vrow[0], so);
-        dma16(xr, &S.x[(2 * wave + 1) * 1024], vrow[1], so);
-        dma16(wr, &S.w[(2 * wave) * 1024], vrow[0], so);
-        dma16(wr, &S.w[(2 * wave + 1) * 1024], vrow[1], so);
-        int p = -1;
-        if (rp < re && res_kb[rp] == g) p = rp++;
-        const __amdgpu_buffer_rsrc_t rr = p >= 0 ? make_rsrc(a.Rq + (int64_t)p * kTile, (uint32_t)kTile) : nullr;
-        dma16(rr, &S.r[(2 * wave) * 1024], vres[0], 0);
-        dma16(rr, &S.r[(2 * wave + 1) * 1024], vres[1], 0);
+        const i32x4 xr = buf_desc(a.Xq + piece_offset(M, m0, g), xbytes);
+        const i32x4 wr = buf_desc(a.Wq + piece_offset(N, n0, g), (uint32_t)kTile);
+        dma16(xr, &S.x[(2 * wave) * 1024], vt[0]);
+        dma16(xr, &S.x[(2 * wave + 1) * 1024], vt[1]);
+        dma16(wr, &S.w[(2 * wave) * 1024], vt[0]);
+        dma16(wr, &S.w[(2 * wave + 1) * 1024], vt[1]);
+        int n = 4;
         if constexpr (!RAW) {
-            if (wave < 2) {
-                dma2(swr, &S.sw[64 * wave], vsw, (uint32_t)g * 2);
-            } else {
-                const __amdgpu_buffer_rsrc_t srr =
-                    p >= 0 ? make_rsrc(a.s_r + (int64_t)p * kTB, (uint32_t)kTB * 2) : nullr;
-                dma2(srr, &S.sr[64 * (wave - 2)], (uint32_t)(64 * (wave - 2) + lane) * 2, 0);
+            if (wave == 0) {
+                dma4(buf_desc(a.s_w + wscale_index(N, n0, g), kTB * 2), S.sw, (uint32_t)lane * 4);
+                ++n;
             }
         }
-        if (t == 0) pres[slot] = p;
-    };
-    // wait until this wave's loads of the group about to be computed have
-    // landed (the next group's may stay in flight), then synchronise
-    auto sync_group = [&](bool next_in_flight) {
-        if (next_in_flight) {
-            if constexpr (kLoadsPerStage == 7) asm volatile("s_waitcnt vmcnt(7) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-            else asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        } else {
-            asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        p = -1;
+        if (rp < re && res_kb[rp] == g) p = rp++;
+        if (p >= 0) {
+            const i32x4 rr = buf_desc(a.Rq + (int64_t)p * kTile, (uint32_t)kTile);
+            dma16(rr, &S.r[(2 * wave) * 1024], vt[0]);
+            dma16(rr, &S.r[(2 * wave + 1) * 1024], vt[1]);
+            n += 2;
+            if constexpr (!RAW) {
+                if (wave == 1) {
+                    dma4(buf_desc(a.s_r + (int64_t)p * kTB, kTB * 2), S.sr, (uint32_t)lane * 4);
+                    ++n;
+                }
+            }
         }
+        return n;
     };
 
     f32x4 acc[WM][WN];
@@ -293,7 +318,7 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
         for (int j = 0; j < WN; ++j) {
             const int row = wcol + 16 * j + lrow;
             b[j] = unfold_codes(*reinterpret_cast<const uint4*>(&bt[row * kRow + (swz(row, lq) << 4)]));
-            bs[j] = RAW ? 0.f : half_bits_to_float((uint16_t)sc[wcol + 16 * j + lrow]) * kCodeScale;
+            bs[j] = RAW ? 0.f : half_bits_to_float(reinterpret_cast<const uint16_t*>(sc)[wcol + 16 * j + lrow]) * kCodeScale;
             dummy[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0};
             dscale[j] = 0.f;
         }
@@ -319,17 +344,25 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
             }
     };
 
-    if (gb < ge) issue(gb, 0);
-    if (gb + 1 < ge) issue(gb + 1, 1);
+    // (loads in flight, residual block) of the groups one and two ahead
+    int p_cur = -1, p_next = -1, n_next = 0;
+    if (gb < ge) issue(gb, 0, p_cur);
+    if (gb + 1 < ge) n_next = issue(gb + 1, 1, p_next);
+    int slot = 0;
     for (int g = gb; g < ge; ++g) {
-        const int slot = (g - gb) % kStages;
-        // group g landed for everyone; everyone finished group g - 1, whose
-        // slot (g + 2) % 3 is refilled next
-        sync_group(g + 1 < ge);
-        if (g + 2 < ge) issue(g + 2, (g + 2 - gb) % kStages);
+        // group g landed for everyone (group g + 1's loads may stay in
+        // flight); everyone finished group g - 1, whose slot is refilled next
+        wait_loads_and_sync(g + 1 < ge ? n_next : 0);
+        int p_new = -1, n_new = 0;
+        const int slot2 = slot == 0 ? 2 : slot - 1;
+        if (g + 2 < ge) n_new = issue(g + 2, slot2, p_new);
         const Slot& S = ring[slot];
         phase(S.x, S.w, S.sw, std::false_type{});
-        if (pres[slot] >= 0) phase(S.x, S.r, S.sr, std::true_type{});
+        if (p_cur >= 0) phase(S.x, S.r, S.sr, std::true_type{});
+        p_cur = p_next;
+        p_next = p_new;
+        n_next = n_new;
+        slot = slot == 2 ? 0 : slot + 1;
     }
 
     // epilogue: lane holds rows 4 * (lane / 16) + r of each sub-tile, column lane % 16
@@ -395,7 +428,6 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n0 = blockIdx.x * 16 * WN;
-    const int64_t ldk = K / 2;
     const int lrow = lane & 15, lq = lane >> 4;
 
     // contiguous run of groups for this wave
@@ -413,8 +445,6 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
     }
     const int rrow0 = n0 % 128;
 
-    const uint8_t* wbase = a.Wq + (int64_t)(n0 + lrow) * ldk + lq * 16;
-    const uint16_t* swbase = a.s_w + (int64_t)(n0 + lrow) * G;
 
     f32x4 acc[WM][WN];
     i32x4 iacc[WM][WN], racc[WM][WN];
@@ -435,12 +465,13 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
         for (int i = 0; i < WM; ++i) {
             const int row = i * 16 + lrow;
             xpk[i] = make_uint4(0, 0, 0, 0);
-            if (row < M) xpk[i] = ldg16(a.Xq + (int64_t)row * ldk + (int64_t)g * kGroupBytes + lq * 16);
+            if (row < M) xpk[i] = ldg16(a.Xq + piece_offset(M, row, g) + lq * 16);
         }
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
-            wpk[j] = ldg16(wbase + (int64_t)j * 16 * ldk + (int64_t)g * kGroupBytes);
-            if constexpr (!RAW) swb[j] = swbase[(int64_t)j * 16 * G + g];
+            const int n = n0 + 16 * j + lrow;
+            wpk[j] = ldg16(a.Wq + piece_offset(N, n, g) + lq * 16);
+            if constexpr (!RAW) swb[j] = a.s_w[wscale_index(N, n, g)];
         }
         cur_p = -1;
         if (rp < rend && a.res_kb[rp] == g) {

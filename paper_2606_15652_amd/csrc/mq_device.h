@@ -97,6 +97,19 @@ __device__ __forceinline__ f32x4 mfma_codes(const i32x8 a, const i32x8 b, const 
 // removes the 1/64 of the e2m3 encoding (exact)
 constexpr float kCodeScale = 64.0f;
 
+// ----------------------------------------------------- device group order --
+// Packed rows (Xq, Wq) are stored group-major: the 64-byte piece of row r and
+// 128-code group g sits at byte (g rows + r) 64, so every 128-row x 128-code
+// tile is one contiguous run and the tiles of neighbouring row blocks are
+// neighbours in memory.  Weight scales are stored [K/128][N]: s_w of (row n,
+// group g) at element g N + n, 256 contiguous bytes per tile.
+__device__ __forceinline__ int64_t piece_offset(int rows, int r, int g) {
+    return ((int64_t)g * rows + r) * kGroupBytes;
+}
+__device__ __forceinline__ int64_t wscale_index(int N, int n, int g) {
+    return (int64_t)g * N + n;
+}
+
 __device__ __forceinline__ uint4 ldg16(const uint8_t* p) {
     return *reinterpret_cast<const uint4*>(p);
 }

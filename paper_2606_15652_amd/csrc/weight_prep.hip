@@ -26,8 +26,8 @@ __global__ __launch_bounds__(256) void quant_base_kernel(
     }
     const uint16_t sb = scale_bits_from_amax(amax);
     const float s = half_bits_to_float(sb);
-    s_w[(int64_t)n * G + g] = sb;
-    uint2* dst = reinterpret_cast<uint2*>(Wq + (int64_t)n * (K / 2) + (int64_t)g * kGroupBytes);
+    s_w[wscale_index(N, n, g)] = sb;
+    uint2* dst = reinterpret_cast<uint2*>(Wq + piece_offset(N, n, g));
     for (int c = 0; c < kGroup / 16; ++c) {   // one folded chunk per 16 elements
         int q[16];
         for (int i = 0; i < 4; ++i) {
@@ -68,8 +68,8 @@ __global__ __launch_bounds__(128) void score_frob_kernel(
     const int r = threadIdx.x;
     const int n = nb * kGroup + r;
     const float* w = W + (int64_t)n * ldw + (int64_t)kb * kGroup;
-    const uint8_t* q = Wq + (int64_t)n * (K / 2) + (int64_t)kb * kGroupBytes;
-    const float s = half_bits_to_float(s_w[(int64_t)n * G + kb]);
+    const uint8_t* q = Wq + piece_offset(N, n, kb);
+    const float s = half_bits_to_float(s_w[wscale_index(N, n, kb)]);
     double acc = 0.0;
     for (int c = 0; c < kGroup; ++c) {
         const double rv = residual_at(w[c], s, code_at(q, c));
@@ -121,8 +121,8 @@ __global__ __launch_bounds__(128) void score_dhessian_kernel(
     const int r = threadIdx.x;
     const int n = nb * kGroup + r;
     const float* w = W + (int64_t)n * ldw + (int64_t)kb * kGroup;
-    const uint8_t* q = Wq + (int64_t)n * (K / 2) + (int64_t)kb * kGroupBytes;
-    const float s = half_bits_to_float(s_w[(int64_t)n * G + kb]);
+    const uint8_t* q = Wq + piece_offset(N, n, kb);
+    const float s = half_bits_to_float(s_w[wscale_index(N, n, kb)]);
     const uint16_t srb = residual_row_scale(w, q, s);
     const float sr = half_bits_to_float(srb);
     double before = 0.0, after = 0.0;
@@ -234,8 +234,8 @@ __global__ __launch_bounds__(128) void quant_residual_kernel(
     const int r = threadIdx.x;
     const int n = nb * kGroup + r;
     const float* w = W + (int64_t)n * ldw + (int64_t)kb * kGroup;
-    const uint8_t* q = Wq + (int64_t)n * (K / 2) + (int64_t)kb * kGroupBytes;
-    const float s = half_bits_to_float(s_w[(int64_t)n * G + kb]);
+    const uint8_t* q = Wq + piece_offset(N, n, kb);
+    const float s = half_bits_to_float(s_w[wscale_index(N, n, kb)]);
     const uint16_t srb = residual_row_scale(w, q, s);
     const float sr = half_bits_to_float(srb);
     s_r[(int64_t)p * kGroup + r] = srb;

@@ -16,6 +16,7 @@ import sys
 import numpy as np
 import pytest
 
+import oracle as layout    # the device group order, as a permutation of the oracle's row-major packing
 import synth
 
 pytestmark = pytest.mark.gpu
@@ -96,9 +97,15 @@ def orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r):
     return orc.PackedWeight(N, K, Wq, s_w, rowptr, kb, Rq, s_r, None, sel)
 
 
+def dev_x(tc, Xq):
+    """Row-major packed activations -> the library's group order on the GPU."""
+    return dev(tc, layout.block_rows(Xq, Xq.shape[1] * 2))
+
+
 def gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r):
     import torch
-    return mq.PackedWeight(N, K, dev(tc, Wq), dev(tc, s_w).view(torch.float16),
+    return mq.PackedWeight(N, K, dev(tc, layout.block_rows(Wq, K)),
+                           dev(tc, layout.block_scales(s_w)).view(torch.float16),
                            dev(tc, rowptr), dev(tc, kb),
                            dev(tc, Rq), dev(tc, s_r).view(torch.float16))
 
@@ -123,7 +130,7 @@ def test_act_quant_parity(tc, mq, orc, M, K):
     Xq, s_x = mq.quantize_act(dev(tc, X))
     Xq_ref, sx_ref = orc.quantize_act(X)
     assert np.array_equal(half_bits(s_x), sx_ref)
-    assert np.array_equal(host(Xq), Xq_ref)
+    assert np.array_equal(orc.unblock_rows(host(Xq), K), Xq_ref)
 
 
 def test_act_quant_strided(tc, mq, orc):
@@ -138,7 +145,8 @@ def test_act_quant_strided(tc, mq, orc):
     tc.cuda.synchronize()
     assert st == 0
     Xq_ref, sx_ref = orc.quantize_act(X)
-    assert np.array_equal(host(Xq), Xq_ref) and np.array_equal(half_bits(s_x), sx_ref)
+    assert np.array_equal(orc.unblock_rows(host(Xq), 640), Xq_ref)
+    assert np.array_equal(half_bits(s_x), sx_ref)
 
 
 # ------------------------------------------------------- weight prep -------
@@ -152,8 +160,8 @@ def check_prep(tc, mq, orc, W, nnzb, criterion="frob", Xc=None):
                            X_calib=None if Xc is None else dev(tc, Xc))
     ref = orc.prepare_weight(W, nnzb, criterion=criterion, X_calib=Xc)
     tc.cuda.synchronize()
-    assert np.array_equal(host(pw.Wq), ref.Wq)
-    assert np.array_equal(half_bits(pw.s_w), ref.s_w)
+    assert np.array_equal(orc.unblock_rows(host(pw.Wq), W.shape[1]), ref.Wq)
+    assert np.array_equal(orc.unblock_scales(half_bits(pw.s_w)), ref.s_w)
     sc = host(pw.score)
     assert np.allclose(sc, ref.score, rtol=1e-12, atol=1e-300)
     # selection: exact unless two scores closer than the comparison tolerance
@@ -216,7 +224,7 @@ def test_gemm_parity_random_codes(tc, mq, orc, M, N, K, nnzb):
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = ops
     Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
-    Xq_d, sx_d = dev(tc, Xq), dev(tc, s_x).view(tc.float16)
+    Xq_d, sx_d = dev_x(tc, Xq), dev(tc, s_x).view(tc.float16)
     for v in _variants(M):
         Tb, Tr = mq.fused_gemm_acc_i32(Xq_d, pw, variant=v)
         Y = mq.fused_gemm(Xq_d, sx_d, pw, variant=v)
@@ -264,8 +272,8 @@ def test_gemm_extreme_codes_long_k(tc, mq, orc):
     assert np.abs(Tb_ref).max() == 49 * K
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
     for v in ("skinny", "tiled"):
-        Tb, Tr = mq.fused_gemm_acc_i32(dev(tc, Xq), pw, variant=v)
-        Y = mq.fused_gemm(dev(tc, Xq), dev(tc, s_x).view(tc.float16), pw, variant=v)
+        Tb, Tr = mq.fused_gemm_acc_i32(dev_x(tc, Xq), pw, variant=v)
+        Y = mq.fused_gemm(dev_x(tc, Xq), dev(tc, s_x).view(tc.float16), pw, variant=v)
         tc.cuda.synchronize()
         assert np.array_equal(host(Tb), Tb_ref) and np.array_equal(host(Tr), Tr_ref), v
         assert maxabsrel(Y, Y64) <= TIGHT, v
@@ -277,7 +285,7 @@ def test_gemm_guard_bands_and_empty(tc, mq, orc):
     ops = random_operands(M, N, K, nnzb, seed=5)
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = ops
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
-    Xq_d, sx_d = dev(tc, Xq), dev(tc, s_x)          # kept alive across the launches
+    Xq_d, sx_d = dev_x(tc, Xq), dev(tc, s_x)        # kept alive across the launches
     lib = mq.load()
     for v in (1, 2):
         if v == 1 and M > 32:
@@ -308,7 +316,8 @@ def test_gemm_no_residual_null_pointers(tc, mq, orc):
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, 0, seed=9)
     Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
     Y = tc.empty((M, N), dtype=tc.float16, device="cuda")
-    keep = [dev(tc, a) for a in (Xq, s_x, Wq, s_w)]       # kept alive across the launches
+    keep = [dev_x(tc, Xq), dev(tc, s_x), dev(tc, layout.block_rows(Wq, K)),
+            dev(tc, layout.block_scales(s_w))]               # kept alive across the launches
     lib = mq.load()
     for v in (1, 2):
         st = lib.mq_fused_gemm_variant(v, M, N, K, *[t.data_ptr() for t in keep], None, None, 0,
@@ -323,14 +332,15 @@ def test_gemm_deterministic_and_row_independent(tc, mq, orc):
     M, N, K, nnzb = 48, 512, 1024, 6
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=21)
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
-    Xd, sd = dev(tc, Xq), dev(tc, s_x).view(tc.float16)
+    sd = dev(tc, s_x).view(tc.float16)
     for v in ("tiled", "skinny"):
-        rows = slice(0, M) if v == "tiled" else slice(0, 16)
-        Y1 = host(mq.fused_gemm(Xd[rows].contiguous(), sd[rows].contiguous(), pw, variant=v).view(tc.int16))
-        Y2 = host(mq.fused_gemm(Xd[rows].contiguous(), sd[rows].contiguous(), pw, variant=v).view(tc.int16))
+        rows = M if v == "tiled" else 16
+        Xd = dev_x(tc, Xq[:rows])
+        Y1 = host(mq.fused_gemm(Xd, sd[:rows].contiguous(), pw, variant=v).view(tc.int16))
+        Y2 = host(mq.fused_gemm(Xd, sd[:rows].contiguous(), pw, variant=v).view(tc.int16))
         assert np.array_equal(Y1, Y2)
         for m in (0, 5, 15):
-            Ym = host(mq.fused_gemm(Xd[m:m + 1].contiguous(), sd[m:m + 1].contiguous(), pw,
+            Ym = host(mq.fused_gemm(dev_x(tc, Xq[m:m + 1]), sd[m:m + 1].contiguous(), pw,
                                     variant=v).view(tc.int16))
             assert np.array_equal(Ym[0], Y1[m]), (v, m)
 
@@ -347,8 +357,8 @@ def _prepared(tc, mq, orc, layer):
         ref = orc.prepare_weight(W, layer.nnzb)
         pw = mq.prepare_weight(dev(tc, W), layer.nnzb)
         tc.cuda.synchronize()
-        assert np.array_equal(host(pw.Wq), ref.Wq)
-        assert np.array_equal(half_bits(pw.s_w), ref.s_w)
+        assert np.array_equal(orc.unblock_rows(host(pw.Wq), layer.K), ref.Wq)
+        assert np.array_equal(orc.unblock_scales(half_bits(pw.s_w)), ref.s_w)
         assert np.array_equal(host(pw.rowptr), ref.rowptr) and np.array_equal(host(pw.kb), ref.kb)
         assert np.array_equal(host(pw.Rq), ref.Rq) and np.array_equal(half_bits(pw.s_r), ref.s_r)
         des = layer.designated()
@@ -386,7 +396,8 @@ def test_full_size_sampled(tc, mq, orc, name, M):
     Xd = dev(tc, X)
     Xq, s_x = mq.quantize_act(Xd)
     Xq_ref, sx_ref = orc.quantize_act(X)
-    assert np.array_equal(host(Xq), Xq_ref) and np.array_equal(half_bits(s_x), sx_ref)
+    assert np.array_equal(orc.unblock_rows(host(Xq), layer.K), Xq_ref)
+    assert np.array_equal(half_bits(s_x), sx_ref)
     rng = np.random.default_rng(M + layer.seed)
     ms, ns = _samples(M, layer.N, ref.rowptr, rng)
     tb_ref, tr_ref, y64 = orc.linear_sampled(Xq_ref, sx_ref, ref, ms, ns)
