@@ -8,17 +8,20 @@ outliers, base INT4 with group-128 fp16 scales, 10 % of the 128x128 blocks
 N(0,1) with 4 channels x30 -- swept over M = 1, 16, 256, 4096 tokens.
 
 One step = the whole hot path at every M of the sweep: per-token activation
-quantisation (mq_quantize_act) then the fused GEMM (mq_fused_gemm).  Inputs
+quantisation and the fused GEMM, called as one layer (mq_linear: a single
+kernel at decode sizes, mq_quantize_act then mq_fused_gemm otherwise).  Inputs
 are resident in HBM before timing; every call of a step reads its own copy of
 the packed weights, rotating through more than 512 MB of copies so that the
 256 MB last-level cache cannot serve weights from an earlier call.
 
 value = effective TOPS of a step = sum_M 2*M*N*K / step time (the residual
 MACs are extra work, not counted in "effective").  Per-M rows report
-microseconds per call, effective TOPS, the fraction of the INT8 MFMA peak
-(algorithmic ops including residual) and of HBM bandwidth (algorithmic
-bytes), and hipBLASLt W16A16 (torch.nn.functional.linear, fp16) timed the
-same way on the same shapes with rotating weights.
+microseconds per layer call (us_call, mq_linear) and, separately, of the
+fused GEMM alone on quantised input (us_gemm) and of the quantiser alone
+(us_quant); effective TOPS, the fraction of the INT8 MFMA peak (algorithmic
+ops including residual) and of HBM bandwidth (algorithmic bytes) of the GEMM;
+and hipBLASLt W16A16 (torch.nn.functional.linear, fp16) timed the same way on
+the same shapes with rotating weights, compared with us_call.
 
 All timing replays HIP graphs (captured with torch.cuda.graph, which the
 binding follows because it launches on torch's current stream), so host-side
@@ -173,6 +176,7 @@ def main():
     Xqs = {m: torch.empty((m, K // 2), dtype=torch.uint8, device=dev) for m in ms}
     sxs = {m: torch.empty((m,), dtype=torch.float16, device=dev) for m in ms}
     Ys = {m: torch.empty((m, N), dtype=torch.float16, device=dev) for m in ms}
+    Ws = {m: torch.empty(max(1, mq.linear_workspace_bytes(m, N, K)), dtype=torch.uint8, device=dev) for m in ms}
     del W
     torch.cuda.synchronize()
 
@@ -184,8 +188,7 @@ def main():
 
     def step():
         for m in ms:
-            mq.quantize_act(Xs[m], out=(Xqs[m], sxs[m]))
-            mq.fused_gemm(Xqs[m], sxs[m], next_pw(), out=Ys[m])
+            mq.linear(Xs[m], next_pw(), out=Ys[m], workspace=Ws[m])
 
     def graph_of(fn, calls):
         """Capture `calls` back-to-back invocations of fn in one HIP graph."""
@@ -216,7 +219,7 @@ def main():
         # For rocprofv3 --pmc: TRAFFIC_CALLS GEMM dispatches at the largest M,
         # each on its own weight copy, then TRAFFIC_CALLS copies of 256 MiB.
         mdom = max(ms)
-        mq.quantize_act(Xs[mdom], out=(Xqs[mdom], sxs[mdom]))
+        mq.quantize_act(Xs[mdom], out=(Xqs[mdom], sxs[mdom]))     # the GEMM's own input
         for _ in range(TRAFFIC_CALLS):
             mq.fused_gemm(Xqs[mdom], sxs[mdom], next_pw(), out=Ys[mdom])
         # an elementwise kernel that reads and writes COPY_BYTES each (a
@@ -253,10 +256,10 @@ def main():
     rows = []
     for m in ms:
         ops, byts = algorithmic(m, N, K, nnzb)
-        t_gemm = timed(lambda: mq.fused_gemm(Xqs[m], sxs[m], next_pw(), out=Ys[m]), args.reps)
+        t_call = timed(lambda: mq.linear(Xs[m], next_pw(), out=Ys[m], workspace=Ws[m]), args.reps)
         t_q = timed(lambda: mq.quantize_act(Xs[m], out=(Xqs[m], sxs[m])), args.reps)
-        row = {"M": m, "us_gemm": round(t_gemm, 3), "us_quant": round(t_q, 3),
-               "us_call": round(t_gemm + t_q, 3),
+        t_gemm = timed(lambda: mq.fused_gemm(Xqs[m], sxs[m], next_pw(), out=Ys[m]), args.reps)
+        row = {"M": m, "us_call": round(t_call, 3), "us_gemm": round(t_gemm, 3), "us_quant": round(t_q, 3),
                "eff_tops": round(2.0 * m * N * K / (t_gemm * 1e-6) / 1e12, 2),
                "int8_peak_frac": round(ops / (t_gemm * 1e-6) / 1e12 / PEAK_I8_TOPS, 4),
                "hbm_frac": round(byts / (t_gemm * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),

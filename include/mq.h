@@ -155,6 +155,26 @@ mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int K,
                                 const uint8_t* Rq,
                                 int32_t* Tb, int32_t* Tr, hipStream_t stream);
 
+/*
+ * The whole layer from fp16 activations: mq_quantize_act followed by
+ * mq_fused_gemm, with the same results bit for bit (Section 4.2 "Kernel
+ * Fusion": quantisation fused into the GEMM).  For decode-sized inputs
+ * (M <= 4, M * K <= 32768) one kernel does both: every workgroup quantises the
+ * activation rows into LDS itself, which saves a launch.  Otherwise the
+ * activations are quantised into the workspace first.
+ *   X, ldx   : fp16 [M, ldx], ldx >= K, ldx % 8 == 0, 16-byte aligned.
+ *   others   : as for mq_fused_gemm.
+ *   workspace: >= mq_linear_workspace_size(M, N, K) bytes, 16-byte aligned
+ *              (may be NULL when that is 0).
+ */
+size_t mq_linear_workspace_size(int M, int N, int K);
+mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
+                    const uint8_t* Wq, const void* s_w,
+                    const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                    const uint8_t* Rq, const void* s_r,
+                    void* Y, int ldy,
+                    void* workspace, size_t ws_bytes, hipStream_t stream);
+
 /* ======================================================================== */
 /* Offline weight preparation (not on the timed path)                        */
 /* ======================================================================== */

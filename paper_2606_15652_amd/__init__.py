@@ -31,6 +31,9 @@ _SIG = {
     "mq_fused_gemm_workspace_size": (C.c_size_t, [_I, _I, _I]),
     "mq_fused_gemm": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P,
                           C.c_size_t, _P]),
+    "mq_linear_workspace_size": (C.c_size_t, [_I, _I, _I]),
+    "mq_linear": (_I, [_I, _I, _I, _P, _I, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P,
+                      C.c_size_t, _P]),
     "mq_fused_gemm_variant": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I,
                                   _P, C.c_size_t, _P]),
     "mq_fused_gemm_acc_i32": (_I, [_I, _I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _P, _P]),
@@ -120,11 +123,13 @@ def quantize_act(X, out=None, stream=None):
 
 @dataclass
 class PackedWeight:
-    """Device-resident operands of one MosaicQuant linear layer (canonical layouts)."""
+    """Device-resident operands of one MosaicQuant linear layer, in the
+    library's storage order (include/mq.h): Wq's N*K/2 bytes group-major
+    (piece (row n, group g) at (g N + n) 64), s_w's N*K/128 values [K/128][N]."""
     N: int
     K: int
-    Wq: "object"          # uint8 [N, K/2]
-    s_w: "object"         # fp16 [N, K/128]
+    Wq: "object"          # uint8, N*K/2 bytes held as [N, K/2], group order
+    s_w: "object"         # fp16, N*K/128 values held as [N, K/128], order [K/128][N]
     rowptr: "object"      # int32 [N/128 + 1]
     kb: "object"          # int32 [nnzb] (may be empty)
     Rq: "object"          # uint8 [nnzb, 128, 64]
@@ -182,10 +187,33 @@ def fused_gemm_acc_i32(Xq, pw: PackedWeight, variant: str = "auto", stream=None)
     return Tb, Tr
 
 
-def linear(X, pw: PackedWeight, variant: str = "auto", stream=None):
-    """The whole hot path: quantise fp16 X [M, K] then the fused GEMM."""
-    Xq, s_x = quantize_act(X, stream=stream)
-    return fused_gemm(Xq, s_x, pw, variant=variant, stream=stream)
+def linear_workspace_bytes(M: int, N: int, K: int) -> int:
+    return int(load().mq_linear_workspace_size(M, N, K))
+
+
+def linear(X, pw: PackedWeight, out=None, workspace=None, stream=None):
+    """The whole hot path from fp16 X [M, K]: quantisation and the fused GEMM
+    (one kernel at decode sizes), Y fp16 [M, N]."""
+    torch = _torch()
+    _need(X, torch.float16, "X", 2)
+    M, K = X.shape
+    if K != pw.K:
+        raise ValueError("X does not match the weight")
+    Y = out if out is not None else torch.empty((M, pw.N), dtype=torch.float16, device=X.device)
+    if out is not None:
+        _need(Y, torch.float16, "out", 2)
+    rp, kb, rq, sr = _res_ptrs(pw)
+    lib = load()
+    ws = lib.mq_linear_workspace_size(M, pw.N, pw.K)
+    wbuf = None
+    if ws:
+        wbuf = workspace if workspace is not None else torch.empty(ws, dtype=torch.uint8, device=X.device)
+        if wbuf.numel() * wbuf.element_size() < ws:
+            raise ValueError(f"workspace needs {ws} bytes")
+    _check("mq_linear", lib.mq_linear(
+        M, pw.N, pw.K, _ptr(X), X.stride(0), _ptr(pw.Wq), _ptr(pw.s_w), rp, kb, pw.nnzb, rq, sr,
+        _ptr(Y), Y.stride(0), _ptr(wbuf), ws, _stream(stream)))
+    return Y
 
 
 # --------------------------------------------------- weight preparation --

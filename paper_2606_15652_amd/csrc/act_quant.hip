@@ -16,31 +16,6 @@ namespace mq {
 
 constexpr int kActThreads = 256;
 
-__device__ __forceinline__ uint32_t chunk_absmax_bits(const uint4 v) {
-    uint32_t m = 0;
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        uint32_t lo = w[i] & 0x7FFFu, hi = (w[i] >> 16) & 0x7FFFu;
-        m = lo > m ? lo : m;
-        m = hi > m ? hi : m;
-    }
-    return m;
-}
-
-// 16 fp16 -> 16 codes -> one folded chunk.
-__device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, float s) {
-    if (s == 0.0f) return make_uint2(0u, 0u);
-    const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-    int q[16];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        q[2 * i] = quant_code(half_bits_to_float((uint16_t)(w[i] & 0xFFFFu)), s);
-        q[2 * i + 1] = quant_code(half_bits_to_float((uint16_t)(w[i] >> 16)), s);
-    }
-    return fold_codes(q);
-}
-
 // CPT > 0: the row stays in registers (CPT chunks per thread); CPT == 0: the
 // row is read twice.
 template <int CPT>

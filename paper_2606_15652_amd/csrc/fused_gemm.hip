@@ -48,6 +48,8 @@ struct GemmArgs {
     int ldy;
     int32_t* Tb;             // raw mode outputs
     int32_t* Tr;
+    const uint16_t* X;       // fused-quantisation decode path: fp16 activations
+    int ldx;
 };
 
 // Keeps a value in registers at this point of the program: an empty volatile
@@ -416,12 +418,22 @@ static int tiled_splits(int M, int N, int K) {
 // Skinny kernel: 16 * WN output columns per workgroup, all M (<= 16 * WM)
 // rows, the K-loop split over NW waves.
 // --------------------------------------------------------------------------
-template <int WM, int WN, int NW, bool RAW>
+// Fused activation quantisation (FQ): at most kFusedMaxM rows and
+// kFusedCPT 16-element chunks per thread; the workgroup quantises the rows
+// into LDS itself (same arithmetic as mq_quantize_act) instead of reading Xq.
+constexpr int kFusedMaxM = 4, kFusedCPT = 4;
+
+template <int WM, int WN, int NW, bool RAW, bool FQ = false>
 __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
     static_assert(WN * 16 <= 128 && 128 % (WN * 16) == 0, "workgroup columns must sit in one block row");
+    static_assert(!(FQ && RAW), "fused quantisation feeds the fp16 path");
     // reduction buffer: fp32 partials, or (raw mode) int32 base and residual sums
     constexpr int kSlotsPerWave = WM * WN * 4 * (RAW ? 2 : 1);
     __shared__ __attribute__((aligned(16))) uint32_t red[NW][kSlotsPerWave][64];
+    // FQ: packed codes of the M rows (M x K/2 bytes, row-major), row maxima, scales
+    extern __shared__ __attribute__((aligned(16))) uint8_t xs[];
+    __shared__ uint32_t amax_sh[kFusedMaxM];
+    __shared__ uint16_t sx_sh[kFusedMaxM];
 
     const int M = a.M, K = a.K, N = a.N;
     const int G = K / kGroup;
@@ -435,16 +447,18 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
     const int gb = wave * per + (wave < extra ? wave : extra);
     const int ge = gb + per + (wave < extra ? 1 : 0);
 
-    // residual walk: first entry of the block row with column >= gb
+    // residual walk: first entry of the block row with column >= gb (scalar
+    // loads through the constant address space, off the vector-memory counter)
+    const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
     int rp = 0, rend = 0;
     if (a.rowptr) {
+        const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
         const int nb = n0 / 128;
-        rp = a.rowptr[nb];
-        rend = a.rowptr[nb + 1];
-        while (rp < rend && a.res_kb[rp] < gb) ++rp;
+        rp = rowptr[nb];
+        rend = rowptr[nb + 1];
+        while (rp < rend && res_kb[rp] < gb) ++rp;
     }
     const int rrow0 = n0 % 128;
-
 
     f32x4 acc[WM][WN];
     i32x4 iacc[WM][WN], racc[WM][WN];
@@ -457,61 +471,189 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
             racc[i][j] = i32x4{0, 0, 0, 0};
         }
 
-    uint4 xpk[WM], wpk[WN], rpk[WN];
-    uint16_t swb[WN], srb[WN];
-    int cur_p = -1;
-    auto load = [&](int g) {
+    // Operands of kChunk consecutive groups per stage; two stages alternate so
+    // that a wave keeps up to 2 * kChunk groups of loads in flight (decode is
+    // bound by how many bytes are in flight, not by the arithmetic).
+    constexpr int kChunk = 4;
+    struct Stage {
+        uint4 x[kChunk][WM], w[kChunk][WN], r[kChunk][WN];
+        uint16_t sw[kChunk][WN], sr[kChunk][WN];
+        int p[kChunk];
+    };
+    // Every load is issued unconditionally through a range-checked buffer
+    // resource (rows past M, absent residual blocks and groups past ge read
+    // zero from a resource that does not cover them), so each stage issues a
+    // fixed number of loads and the compiler's waits can leave the other
+    // stage in flight.
+    auto load = [&](int c0, Stage& S) {
+        // dense operands first: they do not wait for the scalar CSR walk
 #pragma unroll
-        for (int i = 0; i < WM; ++i) {
-            const int row = i * 16 + lrow;
-            xpk[i] = make_uint4(0, 0, 0, 0);
-            if (row < M) xpk[i] = ldg16(a.Xq + piece_offset(M, row, g) + lq * 16);
+        for (int q = 0; q < kChunk; ++q) {
+            const int g = c0 + q;
+            const bool live = g < ge;
+            const __amdgpu_buffer_rsrc_t xr =
+                make_rsrc(a.Xq + (live ? piece_offset(M, 0, g) : 0), live ? (uint32_t)M * kGroupBytes : 0u);
+            const __amdgpu_buffer_rsrc_t wr =
+                make_rsrc(a.Wq + (live ? piece_offset(N, n0, g) : 0), live ? 16u * WN * kGroupBytes : 0u);
+            if constexpr (!FQ) {
+#pragma unroll
+                for (int i = 0; i < WM; ++i)
+                    S.x[q][i] = bload16(xr, (uint32_t)(i * 16 + lrow) * kGroupBytes + lq * 16, 0);
+            }
+#pragma unroll
+            for (int j = 0; j < WN; ++j)
+                S.w[q][j] = bload16(wr, (uint32_t)(16 * j + lrow) * kGroupBytes + lq * 16, 0);
+            if constexpr (!RAW) {
+                const __amdgpu_buffer_rsrc_t swr =
+                    make_rsrc(a.s_w + (live ? wscale_index(N, n0, g) : 0), live ? 32u * WN : 0u);
+#pragma unroll
+                for (int j = 0; j < WN; ++j)
+                    S.sw[q][j] = __builtin_amdgcn_raw_buffer_load_b16(swr, (uint32_t)(16 * j + lrow) * 2, 0, 0);
+            }
         }
 #pragma unroll
-        for (int j = 0; j < WN; ++j) {
-            const int n = n0 + 16 * j + lrow;
-            wpk[j] = ldg16(a.Wq + piece_offset(N, n, g) + lq * 16);
-            if constexpr (!RAW) swb[j] = a.s_w[wscale_index(N, n, g)];
+        for (int q = 0; q < kChunk; ++q) {
+            const int g = c0 + q;
+            int pr = -1;
+            if (g < ge && rp < rend && res_kb[rp] == g) pr = rp++;
+            S.p[q] = pr;
+            const bool hr = pr >= 0;
+            // (an absent block reads through a zero-size resource on the
+            // weight base: a.Rq may be null when there are no residual blocks)
+            const __amdgpu_buffer_rsrc_t rr = hr ? make_rsrc(a.Rq + ((int64_t)pr * 128 + rrow0) * kGroupBytes,
+                                                             16u * WN * kGroupBytes)
+                                                 : make_rsrc(a.Wq, 0u);
+#pragma unroll
+            for (int j = 0; j < WN; ++j)
+                S.r[q][j] = bload16(rr, (uint32_t)(16 * j + lrow) * kGroupBytes + lq * 16, 0);
+            if constexpr (!RAW) {
+                const __amdgpu_buffer_rsrc_t srr =
+                    hr ? make_rsrc(a.s_r + (int64_t)pr * 128 + rrow0, 32u * WN) : make_rsrc(a.Wq, 0u);
+#pragma unroll
+                for (int j = 0; j < WN; ++j)
+                    S.sr[q][j] = __builtin_amdgcn_raw_buffer_load_b16(srr, (uint32_t)(16 * j + lrow) * 2, 0, 0);
+            }
         }
-        cur_p = -1;
-        if (rp < rend && a.res_kb[rp] == g) {
-            cur_p = rp++;
-            const uint8_t* rb = a.Rq + ((int64_t)cur_p * 128 + rrow0 + lrow) * kGroupBytes + lq * 16;
+    };
+    // each group's epilogue completes inside the block of its MFMAs (see pin)
+    auto pin_all = [&]() {
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
 #pragma unroll
             for (int j = 0; j < WN; ++j) {
-                rpk[j] = ldg16(rb + j * 16 * kGroupBytes);
-                if constexpr (!RAW) srb[j] = a.s_r[(int64_t)cur_p * 128 + rrow0 + j * 16 + lrow];
+                if constexpr (RAW) { pin(iacc[i][j]); pin(racc[i][j]); }
+                else pin(acc[i][j]);
+            }
+    };
+    auto compute = [&](const Stage& S, int c0) {
+#pragma unroll
+        for (int q = 0; q < kChunk; ++q) {
+            if (c0 + q >= ge) continue;
+            const int p = S.p[q];
+            i32x8 av[WM], wv[WN], rv[WN];
+            float sw_f[WN], sr_f[WN];
+#pragma unroll
+            for (int i = 0; i < WM; ++i) {
+                if constexpr (FQ) {
+                    const int row = i * 16 + lrow;
+                    uint4 v = make_uint4(0, 0, 0, 0);
+                    if (row < M) v = *reinterpret_cast<const uint4*>(&xs[(int64_t)row * (K / 2) + (c0 + q) * kGroupBytes + lq * 16]);
+                    av[i] = unfold_codes(v);
+                } else {
+                    av[i] = unfold_codes(S.x[q][i]);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < WN; ++j) {
+                wv[j] = unfold_codes(S.w[q][j]);
+                sw_f[j] = RAW ? 0.f : half_bits_to_float(S.sw[q][j]) * kCodeScale;
+                rv[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0};
+                sr_f[j] = 0.f;
+            }
+            if (p >= 0) {
+#pragma unroll
+                for (int j = 0; j < WN; ++j) {
+                    rv[j] = unfold_codes(S.r[q][j]);
+                    sr_f[j] = RAW ? 0.f : half_bits_to_float(S.sr[q][j]) * kCodeScale;
+                }
+#pragma unroll
+                for (int i = 0; i < WM; ++i)
+                    group_row<WN, RAW, true>(av[i], wv, rv, sw_f, sr_f, acc[i], iacc[i], racc[i]);
+                pin_all();
+            } else {
+#pragma unroll
+                for (int i = 0; i < WM; ++i)
+                    group_row<WN, RAW, false>(av[i], wv, rv, sw_f, sr_f, acc[i], iacc[i], racc[i]);
+                pin_all();
             }
         }
     };
 
-    if (gb < ge) load(gb);
-    for (int g = gb; g < ge; ++g) {
-        i32x8 av[WM], wv[WN], rv[WN];
-        float sw_f[WN], sr_f[WN];
-        const int p = cur_p;
+    // FQ, part 1: this thread's chunks of X (loaded first, so that they are
+    // the first loads to land) and their per-row maxima
+    const int nxc = K / 16;
+    uint4 xv[FQ ? kFusedCPT : 1][2];
+    // row of chunk index idx (M <= kFusedMaxM rows of nxc chunks)
+    auto row_of = [&](int idx) { return (idx >= nxc) + (idx >= 2 * nxc) + (idx >= 3 * nxc); };
+    if constexpr (FQ) {
+        if (threadIdx.x < kFusedMaxM) amax_sh[threadIdx.x] = 0u;
 #pragma unroll
-        for (int j = 0; j < WN; ++j) { rv[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0}; sw_f[j] = sr_f[j] = 0.f; }
-#pragma unroll
-        for (int i = 0; i < WM; ++i) av[i] = unfold_codes(xpk[i]);
-#pragma unroll
-        for (int j = 0; j < WN; ++j) {
-            wv[j] = unfold_codes(wpk[j]);
-            if constexpr (!RAW) sw_f[j] = half_bits_to_float(swb[j]) * kCodeScale;
-            if (p >= 0) {
-                rv[j] = unfold_codes(rpk[j]);
-                if constexpr (!RAW) sr_f[j] = half_bits_to_float(srb[j]) * kCodeScale;
+        for (int i = 0; i < kFusedCPT; ++i) {
+            const int idx = (int)threadIdx.x + i * 64 * NW;
+            xv[i][0] = xv[i][1] = make_uint4(0, 0, 0, 0);
+            if (idx < M * nxc) {
+                const int m = row_of(idx), c = idx - m * nxc;
+                const uint16_t* src = a.X + (int64_t)m * a.ldx + 16 * c;
+                xv[i][0] = ldg16(reinterpret_cast<const uint8_t*>(src));
+                xv[i][1] = ldg16(reinterpret_cast<const uint8_t*>(src + 8));
             }
         }
-        if (g + 1 < ge) load(g + 1);
-        auto tiles = [&](auto has_res) {
-            constexpr bool HR = decltype(has_res)::value;
+    }
+
+    Stage SA, SB;
+    int c0 = gb;
+    if (c0 < ge) load(c0, SA);
+
+    if constexpr (FQ) {
+        // FQ, part 2: row maxima across the workgroup (LDS atomic max on the
+        // sign-cleared fp16 bits), scales, codes into LDS
+        __syncthreads();                                   // amax_sh cleared
 #pragma unroll
-            for (int i = 0; i < WM; ++i)
-                group_row<WN, RAW, HR>(av[i], wv, rv, sw_f, sr_f, acc[i], iacc[i], racc[i]);
-        };
-        if (p >= 0) tiles(std::true_type{});
-        else tiles(std::false_type{});
+        for (int i = 0; i < kFusedCPT; ++i) {
+            const int idx = (int)threadIdx.x + i * 64 * NW;
+            if (idx < M * nxc) {
+                const uint32_t c0m = chunk_absmax_bits(xv[i][0]), c1m = chunk_absmax_bits(xv[i][1]);
+                atomicMax(&amax_sh[row_of(idx)], c0m > c1m ? c0m : c1m);
+            }
+        }
+        __syncthreads();
+        float sc[kFusedMaxM];
+#pragma unroll
+        for (int r = 0; r < kFusedMaxM; ++r) {
+            const uint16_t sb = scale_bits_from_amax(half_bits_to_float((uint16_t)amax_sh[r]));
+            sc[r] = half_bits_to_float(sb);
+            if (threadIdx.x == 0) sx_sh[r] = sb;
+        }
+#pragma unroll
+        for (int i = 0; i < kFusedCPT; ++i) {
+            const int idx = (int)threadIdx.x + i * 64 * NW;
+            if (idx < M * nxc) {
+                const int m = row_of(idx), c = idx - m * nxc;
+                const float s = m == 0 ? sc[0] : m == 1 ? sc[1] : m == 2 ? sc[2] : sc[3];
+                *reinterpret_cast<uint2*>(&xs[(int64_t)m * (K / 2) + 8 * c]) = quant_chunk(xv[i][0], xv[i][1], s);
+            }
+        }
+        __syncthreads();
+    }
+
+    while (c0 < ge) {
+        if (c0 + kChunk < ge) load(c0 + kChunk, SB);
+        compute(SA, c0);
+        c0 += kChunk;
+        if (c0 >= ge) break;
+        if (c0 + kChunk < ge) load(c0 + kChunk, SA);
+        compute(SB, c0);
+        c0 += kChunk;
     }
 
     // cross-wave reduction in wave order
@@ -555,7 +697,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
         } else {
             float v = 0.f;
             for (int w = 0; w < NW; ++w) v += __uint_as_float(red[w][slot][l]);
-            a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(a.s_x[m]) * v);
+            const uint16_t sxb = FQ ? sx_sh[m] : a.s_x[m];
+            a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * v);
         }
     }
 }
@@ -677,4 +820,56 @@ extern "C" mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int
     GemmArgs a{M, N, K, Xq, nullptr, Wq, nullptr, nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq,
                nullptr, nullptr, 0, Tb, Tr};
     return launch<true>(variant, a, nullptr, 0, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Whole layer from fp16 activations
+// ---------------------------------------------------------------------------
+static bool fused_decode_ok(int M, int K) {
+    return M >= 1 && M <= kFusedMaxM && (int64_t)M * (K / 16) <= (int64_t)kFusedCPT * 64 * 8 &&
+           (int64_t)M * (K / 2) <= 64 * 1024;
+}
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+extern "C" size_t mq_linear_workspace_size(int M, int N, int K) {
+    if (M <= 0 || !mq_host::shape_ok(N, K) || fused_decode_ok(M, K)) return 0;
+    return align256(mq_fused_gemm_workspace_size(M, N, K)) + align256((size_t)M * (K / 2)) +
+           align256((size_t)2 * M);
+}
+
+extern "C" mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
+                               const uint8_t* Wq, const void* s_w,
+                               const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                               const uint8_t* Rq, const void* s_r,
+                               void* Y, int ldy,
+                               void* workspace, size_t ws_bytes, hipStream_t stream) {
+    mq_status st = check_common(M, N, K, static_cast<const uint8_t*>(X), Wq, res_rowptr, res_kb, nnzb, Rq);
+    if (st != MQ_OK) return st;
+    if (ldx < K || ldx % 8 != 0 || ldy < N || ldy % 8 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
+    const size_t need = mq_linear_workspace_size(M, N, K);
+    if (ws_bytes < need) return MQ_ERR_WORKSPACE;
+    if (M == 0) return MQ_OK;
+    if (!s_w || !Y || (nnzb > 0 && !s_r) || (need > 0 && !workspace)) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::aligned(s_w, 2) || !mq_host::aligned(Y, 2) || (s_r && !mq_host::aligned(s_r, 2)) ||
+        (workspace && !mq_host::aligned(workspace, 16)))
+        return MQ_ERR_MISALIGNED;
+    if (fused_decode_ok(M, K)) {
+        GemmArgs a{M, N, K, nullptr, nullptr, Wq, static_cast<const uint16_t*>(s_w),
+                   nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq, static_cast<const uint16_t*>(s_r),
+                   static_cast<uint16_t*>(Y), ldy, nullptr, nullptr, static_cast<const uint16_t*>(X), ldx};
+        constexpr int NW = 8;
+        hipLaunchKernelGGL((gemm_skinny_kernel<1, 1, NW, false, true>), dim3(N / 16), dim3(64 * NW),
+                           (size_t)M * (K / 2), stream, a);
+        return mq_host::launch_status();
+    }
+    // quantise into the workspace, then the fused GEMM
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    const size_t gws = mq_fused_gemm_workspace_size(M, N, K);
+    uint8_t* Xq = ws + align256(gws);
+    void* sx = Xq + align256((size_t)M * (K / 2));
+    st = mq_quantize_act(X, M, K, ldx, Xq, sx, stream);
+    if (st != MQ_OK) return st;
+    return mq_fused_gemm(M, N, K, Xq, sx, Wq, s_w, res_rowptr, res_kb, nnzb, Rq, s_r, Y, ldy,
+                         gws > 0 ? ws : nullptr, gws, stream);
 }

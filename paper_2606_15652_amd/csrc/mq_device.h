@@ -97,6 +97,34 @@ __device__ __forceinline__ f32x4 mfma_codes(const i32x8 a, const i32x8 b, const 
 // removes the 1/64 of the e2m3 encoding (exact)
 constexpr float kCodeScale = 64.0f;
 
+// ------------------------------------------------- activation quantiser --
+// Largest |x| of 8 fp16 values, as fp16 bits with the sign cleared (an
+// order-preserving integer maximum for finite values).
+__device__ __forceinline__ uint32_t chunk_absmax_bits(const uint4 v) {
+    uint32_t m = 0;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        uint32_t lo = w[i] & 0x7FFFu, hi = (w[i] >> 16) & 0x7FFFu;
+        m = lo > m ? lo : m;
+        m = hi > m ? hi : m;
+    }
+    return m;
+}
+
+// 16 fp16 (two 16-byte loads) -> 16 codes for scale s -> one folded chunk.
+__device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, float s) {
+    if (s == 0.0f) return make_uint2(0u, 0u);
+    const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+    int q[16];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        q[2 * i] = quant_code(half_bits_to_float((uint16_t)(w[i] & 0xFFFFu)), s);
+        q[2 * i + 1] = quant_code(half_bits_to_float((uint16_t)(w[i] >> 16)), s);
+    }
+    return fold_codes(q);
+}
+
 // ----------------------------------------------------- device group order --
 // Packed rows (Xq, Wq) are stored group-major: the 64-byte piece of row r and
 // 128-code group g sits at byte (g rows + r) 64, so every 128-row x 128-code

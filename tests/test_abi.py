@@ -102,3 +102,30 @@ def test_weight_prep_validation(lib):
     assert lib.mq_quantize_residual(A, 256, 256, 256, A, A, A, A, 0, None, None, None) == OK
     assert lib.mq_hessian_diag(A, 0, 128, 128, A, None) == INVALID
     assert lib.mq_block_scores_dhessian(A, 256, 256, 256, A, A, None, A, None) == INVALID
+
+
+def _lin(lib, M=4, N=256, K=256, X=A, ldx=None, Wq=A, sw=A, rp=A, kb=A, nnzb=1, Rq=A, sr=A,
+         Y=A, ldy=None, ws=None, ws_bytes=0):
+    return lib.mq_linear(M, N, K, X, K if ldx is None else ldx, Wq, sw, rp, kb, nnzb, Rq, sr, Y,
+                         N if ldy is None else ldy, ws, ws_bytes, None)
+
+
+def test_linear_validation(lib):
+    assert _lin(lib, M=0) == OK
+    assert _lin(lib, M=-1) == INVALID
+    assert _lin(lib, K=200) == SHAPE
+    assert _lin(lib, ldx=128) == SHAPE                         # ldx < K
+    assert _lin(lib, ldx=260) == SHAPE                         # ldx % 8
+    assert _lin(lib, ldy=264 - 16) == SHAPE
+    assert _lin(lib, X=None) == INVALID
+    assert _lin(lib, X=A + 8) == MISALIGNED
+    assert _lin(lib, Rq=None) == INVALID
+    assert _lin(lib, Y=None) == INVALID
+    # decode sizes need no workspace; larger M need room for the quantised rows
+    assert lib.mq_linear_workspace_size(1, 4096, 4096) == 0
+    assert lib.mq_linear_workspace_size(4, 4096, 8192) == 0
+    need = lib.mq_linear_workspace_size(64, 256, 1024)
+    assert need >= 64 * 512 + 2 * 64
+    assert _lin(lib, M=64, K=1024, ws=A, ws_bytes=need - 1) == WORKSPACE
+    assert _lin(lib, M=64, K=1024, ws=None, ws_bytes=need) == INVALID
+    assert _lin(lib, M=64, K=1024, ws=A + 8, ws_bytes=need) == MISALIGNED

@@ -235,6 +235,34 @@ def test_gemm_parity_random_codes(tc, mq, orc, M, N, K, nnzb):
         assert err <= TIGHT, f"{v}: max-abs-rel {err:.3e}"
 
 
+# ------------------------------------------- whole layer from fp16 X ------
+# (M, N, K, nnzb): M <= 4 with M * K <= 32768 take the one-kernel decode path
+# (activation quantisation fused into the GEMM), the others quantise first.
+LINEAR_CASES = [(1, 256, 128, 1), (2, 512, 1024, 4), (3, 384, 4096, 6), (4, 1024, 8192, 20),
+                (1, 256, 32768, 8), (4, 256, 4096, 3), (1, 128, 40960, 2), (5, 256, 1024, 2),
+                (64, 512, 2048, 7)]
+
+
+@pytest.mark.parametrize("M,N,K,nnzb", LINEAR_CASES, ids=[f"M{c[0]}_N{c[1]}_K{c[2]}_r{c[3]}" for c in LINEAR_CASES])
+def test_linear_matches_oracle_and_two_step(tc, mq, orc, M, N, K, nnzb):
+    """mq_linear from fp16 X: within the bar of the oracle (quantise + layer) and
+    bit-identical to mq_quantize_act followed by mq_fused_gemm."""
+    _, _, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=M * 977 + K + nnzb)
+    X = synth.gen_act(M, K, 7000 + M + K)
+    if M > 1:
+        X[1] = 0                                                  # zero row: scale 0
+    Xq_r, sx_r = orc.quantize_act(X)
+    _, _, Y64 = orc.linear(Xq_r, sx_r, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    Xd = dev(tc, X)
+    Y = mq.linear(Xd, pw)
+    Xq, s_x = mq.quantize_act(Xd)
+    Y2 = mq.fused_gemm(Xq, s_x, pw)
+    tc.cuda.synchronize()
+    assert maxabsrel(Y, Y64) <= TIGHT
+    assert np.array_equal(host(Y.view(tc.int16)), host(Y2.view(tc.int16)))
+
+
 def test_gemm_quantized_layer_matches_oracle(tc, mq, orc):
     """The whole hot path on a synthetic quantised layer (config-1 recipe)."""
     L = synth.workload("c1_1024")
