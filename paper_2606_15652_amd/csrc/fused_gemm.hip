@@ -125,10 +125,7 @@ __device__ __forceinline__ void group_row(const i32x8 a, const i32x8 (&w)[WN], c
 // registers.  With split-K (SPLIT), workgroup z handles a contiguous run of
 // groups and writes fp32 partial sums; reduce_splits_kernel adds them in split
 // order (deterministic) and applies s_x.
-constexpr int kTB = 128, kTThreads = 256;
-// Extra dynamic LDS per workgroup (none needed: the 3-stage ring already
-// limits a CU to two workgroups).
-constexpr int kTOccPadLds = 0;
+constexpr int kTB = 128;
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
 
@@ -203,16 +200,34 @@ __device__ __forceinline__ void wait_loads_and_sync(int n) {
     }
 }
 
-template <bool RAW, bool SPLIT>
-__global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, int groups_per_split,
-                                                                 float* __restrict__ part) {
-    constexpr int WM = 4, WN = 4;
+// Tile geometry: two waves along M of WMB 16-row sub-tiles each, WAVES_N
+// waves along N of 64 columns each.  <4, 2>: 128 x 128 tile, 4 waves, two
+// workgroups per CU; <8, 4>: 256 x 256 tile, 8 waves, one workgroup per CU
+// (half the L2 -> LDS bytes per output, the L2 being the busiest unit).
+template <int WMB, int WAVES_N>
+struct TileShape {
+    static constexpr int kWaves = 2 * WAVES_N;
+    static constexpr int kThreads = 64 * kWaves;
+    static constexpr int kTM = 2 * 16 * WMB;
+    static constexpr int kTN = 64 * WAVES_N;
+    static constexpr int kBlockRows = kTN / kTB;          // residual block rows per tile
+    static constexpr int kPerCU = kWaves == 4 ? 2 : 1;
+    static_assert(kTM / 16 == 2 * kWaves && kTN / 16 == 2 * kWaves, "two 1 KB load blocks per wave and operand");
+};
+
+template <int WMB, int WAVES_N, bool RAW, bool SPLIT>
+__global__ __launch_bounds__(128 * WAVES_N, (WAVES_N == 2 ? 2 : 1))   // TileShape's kThreads, kPerCU
+void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ part) {
+    using TS = TileShape<WMB, WAVES_N>;
+    static_assert(TS::kThreads == 128 * WAVES_N && TS::kPerCU == (WAVES_N == 2 ? 2 : 1), "launch bounds");
+    constexpr int WM = WMB, WN = 4;
     constexpr int kRow = kGroupBytes;                       // 64 packed bytes per row per group
-    constexpr int kTile = kTB * kRow;                       // 8 KB
+    constexpr int kTile = kTB * kRow;                       // 8 KB: one 128-row tile
+    constexpr int TM = TS::kTM, TN = TS::kTN, NBR = TS::kBlockRows;
     constexpr int kStages = 3;
     struct Slot {
-        uint8_t x[kTile], w[kTile], r[kTile];
-        uint32_t sw[kTB / 2], sr[kTB / 2];                  // fp16 scales, two per dword
+        uint8_t x[TM * kRow], w[TN * kRow], r[NBR][kTile];
+        uint32_t sw[TN / 2], sr[NBR][kTB / 2];              // fp16 scales, two per dword
     };
     __shared__ __attribute__((aligned(16))) Slot ring[kStages];
 
@@ -221,64 +236,70 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const int lrow = lane & 15, lq = lane >> 4;
-    const int tiles_m = (M + kTB - 1) / kTB, tiles_n = N / kTB;
+    const int tiles_m = (M + TM - 1) / TM, tiles_n = N / TN;
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * kTB, n0 = tn * kTB;
+    const int m0 = tm * TM, n0 = tn * TN;
     const int gb = SPLIT ? blockIdx.y * groups_per_split : 0;
     const int ge = SPLIT ? min(G, gb + groups_per_split) : G;
 
     // Operands in device group order: the group-g tile of X rows m0.. is
-    // xrows * 64 contiguous bytes at (g M + m0) 64, that of W rows n0.. 8 KB at
-    // (g N + n0) 64, and R block p is 8 KB.  Every tile load goes through a
-    // resource spanning exactly that tile (offsets in the vector operand
-    // only), so X rows past xrows fail the range check and read zero.
-    const uint32_t xrows = (uint32_t)min(kTB, M - m0);
+    // xrows * 64 contiguous bytes at (g M + m0) 64, that of W rows n0.. TN * 64
+    // bytes at (g N + n0) 64, and R block p is 8 KB.  Every tile load goes
+    // through a resource spanning exactly that tile (offsets in the vector
+    // operand only), so X rows past xrows fail the range check and read zero.
+    const uint32_t xrows = (uint32_t)min(TM, M - m0);
     const uint32_t xbytes = xrows * (uint32_t)kRow;
 
-    // residual walk of the tile's block row, from the first entry at or after
-    // gb.  The CSR is read through the constant address space so the walk stays
-    // in scalar registers (scalar loads do not count against the vector-memory
-    // counter the pipeline waits on).
+    // This wave's residual block row (its 64 columns lie in one) and its place
+    // (0..3) among that block row's four waves.  The CSR walk of that block
+    // row starts at the first entry at or after gb; it reads through the
+    // constant address space so it stays in scalar registers (scalar loads do
+    // not count against the vector-memory counter the pipeline waits on).
+    const int br = (64 * wn) / kTB;
+    const int lw = 2 * wm + (wn & 1);
     const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
     int rp = 0, re = 0;
     if (a.rowptr) {
         const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
-        rp = rowptr[tn];
-        re = rowptr[tn + 1];
+        rp = rowptr[tn * NBR + br];
+        re = rowptr[tn * NBR + br + 1];
         while (rp < re && res_kb[rp] < gb) ++rp;
     }
 
-    // DMA lane mapping: wave w fills 1 KB blocks 2w and 2w + 1 of each 8 KB
-    // tile (16 rows each); lane l takes row 16 b + l / 4 and physical chunk
-    // l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row.  Each load
-    // instruction reads 1 KB of whole 64-byte rows, contiguous in memory.
-    uint32_t vt[2];
+    // DMA lane mapping: a wave fills two 1 KB blocks (16 rows each) of a
+    // tile: blocks 2 wave, 2 wave + 1 of the X and W tiles, blocks 2 lw,
+    // 2 lw + 1 of its block row's R tile.  Lane l takes row 16 b + l / 4 and
+    // physical chunk l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row.
+    // Each load instruction reads 1 KB of whole 64-byte rows, contiguous.
+    uint32_t vt[2], vr[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int row = 16 * (2 * wave + i) + (lane >> 2);
-        const int c = (lane & 3) ^ ((row >> 1) & 3);
-        vt[i] = (uint32_t)row * kRow + c * 16;
+        vt[i] = (uint32_t)row * kRow + (((lane & 3) ^ ((row >> 1) & 3)) << 4);
+        const int rrow = 16 * (2 * lw + i) + (lane >> 2);
+        vr[i] = (uint32_t)rrow * kRow + (((lane & 3) ^ ((rrow >> 1) & 3)) << 4);
     }
 
     // Loads of group g into `slot`; returns the number of vector-memory loads
-    // this wave issued and sets p to the group's residual block (or -1).
-    // Wave 0 also fetches the tile's 128 weight scales (256 B), wave 1 the
-    // residual block's 128 scales.
+    // this wave issued and sets p to its block row's residual block at g (or
+    // -1).  Waves 0 .. NBR-1 also fetch the tile's weight scales (256 B per
+    // block row); the wave with lw == 1 of each block row that block's scales.
     auto issue = [&](int g, int slot, int& p) -> int {
         Slot& S = ring[slot];
         const i32x4 xr = buf_desc(a.Xq + piece_offset(M, m0, g), xbytes);
-        const i32x4 wr = buf_desc(a.Wq + piece_offset(N, n0, g), (uint32_t)kTile);
+        const i32x4 wr = buf_desc(a.Wq + piece_offset(N, n0, g), (uint32_t)(TN * kRow));
         dma16(xr, &S.x[(2 * wave) * 1024], vt[0]);
         dma16(xr, &S.x[(2 * wave + 1) * 1024], vt[1]);
         dma16(wr, &S.w[(2 * wave) * 1024], vt[0]);
         dma16(wr, &S.w[(2 * wave + 1) * 1024], vt[1]);
         int n = 4;
         if constexpr (!RAW) {
-            if (wave == 0) {
-                dma4(buf_desc(a.s_w + wscale_index(N, n0, g), kTB * 2), S.sw, (uint32_t)lane * 4);
+            if (wave < NBR) {
+                dma4(buf_desc(a.s_w + wscale_index(N, n0 + kTB * wave, g), kTB * 2), &S.sw[64 * wave],
+                     (uint32_t)lane * 4);
                 ++n;
             }
         }
@@ -286,12 +307,12 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
         if (rp < re && res_kb[rp] == g) p = rp++;
         if (p >= 0) {
             const i32x4 rr = buf_desc(a.Rq + (int64_t)p * kTile, (uint32_t)kTile);
-            dma16(rr, &S.r[(2 * wave) * 1024], vt[0]);
-            dma16(rr, &S.r[(2 * wave + 1) * 1024], vt[1]);
+            dma16(rr, &S.r[br][(2 * lw) * 1024], vr[0]);
+            dma16(rr, &S.r[br][(2 * lw + 1) * 1024], vr[1]);
             n += 2;
             if constexpr (!RAW) {
-                if (wave == 1) {
-                    dma4(buf_desc(a.s_r + (int64_t)p * kTB, kTB * 2), S.sr, (uint32_t)lane * 4);
+                if (lw == 1) {
+                    dma4(buf_desc(a.s_r + (int64_t)p * kTB, kTB * 2), S.sr[br], (uint32_t)lane * 4);
                     ++n;
                 }
             }
@@ -310,17 +331,18 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
             racc[i][j] = i32x4{0, 0, 0, 0};
         }
 
-    const int wrow = 64 * wm, wcol = 64 * wn;
-    // one phase of a group: B fragments from `bt` (scales `sc`), A from xt
-    auto phase = [&](const uint8_t* xt, const uint8_t* bt, const uint32_t* sc, auto is_res) {
+    const int wrow = 16 * WM * wm, wcol = 64 * wn;
+    // One phase of a group: B fragments from rows bcol0 + 16 j + lrow of `bt`
+    // (scales `sc`, same row index), A fragments from xt.
+    auto phase = [&](const uint8_t* xt, const uint8_t* bt, const uint32_t* sc, int bcol0, auto is_res) {
         constexpr bool R = decltype(is_res)::value;
         i32x8 b[WN], dummy[WN];
         float bs[WN], dscale[WN];
 #pragma unroll
         for (int j = 0; j < WN; ++j) {
-            const int row = wcol + 16 * j + lrow;
+            const int row = bcol0 + 16 * j + lrow;
             b[j] = unfold_codes(*reinterpret_cast<const uint4*>(&bt[row * kRow + (swz(row, lq) << 4)]));
-            bs[j] = RAW ? 0.f : half_bits_to_float(reinterpret_cast<const uint16_t*>(sc)[wcol + 16 * j + lrow]) * kCodeScale;
+            bs[j] = RAW ? 0.f : half_bits_to_float(reinterpret_cast<const uint16_t*>(sc)[row]) * kCodeScale;
             dummy[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0};
             dscale[j] = 0.f;
         }
@@ -359,8 +381,8 @@ __global__ __launch_bounds__(kTThreads, 2) void gemm_tiled_kernel(GemmArgs a, in
         const int slot2 = slot == 0 ? 2 : slot - 1;
         if (g + 2 < ge) n_new = issue(g + 2, slot2, p_new);
         const Slot& S = ring[slot];
-        phase(S.x, S.w, S.sw, std::false_type{});
-        if (p_cur >= 0) phase(S.x, S.r, S.sr, std::true_type{});
+        phase(S.x, S.w, S.sw, wcol, std::false_type{});
+        if (p_cur >= 0) phase(S.x, S.r[br], S.sr[br], wcol % kTB, std::true_type{});
         p_cur = p_next;
         p_next = p_new;
         n_next = n_new;
@@ -709,12 +731,28 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
 constexpr int kSkinnyMaxM = 32;
 constexpr int kSkinnyAutoM = 32;   // AUTO picks the skinny kernel up to this M
 
+// The 256 x 256 tile is used when every CU gets at least one tile; smaller
+// problems keep the 128 x 128 tile (and split-K when even those are few).
+constexpr int kLargeTileMinTiles = 256;
+static bool large_tiles_fit(int M, int N) {
+    return N % 256 == 0 && (int64_t)((M + 255) / 256) * (N / 256) >= kLargeTileMinTiles;
+}
+
 template <bool RAW>
 static mq_status launch(mq_variant variant, const GemmArgs& a, void* workspace, size_t ws_bytes,
                         hipStream_t stream) {
-    if (variant == MQ_VARIANT_AUTO) variant = a.M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY : MQ_VARIANT_TILED;
+    if (variant == MQ_VARIANT_AUTO)
+        variant = a.M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY
+                  : large_tiles_fit(a.M, a.N) ? MQ_VARIANT_TILED_LARGE : MQ_VARIANT_TILED;
     if (variant == MQ_VARIANT_SKINNY && a.M > kSkinnyMaxM) variant = MQ_VARIANT_TILED;
-    if (variant == MQ_VARIANT_SKINNY) {
+    if (variant == MQ_VARIANT_TILED_LARGE && a.N % 256 != 0) variant = MQ_VARIANT_TILED;
+    if (variant == MQ_VARIANT_TILED_LARGE) {
+        using TS = TileShape<8, 4>;
+        const int64_t tiles = (int64_t)((a.M + TS::kTM - 1) / TS::kTM) * (a.N / TS::kTN);
+        if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
+        hipLaunchKernelGGL((gemm_tiled_kernel<8, 4, RAW, false>), dim3((unsigned)tiles), dim3(TS::kThreads), 0,
+                           stream, a, 0, (float*)nullptr);
+    } else if (variant == MQ_VARIANT_SKINNY) {
         constexpr int NW = 8;
         const dim3 grid(a.N / 16), block(64 * NW);
         if (a.M <= 16)
@@ -726,15 +764,15 @@ static mq_status launch(mq_variant variant, const GemmArgs& a, void* workspace, 
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
         const int splits = RAW ? 1 : tiled_splits(a.M, a.N, a.K);
         if (splits == 1) {
-            hipLaunchKernelGGL((gemm_tiled_kernel<RAW, false>), dim3((unsigned)tiles), dim3(kTThreads), kTOccPadLds,
-                               stream, a, 0, (float*)nullptr);
+            hipLaunchKernelGGL((gemm_tiled_kernel<4, 2, RAW, false>), dim3((unsigned)tiles),
+                               dim3(TileShape<4, 2>::kThreads), 0, stream, a, 0, (float*)nullptr);
         } else {
             if (!workspace || ws_bytes < (size_t)splits * a.M * a.N * sizeof(float)) return MQ_ERR_WORKSPACE;
             const int G = a.K / kGroup;
             const int gps = (G + splits - 1) / splits;
             float* part = static_cast<float*>(workspace);
-            hipLaunchKernelGGL((gemm_tiled_kernel<RAW, true>), dim3((unsigned)tiles, splits), dim3(kTThreads),
-                               kTOccPadLds, stream, a, gps, part);
+            hipLaunchKernelGGL((gemm_tiled_kernel<4, 2, RAW, true>), dim3((unsigned)tiles, splits),
+                               dim3(TileShape<4, 2>::kThreads), 0, stream, a, gps, part);
             mq_status st = mq_host::launch_status();
             if (st != MQ_OK) return st;
             const int64_t total = (int64_t)a.M * a.N;
@@ -778,7 +816,7 @@ extern "C" mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int
                                            void* Y, int ldy,
                                            void* workspace, size_t ws_bytes, hipStream_t stream) {
     (void)workspace;
-    if (variant < MQ_VARIANT_AUTO || variant > MQ_VARIANT_TILED) return MQ_ERR_INVALID_ARG;
+    if (variant < MQ_VARIANT_AUTO || variant > MQ_VARIANT_TILED_LARGE) return MQ_ERR_INVALID_ARG;
     mq_status st = check_common(M, N, K, Xq, Wq, res_rowptr, res_kb, nnzb, Rq);
     if (st != MQ_OK) return st;
     if (ldy < N || ldy % 8 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
@@ -811,7 +849,7 @@ extern "C" mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int
                                            const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
                                            const uint8_t* Rq,
                                            int32_t* Tb, int32_t* Tr, hipStream_t stream) {
-    if (variant < MQ_VARIANT_AUTO || variant > MQ_VARIANT_TILED) return MQ_ERR_INVALID_ARG;
+    if (variant < MQ_VARIANT_AUTO || variant > MQ_VARIANT_TILED_LARGE) return MQ_ERR_INVALID_ARG;
     mq_status st = check_common(M, N, K, Xq, Wq, res_rowptr, res_kb, nnzb, Rq);
     if (st != MQ_OK) return st;
     if (M == 0) return MQ_OK;

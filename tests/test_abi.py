@@ -87,7 +87,7 @@ def test_acc_i32_validation(lib):
     assert f(0, 0, 256, 256, A, A, A, A, 1, A, A, A, None) == OK
     assert f(0, 4, 256, 256, A, A, A, A, 1, A, None, A, None) == INVALID
     assert f(0, 4, 256, 256, A, A, A, A, 1, A, A + 2, A, None) == MISALIGNED
-    assert f(3, 4, 256, 256, A, A, A, A, 1, A, A, A, None) == INVALID
+    assert f(9, 4, 256, 256, A, A, A, A, 1, A, A, A, None) == INVALID        # no such variant
 
 
 def test_weight_prep_validation(lib):

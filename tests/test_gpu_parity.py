@@ -211,11 +211,15 @@ GEMM_CASES = [
     (1, 128, 128, 1), (5, 384, 256, 3), (16, 1024, 1024, 6), (17, 256, 512, 5),
     (32, 640, 384, 0), (33, 256, 256, 4), (64, 1024, 1024, 6), (100, 384, 640, 9),
     (129, 512, 1024, 12), (256, 1024, 2048, 13), (70, 128, 4096, 32), (48, 2304, 256, 18),
+    (300, 768, 1024, 10), (257, 512, 512, 16),
 ]
 
 
-def _variants(M):
-    return ["skinny", "tiled", "auto"] if M <= 32 else ["tiled", "auto"]
+def _variants(M, N=128):
+    vs = ["skinny", "tiled", "auto"] if M <= 32 else ["tiled", "auto"]
+    if N % 256 == 0:
+        vs.append("tiled_large")            # 256 x 256 tiles (AUTO takes them on large problems)
+    return vs
 
 
 @pytest.mark.parametrize("M,N,K,nnzb", GEMM_CASES, ids=[f"M{c[0]}_N{c[1]}_K{c[2]}_r{c[3]}" for c in GEMM_CASES])
@@ -225,7 +229,7 @@ def test_gemm_parity_random_codes(tc, mq, orc, M, N, K, nnzb):
     Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
     Xq_d, sx_d = dev_x(tc, Xq), dev(tc, s_x).view(tc.float16)
-    for v in _variants(M):
+    for v in _variants(M, N):
         Tb, Tr = mq.fused_gemm_acc_i32(Xq_d, pw, variant=v)
         Y = mq.fused_gemm(Xq_d, sx_d, pw, variant=v)
         tc.cuda.synchronize()
@@ -273,9 +277,10 @@ def test_gemm_quantized_layer_matches_oracle(tc, mq, orc):
     pw = mq.prepare_weight(dev(tc, W), L.nnzb)
     Y = mq.linear(dev(tc, X), pw)
     Xq, s_x = mq.quantize_act(dev(tc, X))
-    for v in ("skinny", "tiled"):
+    for v in ("skinny", "tiled", "tiled_large"):
         Tb, Tr = mq.fused_gemm_acc_i32(Xq, pw, variant=v)
         assert np.array_equal(host(Tb), Tb_ref) and np.array_equal(host(Tr), Tr_ref)
+        assert maxabsrel(mq.fused_gemm(Xq, s_x, pw, variant=v), Y64) <= TIGHT
     assert maxabsrel(Y, Y64) <= TIGHT
 
 
@@ -299,7 +304,7 @@ def test_gemm_extreme_codes_long_k(tc, mq, orc):
     Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
     assert np.abs(Tb_ref).max() == 49 * K
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
-    for v in ("skinny", "tiled"):
+    for v in ("skinny", "tiled", "tiled_large"):
         Tb, Tr = mq.fused_gemm_acc_i32(dev_x(tc, Xq), pw, variant=v)
         Y = mq.fused_gemm(dev_x(tc, Xq), dev(tc, s_x).view(tc.float16), pw, variant=v)
         tc.cuda.synchronize()
@@ -309,13 +314,13 @@ def test_gemm_extreme_codes_long_k(tc, mq, orc):
 
 def test_gemm_guard_bands_and_empty(tc, mq, orc):
     """No writes outside Y[:M, :N] (ldy > N, canary rows); M == 0 is a no-op."""
-    M, N, K, nnzb = 37, 384, 512, 4
+    M, N, K, nnzb = 37, 512, 512, 4
     ops = random_operands(M, N, K, nnzb, seed=5)
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = ops
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
     Xq_d, sx_d = dev_x(tc, Xq), dev(tc, s_x)        # kept alive across the launches
     lib = mq.load()
-    for v in (1, 2):
+    for v in (1, 2, 3):
         if v == 1 and M > 32:
             continue
         canary = 12345
@@ -347,7 +352,7 @@ def test_gemm_no_residual_null_pointers(tc, mq, orc):
     keep = [dev_x(tc, Xq), dev(tc, s_x), dev(tc, layout.block_rows(Wq, K)),
             dev(tc, layout.block_scales(s_w))]               # kept alive across the launches
     lib = mq.load()
-    for v in (1, 2):
+    for v in (1, 2, 3):
         st = lib.mq_fused_gemm_variant(v, M, N, K, *[t.data_ptr() for t in keep], None, None, 0,
                                        None, None, Y.data_ptr(), N, None, 0, None)
         tc.cuda.synchronize()
@@ -361,8 +366,8 @@ def test_gemm_deterministic_and_row_independent(tc, mq, orc):
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=21)
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
     sd = dev(tc, s_x).view(tc.float16)
-    for v in ("tiled", "skinny"):
-        rows = M if v == "tiled" else 16
+    for v in ("tiled", "tiled_large", "skinny"):
+        rows = M if v != "skinny" else 16
         Xd = dev_x(tc, Xq[:rows])
         Y1 = host(mq.fused_gemm(Xd, sd[:rows].contiguous(), pw, variant=v).view(tc.int16))
         Y2 = host(mq.fused_gemm(Xd, sd[:rows].contiguous(), pw, variant=v).view(tc.int16))
