@@ -346,17 +346,40 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
             dummy[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0};
             dscale[j] = 0.f;
         }
-#pragma unroll
-        for (int i = 0; i < WM; ++i) {
+        // Software pipeline over the sub-tile rows: the MFMAs of row i are
+        // issued before the epilogue of row i - 1, so each result is read
+        // four MFMAs after it was started (no wait states to fill).
+        f32x4 tq[2][WN];
+        auto mfma_row = [&](int i) {
             const int row = wrow + 16 * i + lrow;
             const i32x8 av = unfold_codes(*reinterpret_cast<const uint4*>(&xt[row * kRow + (swz(row, lq) << 4)]));
-            // the residual phase feeds its fragments as the "base" operands of
-            // group_row and accumulates into racc in raw mode
-            if constexpr (R)
-                group_row<WN, RAW, false>(av, b, dummy, bs, dscale, acc[i], racc[i], racc[i]);
-            else
-                group_row<WN, RAW, false>(av, b, dummy, bs, dscale, acc[i], iacc[i], racc[i]);
+#pragma unroll
+            for (int j = 0; j < WN; ++j) tq[i & 1][j] = mfma_codes(av, b[j], f32x4{0.f, 0.f, 0.f, 0.f});
+        };
+        auto epilogue_row = [&](int i) {
+#pragma unroll
+            for (int j = 0; j < WN; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if constexpr (RAW) {
+                        // exact integer group sums; the residual phase
+                        // accumulates into racc
+                        if constexpr (R) racc[i][j][r] += (int)(tq[i & 1][j][r] * kCodeScale);
+                        else iacc[i][j][r] += (int)(tq[i & 1][j][r] * kCodeScale);
+                    } else {
+                        acc[i][j][r] = __builtin_fmaf(bs[j], tq[i & 1][j][r], acc[i][j][r]);
+                    }
+                }
+        };
+        mfma_row(0);
+#pragma unroll
+        for (int i = 1; i < WM; ++i) {
+            mfma_row(i);
+            epilogue_row(i - 1);
         }
+        epilogue_row(WM - 1);
+        (void)dummy;
+        (void)dscale;
         // the phase's epilogue completes inside this block (see pin)
 #pragma unroll
         for (int i = 0; i < WM; ++i)
