@@ -63,18 +63,19 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
 
     const uint16_t sb = scale_bits_from_amax(half_bits_to_float((uint16_t)amax));
     const float s = half_bits_to_float(sb);
+    const float inv_s = 1.0f / s;
     if (t == 0) s_x[m] = sb;
 
     if constexpr (CPT > 0) {
 #pragma unroll
         for (int i = 0; i < CPT; ++i) {
             const int c = t + i * kActThreads;
-            if (c < nchunks) out(c) = quant_chunk(v[i][0], v[i][1], s);
+            if (c < nchunks) out(c) = quant_chunk(v[i][0], v[i][1], s, inv_s);
         }
     } else {
         for (int c = t; c < nchunks; c += kActThreads)
             out(c) = quant_chunk(*reinterpret_cast<const uint4*>(row + 16 * c),
-                                 *reinterpret_cast<const uint4*>(row + 16 * c + 8), s);
+                                 *reinterpret_cast<const uint4*>(row + 16 * c + 8), s, inv_s);
     }
 }
 

@@ -685,7 +685,8 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
             if (idx < M * nxc) {
                 const int m = row_of(idx), c = idx - m * nxc;
                 const float s = m == 0 ? sc[0] : m == 1 ? sc[1] : m == 2 ? sc[2] : sc[3];
-                *reinterpret_cast<uint2*>(&xs[(int64_t)m * (K / 2) + 8 * c]) = quant_chunk(xv[i][0], xv[i][1], s);
+                *reinterpret_cast<uint2*>(&xs[(int64_t)m * (K / 2) + 8 * c]) =
+                    quant_chunk(xv[i][0], xv[i][1], s, 1.0f / s);
             }
         }
         __syncthreads();

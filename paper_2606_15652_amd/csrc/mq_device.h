@@ -31,15 +31,25 @@ __device__ __forceinline__ uint16_t scale_bits_from_amax(float amax) {
     return float_to_half_bits(amax / (float)kQmax);
 }
 
-// Code of x for scale s (s != 0): clamp(round_half_even(x / s), -7, 7).
+// Code of x for scale s > 0 (inv_s = 1 / s, rounded any way):
+// clamp(round_half_even(x / s), -7, 7).
 // x is fp16 or fp32 and s is fp16, so the tie points t*s (t = k + 1/2) have at
 // most 15 significant bits: an x that is not a tie lies at least 2^-24
-// (relative) away from one, more than half an fp32 ulp at t, so the correctly
-// rounded fp32 quotient rounds exactly as the real quotient does.
-__device__ __forceinline__ int quant_code(float x, float s) {
-    float r = rintf(x / s);
-    r = fminf(fmaxf(r, -(float)kQmax), (float)kQmax);
-    return (int)r;
+// (relative) away from one, more than half an fp32 ulp at t, so rounding the
+// exact quotient (below) gives what the correctly rounded fp32 quotient does.
+// No division: q = rint(x * inv_s) is within one of the result; e = x - q s
+// is exact (an fma: for q != 0 both terms are multiples of half an ulp of s
+// and |e| is at most about s; for q = 0, e = x); comparing |e| with s/2
+// (exact) moves q to the nearest integer, ties to the even one.
+__device__ __forceinline__ int quant_code(float x, float s, float inv_s) {
+    float q = rintf(x * inv_s);
+    const float e = __builtin_fmaf(-q, s, x);
+    const float h = 0.5f * s;
+    const float ae = fabsf(e);
+    const bool odd = ((int)q & 1) != 0;
+    if (ae > h || (ae == h && odd)) q += e > 0.f ? 1.f : -1.f;
+    q = fminf(fmaxf(q, -(float)kQmax), (float)kQmax);
+    return (int)q;
 }
 
 // ---------------------------------------------------------- packed codes --
@@ -112,15 +122,16 @@ __device__ __forceinline__ uint32_t chunk_absmax_bits(const uint4 v) {
     return m;
 }
 
-// 16 fp16 (two 16-byte loads) -> 16 codes for scale s -> one folded chunk.
-__device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, float s) {
+// 16 fp16 (two 16-byte loads) -> 16 codes for scale s (inv_s = 1 / s) -> one
+// folded chunk.
+__device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, float s, float inv_s) {
     if (s == 0.0f) return make_uint2(0u, 0u);
     const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
     int q[16];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        q[2 * i] = quant_code(half_bits_to_float((uint16_t)(w[i] & 0xFFFFu)), s);
-        q[2 * i + 1] = quant_code(half_bits_to_float((uint16_t)(w[i] >> 16)), s);
+        q[2 * i] = quant_code(half_bits_to_float((uint16_t)(w[i] & 0xFFFFu)), s, inv_s);
+        q[2 * i + 1] = quant_code(half_bits_to_float((uint16_t)(w[i] >> 16)), s, inv_s);
     }
     return fold_codes(q);
 }

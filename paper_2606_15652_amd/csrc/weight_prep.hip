@@ -27,15 +27,16 @@ __global__ __launch_bounds__(256) void quant_base_kernel(
     const uint16_t sb = scale_bits_from_amax(amax);
     const float s = half_bits_to_float(sb);
     s_w[wscale_index(N, n, g)] = sb;
+    const float inv_s = 1.0f / s;
     uint2* dst = reinterpret_cast<uint2*>(Wq + piece_offset(N, n, g));
     for (int c = 0; c < kGroup / 16; ++c) {   // one folded chunk per 16 elements
         int q[16];
         for (int i = 0; i < 4; ++i) {
             const float4 v = src[c * 4 + i];
-            q[4 * i + 0] = s == 0.0f ? 0 : quant_code(v.x, s);
-            q[4 * i + 1] = s == 0.0f ? 0 : quant_code(v.y, s);
-            q[4 * i + 2] = s == 0.0f ? 0 : quant_code(v.z, s);
-            q[4 * i + 3] = s == 0.0f ? 0 : quant_code(v.w, s);
+            q[4 * i + 0] = s == 0.0f ? 0 : quant_code(v.x, s, inv_s);
+            q[4 * i + 1] = s == 0.0f ? 0 : quant_code(v.y, s, inv_s);
+            q[4 * i + 2] = s == 0.0f ? 0 : quant_code(v.z, s, inv_s);
+            q[4 * i + 3] = s == 0.0f ? 0 : quant_code(v.w, s, inv_s);
         }
         dst[c] = fold_codes(q);
     }
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(128) void score_dhessian_kernel(
     double before = 0.0, after = 0.0;
     for (int c = 0; c < kGroup; ++c) {
         const float rv = residual_at(w[c], s, code_at(q, c));
-        const int rq = sr == 0.0f ? 0 : quant_code(rv, sr);
+        const int rq = sr == 0.0f ? 0 : quant_code(rv, sr, 1.0f / sr);
         const double hj = h[kb * kGroup + c];
         const double e = (double)rv - (double)sr * (double)rq;
         before += hj * (double)rv * (double)rv;
@@ -245,7 +246,7 @@ __global__ __launch_bounds__(128) void quant_residual_kernel(
         for (int e = 0; e < 16; ++e) {
             const int k = 16 * c + e;
             const float rv = residual_at(w[k], s, code_at(q, k));
-            rq[e] = sr == 0.0f ? 0 : quant_code(rv, sr);
+            rq[e] = sr == 0.0f ? 0 : quant_code(rv, sr, 1.0f / sr);
         }
         dst[c] = fold_codes(rq);
     }
