@@ -111,9 +111,11 @@ __device__ __forceinline__ void group_row(const i32x8 a, const i32x8 (&w)[WN], c
 // this group, the R tile and its 128 scales go by LDS DMA (buffer loads that
 // write LDS directly, no staging registers) into one slot of a 3-stage ring:
 // at iteration g the waves wait for group g's loads, meet at the barrier that
-// also frees the slot of group g-1, issue group g+2 into it and compute g.
-// The DMA does not raise the compiler's wait counters, so the kernel waits on
-// the vector-memory counter itself (wait_loads_and_sync).
+// also frees the slot of group g-1, and compute g, issuing the loads of group
+// g+2 into that slot a few at a time between the MFMA rows (a wave that
+// issued all of them at once would stall at issue while the memory pipeline
+// drains).  The DMA does not raise the compiler's wait counters, so the
+// kernel waits on the vector-memory counter itself (wait_loads_and_sync).
 //
 // Loads use per-tile buffer resources over operands in device group order, so
 // each load instruction reads 1 KB of whole 64-byte rows, contiguous.  16-byte chunks are XOR-swizzled
@@ -177,27 +179,35 @@ __device__ __forceinline__ i32x4 buf_desc(const void* base, uint32_t bytes) {
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(lds_ptr_t)p;
 }
-__device__ __forceinline__ void dma16(const i32x4 desc, const void* dst, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                 :: "s"(lds_addr(dst)), "v"(voff), "s"(desc) : "memory", "m0");
+// An LDS DMA reads M0; after an SALU write of M0 it needs one wait state
+// (the compiler adds none inside inline assembly, hence the s_nop).
+__device__ __forceinline__ void dma16(const i32x4 desc, uint32_t dst, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(dst), "v"(voff), "s"(desc) : "memory", "m0");
 }
-__device__ __forceinline__ void dma4(const i32x4 desc, const void* dst, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
-                 :: "s"(lds_addr(dst)), "v"(voff), "s"(desc) : "memory", "m0");
+__device__ __forceinline__ void dma4(const i32x4 desc, uint32_t dst, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :: "s"(dst), "v"(voff), "s"(desc) : "memory", "m0");
 }
 
-// Waits until at most n of this wave's vector-memory loads are in flight (the
-// LDS DMA does not raise the compiler's own waits), then meets the other waves
-// of the workgroup.  s_waitcnt takes an immediate, hence one case per count a
-// wave can leave in flight; any other n waits for everything.
-__device__ __forceinline__ void wait_loads_and_sync(int n) {
-    switch (n) {
-        case 4: asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
-        case 5: asm volatile("s_waitcnt vmcnt(5) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
-        case 6: asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
-        case 7: asm volatile("s_waitcnt vmcnt(7) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
-        default: asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
+// f(std::integral_constant<int, I>{}) for I = 0 .. N-1, in order
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for_from(F&& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for_from<I + 1, N>(f);
     }
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    static_for_from<0, N>(f);
+}
+
+// Waits until all of this wave's vector-memory loads have landed (the LDS DMA
+// does not raise the compiler's own waits), then meets the other waves of
+// the workgroup.
+__device__ __forceinline__ void wait_loads_and_sync() {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // Tile geometry: two waves along M of WMB 16-row sub-tiles each, WAVES_N
@@ -223,13 +233,16 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     constexpr int WM = WMB, WN = 4;
     constexpr int kRow = kGroupBytes;                       // 64 packed bytes per row per group
     constexpr int kTile = kTB * kRow;                       // 8 KB: one 128-row tile
-    constexpr int TM = TS::kTM, TN = TS::kTN, NBR = TS::kBlockRows;
+    constexpr int TM = TS::kTM, TN = TS::kTN, NBR = TS::kBlockRows, kWaves = TS::kWaves;
+    constexpr int kCPerBR = WN / NBR;                       // a wave's sub-tiles per block row
     constexpr int kStages = 3;
+    static_assert((NBR == 1 || NBR == 2) && kWaves == 4 * NBR, "one or two block rows, four waves per block row");
     struct Slot {
         uint8_t x[TM * kRow], w[TN * kRow], r[NBR][kTile];
         uint32_t sw[TN / 2], sr[NBR][kTB / 2];              // fp16 scales, two per dword
     };
     __shared__ __attribute__((aligned(16))) Slot ring[kStages];
+    __shared__ __attribute__((aligned(16))) uint8_t spare[1024];   // target of loads that fetch nothing
 
     const int M = a.M, N = a.N, K = a.K;
     const int G = K / kGroup;
@@ -253,71 +266,111 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     const uint32_t xrows = (uint32_t)min(TM, M - m0);
     const uint32_t xbytes = xrows * (uint32_t)kRow;
 
-    // This wave's residual block row (its 64 columns lie in one) and its place
-    // (0..3) among that block row's four waves.  The CSR walk of that block
-    // row starts at the first entry at or after gb; it reads through the
-    // constant address space so it stays in scalar registers (scalar loads do
-    // not count against the vector-memory counter the pipeline waits on).
-    const int br = (64 * wn) / kTB;
-    const int lw = 2 * wm + (wn & 1);
+    // CSR walks of the tile's NBR block rows, from the first entry at or after
+    // gb.  They read through the constant address space so they stay in scalar
+    // registers (scalar loads do not count against the vector-memory counter
+    // the pipeline waits on).
     const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
-    int rp = 0, re = 0;
-    if (a.rowptr) {
-        const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
-        rp = rowptr[tn * NBR + br];
-        re = rowptr[tn * NBR + br + 1];
-        while (rp < re && res_kb[rp] < gb) ++rp;
+    int rp[NBR], re[NBR];
+#pragma unroll
+    for (int b = 0; b < NBR; ++b) {
+        rp[b] = re[b] = 0;
+        if (a.rowptr) {
+            const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
+            rp[b] = rowptr[tn * NBR + b];
+            re[b] = rowptr[tn * NBR + b + 1];
+            while (rp[b] < re[b] && res_kb[rp[b]] < gb) ++rp[b];
+        }
     }
 
-    // DMA lane mapping: a wave fills two 1 KB blocks (16 rows each) of a
-    // tile: blocks 2 wave, 2 wave + 1 of the X and W tiles, blocks 2 lw,
-    // 2 lw + 1 of its block row's R tile.  Lane l takes row 16 b + l / 4 and
+    // DMA lane mapping.  X and W tiles: a wave fills the two 1 KB blocks
+    // (16 rows each) 2 wave and 2 wave + 1.  R tile (8 blocks per block row):
+    // with two block rows (eight waves) wave w fills block w of each, with one
+    // (four waves) blocks 2 w and 2 w + 1.  Lane l takes row 16 b + l / 4 and
     // physical chunk l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row.
     // Each load instruction reads 1 KB of whole 64-byte rows, contiguous.
     uint32_t vt[2], vr[2];
+    int rblk[2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int row = 16 * (2 * wave + i) + (lane >> 2);
-        vt[i] = (uint32_t)row * kRow + (((lane & 3) ^ ((row >> 1) & 3)) << 4);
-        const int rrow = 16 * (2 * lw + i) + (lane >> 2);
-        vr[i] = (uint32_t)rrow * kRow + (((lane & 3) ^ ((rrow >> 1) & 3)) << 4);
+    for (int k = 0; k < 2; ++k) {
+        const int row = 16 * (2 * wave + k) + (lane >> 2);
+        vt[k] = (uint32_t)row * kRow + (((lane & 3) ^ ((row >> 1) & 3)) << 4);
+        rblk[k] = NBR == 2 ? wave : 2 * wave + k;
+        const int rrow = 16 * rblk[k] + (lane >> 2);
+        vr[k] = (uint32_t)rrow * kRow + (((lane & 3) ^ ((rrow >> 1) & 3)) << 4);
     }
 
-    // Loads of group g into `slot`; returns the number of vector-memory loads
-    // this wave issued and sets p to its block row's residual block at g (or
-    // -1).  Waves 0 .. NBR-1 also fetch the tile's weight scales (256 B per
-    // block row); the wave with lw == 1 of each block row that block's scales.
-    auto issue = [&](int g, int slot, int& p) -> int {
+    // Loads of one group.  The X and W tiles: four 1 KB loads per wave, issued
+    // in straight-line code between the MFMA rows of an earlier group's dense
+    // pass (past the last group they read nothing: zero-size resources).  The
+    // rest, only where there is something to fetch, right after that dense
+    // pass (a block boundary: no MFMA result in flight): the residual tiles of
+    // the block rows with a block at this group (each wave two 1 KB loads in
+    // all) and the wave's scale share: waves 0 .. NBR-1 fetch the weight
+    // scales of block row `wave`, waves NBR .. 2 NBR - 1 the residual scales of
+    // block row wave - NBR (256 B each).
+    constexpr int kDma = 4;                  // loads in the dense pass
+    struct Plan {
+        i32x4 xr, wr, rr[2], sc;             // resources
+        uint32_t x, w, r[2], s;              // LDS destinations
+        bool has_r[2], has_s;
+    };
+    auto plan = [&](int g, int slot, int (&p)[NBR]) -> Plan {
         Slot& S = ring[slot];
-        const i32x4 xr = buf_desc(a.Xq + piece_offset(M, m0, g), xbytes);
-        const i32x4 wr = buf_desc(a.Wq + piece_offset(N, n0, g), (uint32_t)(TN * kRow));
-        dma16(xr, &S.x[(2 * wave) * 1024], vt[0]);
-        dma16(xr, &S.x[(2 * wave + 1) * 1024], vt[1]);
-        dma16(wr, &S.w[(2 * wave) * 1024], vt[0]);
-        dma16(wr, &S.w[(2 * wave + 1) * 1024], vt[1]);
-        int n = 4;
+        const bool live = g < ge;
+        const int gl = live ? g : 0;
+        Plan P;
+        P.xr = buf_desc(a.Xq + piece_offset(M, m0, gl), live ? xbytes : 0u);
+        P.wr = buf_desc(a.Wq + piece_offset(N, n0, gl), live ? (uint32_t)(TN * kRow) : 0u);
+        P.x = lds_addr(&S.x[(2 * wave) * 1024]);
+        P.w = lds_addr(&S.w[(2 * wave) * 1024]);
+#pragma unroll
+        for (int b = 0; b < NBR; ++b) {
+            p[b] = -1;
+            if (live && rp[b] < re[b] && res_kb[rp[b]] == g) p[b] = rp[b]++;
+        }
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            const int b = NBR == 2 ? k : 0;
+            P.has_r[k] = p[b] >= 0;
+            P.rr[k] = buf_desc(a.Rq + (int64_t)(p[b] >= 0 ? p[b] : 0) * kTile, (uint32_t)kTile);
+            P.r[k] = lds_addr(&S.r[b][rblk[k] * 1024]);
+        }
+        P.has_s = false;
+        P.sc = buf_desc(a.Wq, 0u);
+        P.s = 0;
         if constexpr (!RAW) {
-            if (wave < NBR) {
-                dma4(buf_desc(a.s_w + wscale_index(N, n0 + kTB * wave, g), kTB * 2), &S.sw[64 * wave],
-                     (uint32_t)lane * 4);
-                ++n;
+            if (live && wave < NBR) {
+                P.has_s = true;
+                P.sc = buf_desc(a.s_w + wscale_index(N, n0 + kTB * wave, g), kTB * 2);
+                P.s = lds_addr(&S.sw[64 * wave]);
+            }
+            const int sb = wave - NBR;
+            const int ps = (NBR == 2 && sb == 1) ? p[NBR - 1] : p[0];
+            if (sb >= 0 && sb < NBR && ps >= 0) {
+                P.has_s = true;
+                P.sc = buf_desc(a.s_r + (int64_t)ps * kTB, kTB * 2);
+                P.s = lds_addr(S.sr[sb]);
             }
         }
-        p = -1;
-        if (rp < re && res_kb[rp] == g) p = rp++;
-        if (p >= 0) {
-            const i32x4 rr = buf_desc(a.Rq + (int64_t)p * kTile, (uint32_t)kTile);
-            dma16(rr, &S.r[br][(2 * lw) * 1024], vr[0]);
-            dma16(rr, &S.r[br][(2 * lw + 1) * 1024], vr[1]);
-            n += 2;
-            if constexpr (!RAW) {
-                if (lw == 1) {
-                    dma4(buf_desc(a.s_r + (int64_t)p * kTB, kTB * 2), S.sr[br], (uint32_t)lane * 4);
-                    ++n;
-                }
-            }
-        }
-        return n;
+        return P;
+    };
+    // X / W load k (0 .. 3) of a plan
+    auto dma_step = [&](const Plan& P, auto kc) {
+        constexpr int k = decltype(kc)::value;
+        if constexpr (k == 0) dma16(P.xr, P.x, vt[0]);
+        else if constexpr (k == 1) dma16(P.xr, P.x + 1024, vt[1]);
+        else if constexpr (k == 2) dma16(P.wr, P.w, vt[0]);
+        else dma16(P.wr, P.w + 1024, vt[1]);
+    };
+    auto issue_extras = [&](const Plan& P) {
+        if (P.has_r[0]) dma16(P.rr[0], P.r[0], vr[0]);
+        if (P.has_r[1]) dma16(P.rr[1], P.r[1], vr[1]);
+        if (P.has_s) dma4(P.sc, P.s, (uint32_t)lane * 4);
+    };
+    auto issue_all = [&](const Plan& P) {
+        static_for<kDma>([&](auto kc) { dma_step(P, kc); });
+        issue_extras(P);
     };
 
     f32x4 acc[WM][WN];
@@ -331,86 +384,153 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
             racc[i][j] = i32x4{0, 0, 0, 0};
         }
 
-    const int wrow = 16 * WM * wm, wcol = 64 * wn;
-    // One phase of a group: B fragments from rows bcol0 + 16 j + lrow of `bt`
-    // (scales `sc`, same row index), A fragments from xt.
-    auto phase = [&](const uint8_t* xt, const uint8_t* bt, const uint32_t* sc, int bcol0, auto is_res) {
-        constexpr bool R = decltype(is_res)::value;
-        i32x8 b[WN], dummy[WN];
-        float bs[WN], dscale[WN];
+    // The wave's rows wrow .. wrow + 16 WM - 1 and its column sub-tiles
+    // c = 0 .. 3 at tile columns 16 (wn + WAVES_N c) .., interleaved so that
+    // every wave has kCPerBR sub-tiles in each residual block row: a residual
+    // block keeps all the waves busy, not only those of its block row.
+    const int wrow = 16 * WM * wm;
+
+    // Operands of a group's dense pass that are read ahead, right after the
+    // barrier that publishes the group (in the middle of the previous group's
+    // dense pass): the wave's four W fragments (folded), their scales and its
+    // first A fragment.  The pass then starts without waiting for LDS.
+    struct Ahead {
+        uint4 w[WN], a0;
+        float s[WN];
+    };
+    auto read_ahead = [&](const Slot& S, Ahead& H) {
+        const uint16_t* sw16 = reinterpret_cast<const uint16_t*>(S.sw);
 #pragma unroll
-        for (int j = 0; j < WN; ++j) {
-            const int row = bcol0 + 16 * j + lrow;
-            b[j] = unfold_codes(*reinterpret_cast<const uint4*>(&bt[row * kRow + (swz(row, lq) << 4)]));
-            bs[j] = RAW ? 0.f : half_bits_to_float(reinterpret_cast<const uint16_t*>(sc)[row]) * kCodeScale;
-            dummy[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0};
-            dscale[j] = 0.f;
+        for (int c = 0; c < WN; ++c) {
+            const int col = 16 * (wn + WAVES_N * c) + lrow;
+            H.w[c] = *reinterpret_cast<const uint4*>(&S.w[col * kRow + (swz(col, lq) << 4)]);
+            H.s[c] = RAW ? 0.f : half_bits_to_float(sw16[col]) * kCodeScale;
+        }
+        const int row = wrow + lrow;
+        H.a0 = *reinterpret_cast<const uint4*>(&S.x[row * kRow + (swz(row, lq) << 4)]);
+    };
+
+    // One pass over the staged group S.  The dense pass (RES == 0) multiplies
+    // all four sub-tiles with the W fragments (from H); after its row
+    // kSync - 1 it waits for the next group's loads, meets the other waves
+    // (which frees the slot of the previous group), reads the next group's
+    // operands ahead into H and spreads the loads of plan P over its remaining
+    // rows.  A residual pass multiplies the sub-tiles in the bit set RES
+    // (those of one block row) with the R fragments of that block row.
+    constexpr int kSync = WM / 2;
+    auto phase = [&](const Slot& S, auto res_c, Ahead& H, const Slot& Snext, const Plan& P) {
+        constexpr int RES = decltype(res_c)::value;
+        constexpr bool DENSE = RES == 0;
+        constexpr int kBR = DENSE ? 0 : (RES >> kCPerBR ? 1 : 0);   // block row of a residual pass
+        auto has = [](int c) { return DENSE || ((RES >> c) & 1); };
+        i32x8 b[WN];
+        float bs[WN];
+#pragma unroll
+        for (int c = 0; c < WN; ++c) {
+            if (!has(c)) continue;
+            if constexpr (DENSE) {
+                b[c] = unfold_codes(H.w[c]);
+                bs[c] = H.s[c];
+            } else {
+                const int row = 16 * (wn + WAVES_N * c) + lrow - kTB * kBR;   // row of the R tile
+                b[c] = unfold_codes(*reinterpret_cast<const uint4*>(&S.r[kBR][row * kRow + (swz(row, lq) << 4)]));
+                bs[c] = RAW ? 0.f : half_bits_to_float(reinterpret_cast<const uint16_t*>(S.sr[kBR])[row]) * kCodeScale;
+            }
         }
         // Software pipeline over the sub-tile rows: the MFMAs of row i are
         // issued before the epilogue of row i - 1, so each result is read
-        // four MFMAs after it was started (no wait states to fill).
+        // several MFMAs after it was started (no wait states to fill).
         f32x4 tq[2][WN];
-        auto mfma_row = [&](int i) {
+        auto mfma_row = [&](auto ic) {
+            constexpr int i = decltype(ic)::value;
             const int row = wrow + 16 * i + lrow;
-            const i32x8 av = unfold_codes(*reinterpret_cast<const uint4*>(&xt[row * kRow + (swz(row, lq) << 4)]));
+            uint4 araw;
+            if constexpr (DENSE && i == 0) araw = H.a0;
+            else araw = *reinterpret_cast<const uint4*>(&S.x[row * kRow + (swz(row, lq) << 4)]);
+            const i32x8 av = unfold_codes(araw);
 #pragma unroll
-            for (int j = 0; j < WN; ++j) tq[i & 1][j] = mfma_codes(av, b[j], f32x4{0.f, 0.f, 0.f, 0.f});
+            for (int c = 0; c < WN; ++c)
+                if (has(c)) tq[i & 1][c] = mfma_codes(av, b[c], f32x4{0.f, 0.f, 0.f, 0.f});
         };
-        auto epilogue_row = [&](int i) {
+        auto epilogue_row = [&](auto ic) {
+            constexpr int i = decltype(ic)::value;
 #pragma unroll
-            for (int j = 0; j < WN; ++j)
+            for (int c = 0; c < WN; ++c) {
+                if (!has(c)) continue;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    if constexpr (RAW) {
-                        // exact integer group sums; the residual phase
-                        // accumulates into racc
-                        if constexpr (R) racc[i][j][r] += (int)(tq[i & 1][j][r] * kCodeScale);
-                        else iacc[i][j][r] += (int)(tq[i & 1][j][r] * kCodeScale);
-                    } else {
-                        acc[i][j][r] = __builtin_fmaf(bs[j], tq[i & 1][j][r], acc[i][j][r]);
-                    }
+                    if constexpr (!RAW) acc[i][c][r] = __builtin_fmaf(bs[c], tq[i & 1][c][r], acc[i][c][r]);
+                    else if constexpr (DENSE) iacc[i][c][r] += (int)(tq[i & 1][c][r] * kCodeScale);   // exact
+                    else racc[i][c][r] += (int)(tq[i & 1][c][r] * kCodeScale);
                 }
+            }
         };
-        mfma_row(0);
-#pragma unroll
-        for (int i = 1; i < WM; ++i) {
-            mfma_row(i);
-            epilogue_row(i - 1);
-        }
-        epilogue_row(WM - 1);
-        (void)dummy;
-        (void)dscale;
-        // the phase's epilogue completes inside this block (see pin)
+        static_for<WM>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            mfma_row(ic);
+            if constexpr (i > 0) epilogue_row(std::integral_constant<int, i - 1>{});
+            if constexpr (DENSE) {
+                if constexpr (i == kSync - 1) {
+                    // the only loads in flight are the next group's
+                    wait_loads_and_sync();
+                    read_ahead(Snext, H);
+                }
+                if constexpr (i >= kSync - 1) {
+                    constexpr int n = WM - kSync + 1, j = i - (kSync - 1);
+                    constexpr int k0 = j * kDma / n, k1 = (j + 1) * kDma / n;
+                    static_for<k1 - k0>([&](auto kc) { dma_step(P, std::integral_constant<int, k0 + decltype(kc)::value>{}); });
+                }
+            }
+        });
+        epilogue_row(std::integral_constant<int, WM - 1>{});
+        // the pass's epilogue completes inside this block (see pin)
 #pragma unroll
         for (int i = 0; i < WM; ++i)
 #pragma unroll
-            for (int j = 0; j < WN; ++j) {
-                if constexpr (!RAW) pin(acc[i][j]);
-                else if constexpr (R) pin(racc[i][j]);
-                else pin(iacc[i][j]);
+            for (int c = 0; c < WN; ++c) {
+                if (!has(c)) continue;
+                if constexpr (!RAW) pin(acc[i][c]);
+                else if constexpr (DENSE) pin(iacc[i][c]);
+                else pin(racc[i][c]);
             }
     };
 
-    // (loads in flight, residual block) of the groups one and two ahead
-    int p_cur = -1, p_next = -1, n_next = 0;
-    if (gb < ge) issue(gb, 0, p_cur);
-    if (gb + 1 < ge) n_next = issue(gb + 1, 1, p_next);
+    // residual blocks of the groups one and two ahead (-1: none), per block row
+    int p_cur[NBR], p_next[NBR], p_new[NBR];
+    issue_all(plan(gb, 0, p_cur));
+    issue_all(plan(gb + 1, 1, p_next));
+    constexpr int kBR0 = (1 << kCPerBR) - 1;                // sub-tiles of block row 0
+    wait_loads_and_sync();                                 // groups gb, gb + 1 landed
+    Ahead H;
+    read_ahead(ring[0], H);
     int slot = 0;
     for (int g = gb; g < ge; ++g) {
-        // group g landed for everyone (group g + 1's loads may stay in
-        // flight); everyone finished group g - 1, whose slot is refilled next
-        wait_loads_and_sync(g + 1 < ge ? n_next : 0);
-        int p_new = -1, n_new = 0;
-        const int slot2 = slot == 0 ? 2 : slot - 1;
-        if (g + 2 < ge) n_new = issue(g + 2, slot2, p_new);
+        // Group g's slot holds its operands (published by the barrier inside
+        // the previous dense pass) and H its dense pass's first operands.  The
+        // dense pass carries the loads of group g + 2 into the slot of group
+        // g - 1, which its barrier frees; then a residual pass per block row
+        // with a block at this group: every wave multiplies its kCPerBR
+        // sub-tiles of that block row.  (Passes rather than variants of the
+        // dense code: one code path per group keeps the accumulators in fixed
+        // registers.)
+        const int snext = slot == 2 ? 0 : slot + 1, sfree = snext == 2 ? 0 : snext + 1;
+        const Plan P = plan(g + 2, sfree, p_new);
         const Slot& S = ring[slot];
-        phase(S.x, S.w, S.sw, wcol, std::false_type{});
-        if (p_cur >= 0) phase(S.x, S.r[br], S.sr[br], wcol % kTB, std::true_type{});
-        p_cur = p_next;
-        p_next = p_new;
-        n_next = n_new;
-        slot = slot == 2 ? 0 : slot + 1;
+        phase(S, std::integral_constant<int, 0>{}, H, ring[snext], P);
+        issue_extras(P);
+        if (p_cur[0] >= 0) phase(S, std::integral_constant<int, kBR0>{}, H, S, P);
+        if constexpr (NBR == 2)
+            if (p_cur[1] >= 0) phase(S, std::integral_constant<int, kBR0 << kCPerBR>{}, H, S, P);
+#pragma unroll
+        for (int b = 0; b < NBR; ++b) {
+            p_cur[b] = p_next[b];
+            p_next[b] = p_new[b];
+        }
+        slot = snext;
     }
+    // the loads issued for the two groups past the end read nothing, but
+    // they still write `spare` or a ring slot: let them finish first
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
     // epilogue: lane holds rows 4 * (lane / 16) + r of each sub-tile, column lane % 16
 #pragma unroll
@@ -421,15 +541,15 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
             if (m >= M) continue;
             const float sx = (RAW || SPLIT) ? 0.f : half_bits_to_float(a.s_x[m]);
 #pragma unroll
-            for (int j = 0; j < WN; ++j) {
-                const int n = n0 + wcol + 16 * j + lrow;
+            for (int c = 0; c < WN; ++c) {
+                const int n = n0 + 16 * (wn + WAVES_N * c) + lrow;
                 if constexpr (RAW) {
-                    a.Tb[(int64_t)m * N + n] = iacc[i][j][r];
-                    a.Tr[(int64_t)m * N + n] = racc[i][j][r];
+                    a.Tb[(int64_t)m * N + n] = iacc[i][c][r];
+                    a.Tr[(int64_t)m * N + n] = racc[i][c][r];
                 } else if constexpr (SPLIT) {
-                    part[((int64_t)blockIdx.y * M + m) * N + n] = acc[i][j][r];
+                    part[((int64_t)blockIdx.y * M + m) * N + n] = acc[i][c][r];
                 } else {
-                    a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(sx * acc[i][j][r]);
+                    a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(sx * acc[i][c][r]);
                 }
             }
         }
