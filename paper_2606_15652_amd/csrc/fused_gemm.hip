@@ -180,14 +180,20 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(lds_ptr_t)p;
 }
 // An LDS DMA reads M0; after an SALU write of M0 it needs one wait state
-// (the compiler adds none inside inline assembly, hence the s_nop).
+// (the compiler adds none inside inline assembly, hence the s_nop).  The
+// destination and the resource are wave-uniform; readfirstlane makes that
+// explicit, so they are always in scalar registers (a no-op when they are).
+__device__ __forceinline__ i32x4 uniform4(const i32x4 d) {
+    return i32x4{__builtin_amdgcn_readfirstlane(d[0]), __builtin_amdgcn_readfirstlane(d[1]),
+                 __builtin_amdgcn_readfirstlane(d[2]), __builtin_amdgcn_readfirstlane(d[3])};
+}
 __device__ __forceinline__ void dma16(const i32x4 desc, uint32_t dst, uint32_t voff) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                 :: "s"(dst), "v"(voff), "s"(desc) : "memory", "m0");
+                 :: "s"(__builtin_amdgcn_readfirstlane(dst)), "v"(voff), "s"(uniform4(desc)) : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(const i32x4 desc, uint32_t dst, uint32_t voff) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
-                 :: "s"(dst), "v"(voff), "s"(desc) : "memory", "m0");
+                 :: "s"(__builtin_amdgcn_readfirstlane(dst)), "v"(voff), "s"(uniform4(desc)) : "memory", "m0");
 }
 
 // f(std::integral_constant<int, I>{}) for I = 0 .. N-1, in order
@@ -242,7 +248,6 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         uint32_t sw[TN / 2], sr[NBR][kTB / 2];              // fp16 scales, two per dword
     };
     __shared__ __attribute__((aligned(16))) Slot ring[kStages];
-    __shared__ __attribute__((aligned(16))) uint8_t spare[1024];   // target of loads that fetch nothing
 
     const int M = a.M, N = a.N, K = a.K;
     const int G = K / kGroup;
@@ -269,51 +274,56 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     // CSR walks of the tile's NBR block rows, from the first entry at or after
     // gb.  They read through the constant address space so they stay in scalar
     // registers (scalar loads do not count against the vector-memory counter
-    // the pipeline waits on).
+    // the pipeline waits on).  nk[b] is the group of block row b's next block
+    // (INT_MAX: none), loaded one entry ahead so no group waits for it.
     const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
-    int rp[NBR], re[NBR];
+    int rp[NBR], re[NBR], nk[NBR];
 #pragma unroll
     for (int b = 0; b < NBR; ++b) {
         rp[b] = re[b] = 0;
+        nk[b] = 0x7fffffff;
         if (a.rowptr) {
             const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
             rp[b] = rowptr[tn * NBR + b];
             re[b] = rowptr[tn * NBR + b + 1];
             while (rp[b] < re[b] && res_kb[rp[b]] < gb) ++rp[b];
+            if (rp[b] < re[b]) nk[b] = res_kb[rp[b]];
         }
     }
 
-    // DMA lane mapping.  X and W tiles: a wave fills the two 1 KB blocks
-    // (16 rows each) 2 wave and 2 wave + 1.  R tile (8 blocks per block row):
-    // with two block rows (eight waves) wave w fills block w of each, with one
-    // (four waves) blocks 2 w and 2 w + 1.  Lane l takes row 16 b + l / 4 and
-    // physical chunk l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row.
-    // Each load instruction reads 1 KB of whole 64-byte rows, contiguous.
-    uint32_t vt[2], vr[2];
-    int rblk[2];
+    // Loads.  The WAVES_N waves with wm == 0 (the loaders, ld = wn) fetch
+    // everything; they are the ones that reach the group's barrier first (the
+    // older waves win issue), so the issue cost lands where there is slack.
+    // Loader ld fills the 1 KB blocks (16 rows each) 4 ld .. 4 ld + 3 of the X
+    // and W tiles, and of the residual tiles of the block rows flattened
+    // (block 8 br + j is block j of block row br), i.e. blocks
+    // 4 (ld & 1) .. + 3 of block row ld / 2, when that block row has a block
+    // at the group; and its scale share: loaders ld < NBR the weight scales of
+    // block row ld, loaders NBR .. 2 NBR - 1 the residual scales of block row
+    // ld - NBR (256 B each).  Lane l takes row 16 b + l / 4 and physical chunk
+    // l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row, so each load
+    // instruction reads 1 KB of whole 64-byte rows, contiguous.
+    static_assert(TM == 64 * WAVES_N && TN == 64 * WAVES_N && 8 * NBR == 4 * WAVES_N,
+                  "four X, W and R blocks per loader");
+    const bool loader = wm == 0;
+    const int ld = wn, lbr = ld >> 1;
+    uint32_t vt[4], vr[4];
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
-        const int row = 16 * (2 * wave + k) + (lane >> 2);
+    for (int k = 0; k < 4; ++k) {
+        const int row = 16 * (4 * ld + k) + (lane >> 2);
         vt[k] = (uint32_t)row * kRow + (((lane & 3) ^ ((row >> 1) & 3)) << 4);
-        rblk[k] = NBR == 2 ? wave : 2 * wave + k;
-        const int rrow = 16 * rblk[k] + (lane >> 2);
+        const int rrow = 16 * (4 * (ld & 1) + k) + (lane >> 2);
         vr[k] = (uint32_t)rrow * kRow + (((lane & 3) ^ ((rrow >> 1) & 3)) << 4);
     }
 
-    // Loads of one group.  The X and W tiles: four 1 KB loads per wave, issued
-    // in straight-line code between the MFMA rows of an earlier group's dense
-    // pass (past the last group they read nothing: zero-size resources).  The
-    // rest, only where there is something to fetch, right after that dense
-    // pass (a block boundary: no MFMA result in flight): the residual tiles of
-    // the block rows with a block at this group (each wave two 1 KB loads in
-    // all) and the wave's scale share: waves 0 .. NBR-1 fetch the weight
-    // scales of block row `wave`, waves NBR .. 2 NBR - 1 the residual scales of
-    // block row wave - NBR (256 B each).
-    constexpr int kDma = 4;                  // loads in the dense pass
+    // Loads of group g into `slot` (issued by the loaders right after the
+    // barrier inside the dense pass of group g - 2; past the last group the X
+    // and W loads read nothing: zero-size resources).  p[b] is block row b's
+    // residual block at g (-1: none).
     struct Plan {
-        i32x4 xr, wr, rr[2], sc;             // resources
-        uint32_t x, w, r[2], s;              // LDS destinations
-        bool has_r[2], has_s;
+        i32x4 xr, wr, rr, sc;                // resources
+        uint32_t x, w, r, s;                 // LDS destinations
+        bool has_r, has_s;
     };
     auto plan = [&](int g, int slot, int (&p)[NBR]) -> Plan {
         Slot& S = ring[slot];
@@ -322,30 +332,30 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         Plan P;
         P.xr = buf_desc(a.Xq + piece_offset(M, m0, gl), live ? xbytes : 0u);
         P.wr = buf_desc(a.Wq + piece_offset(N, n0, gl), live ? (uint32_t)(TN * kRow) : 0u);
-        P.x = lds_addr(&S.x[(2 * wave) * 1024]);
-        P.w = lds_addr(&S.w[(2 * wave) * 1024]);
+        P.x = lds_addr(&S.x[(4 * ld) * 1024]);
+        P.w = lds_addr(&S.w[(4 * ld) * 1024]);
 #pragma unroll
         for (int b = 0; b < NBR; ++b) {
             p[b] = -1;
-            if (live && rp[b] < re[b] && res_kb[rp[b]] == g) p[b] = rp[b]++;
+            if (live && nk[b] == g) {
+                p[b] = rp[b]++;
+                nk[b] = rp[b] < re[b] ? res_kb[rp[b]] : 0x7fffffff;
+            }
         }
-#pragma unroll
-        for (int k = 0; k < 2; ++k) {
-            const int b = NBR == 2 ? k : 0;
-            P.has_r[k] = p[b] >= 0;
-            P.rr[k] = buf_desc(a.Rq + (int64_t)(p[b] >= 0 ? p[b] : 0) * kTile, (uint32_t)kTile);
-            P.r[k] = lds_addr(&S.r[b][rblk[k] * 1024]);
-        }
+        const int pr = (NBR == 2 && lbr == 1) ? p[NBR - 1] : p[0];
+        P.has_r = pr >= 0;
+        P.rr = buf_desc(a.Rq + (int64_t)(pr >= 0 ? pr : 0) * kTile, (uint32_t)kTile);
+        P.r = lds_addr(&S.r[lbr][(4 * (ld & 1)) * 1024]);
         P.has_s = false;
         P.sc = buf_desc(a.Wq, 0u);
         P.s = 0;
         if constexpr (!RAW) {
-            if (live && wave < NBR) {
+            if (live && ld < NBR) {
                 P.has_s = true;
-                P.sc = buf_desc(a.s_w + wscale_index(N, n0 + kTB * wave, g), kTB * 2);
-                P.s = lds_addr(&S.sw[64 * wave]);
+                P.sc = buf_desc(a.s_w + wscale_index(N, n0 + kTB * ld, g), kTB * 2);
+                P.s = lds_addr(&S.sw[64 * ld]);
             }
-            const int sb = wave - NBR;
+            const int sb = ld - NBR;
             const int ps = (NBR == 2 && sb == 1) ? p[NBR - 1] : p[0];
             if (sb >= 0 && sb < NBR && ps >= 0) {
                 P.has_s = true;
@@ -355,22 +365,18 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         }
         return P;
     };
-    // X / W load k (0 .. 3) of a plan
-    auto dma_step = [&](const Plan& P, auto kc) {
-        constexpr int k = decltype(kc)::value;
-        if constexpr (k == 0) dma16(P.xr, P.x, vt[0]);
-        else if constexpr (k == 1) dma16(P.xr, P.x + 1024, vt[1]);
-        else if constexpr (k == 2) dma16(P.wr, P.w, vt[0]);
-        else dma16(P.wr, P.w + 1024, vt[1]);
-    };
-    auto issue_extras = [&](const Plan& P) {
-        if (P.has_r[0]) dma16(P.rr[0], P.r[0], vr[0]);
-        if (P.has_r[1]) dma16(P.rr[1], P.r[1], vr[1]);
+    // the loads of a plan (loaders only; outside any MFMA block)
+    auto issue = [&](const Plan& P) {
+        if (!loader) return;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) dma16(P.xr, P.x + 1024 * k, vt[k]);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) dma16(P.wr, P.w + 1024 * k, vt[k]);
+        if (P.has_r) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) dma16(P.rr, P.r + 1024 * k, vr[k]);
+        }
         if (P.has_s) dma4(P.sc, P.s, (uint32_t)lane * 4);
-    };
-    auto issue_all = [&](const Plan& P) {
-        static_for<kDma>([&](auto kc) { dma_step(P, kc); });
-        issue_extras(P);
     };
 
     f32x4 acc[WM][WN];
@@ -411,12 +417,13 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     };
 
     // One pass over the staged group S.  The dense pass (RES == 0) multiplies
-    // all four sub-tiles with the W fragments (from H); after its row
-    // kSync - 1 it waits for the next group's loads, meets the other waves
-    // (which frees the slot of the previous group), reads the next group's
-    // operands ahead into H and spreads the loads of plan P over its remaining
-    // rows.  A residual pass multiplies the sub-tiles in the bit set RES
-    // (those of one block row) with the R fragments of that block row.
+    // all four sub-tiles with the W fragments (from H) in two halves; between
+    // them (a block boundary: the first half's epilogue is complete) it waits
+    // for the next group's loads, meets the other waves (which frees the slot
+    // of the previous group), has the loaders issue the loads of plan P and
+    // reads the next group's operands ahead into H.  A residual pass
+    // multiplies the sub-tiles in the bit set RES (those of one block row) with
+    // the R fragments of that block row.
     constexpr int kSync = WM / 2;
     auto phase = [&](const Slot& S, auto res_c, Ahead& H, const Slot& Snext, const Plan& P) {
         constexpr int RES = decltype(res_c)::value;
@@ -465,40 +472,41 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
                 }
             }
         };
-        static_for<WM>([&](auto ic) {
-            constexpr int i = decltype(ic)::value;
-            mfma_row(ic);
-            if constexpr (i > 0) epilogue_row(std::integral_constant<int, i - 1>{});
-            if constexpr (DENSE) {
-                if constexpr (i == kSync - 1) {
-                    // the only loads in flight are the next group's
-                    wait_loads_and_sync();
-                    read_ahead(Snext, H);
-                }
-                if constexpr (i >= kSync - 1) {
-                    constexpr int n = WM - kSync + 1, j = i - (kSync - 1);
-                    constexpr int k0 = j * kDma / n, k1 = (j + 1) * kDma / n;
-                    static_for<k1 - k0>([&](auto kc) { dma_step(P, std::integral_constant<int, k0 + decltype(kc)::value>{}); });
-                }
-            }
-        });
-        epilogue_row(std::integral_constant<int, WM - 1>{});
-        // the pass's epilogue completes inside this block (see pin)
+        // rows I0 .. I1 - 1, software-pipelined; their epilogue completes
+        // inside the block (see pin)
+        auto rows = [&](auto i0c, auto i1c) {
+            constexpr int I0 = decltype(i0c)::value, I1 = decltype(i1c)::value;
+            static_for<I1 - I0>([&](auto jc) {
+                constexpr int i = I0 + decltype(jc)::value;
+                mfma_row(std::integral_constant<int, i>{});
+                if constexpr (i > I0) epilogue_row(std::integral_constant<int, i - 1>{});
+            });
+            epilogue_row(std::integral_constant<int, I1 - 1>{});
 #pragma unroll
-        for (int i = 0; i < WM; ++i)
+            for (int i = I0; i < I1; ++i)
 #pragma unroll
-            for (int c = 0; c < WN; ++c) {
-                if (!has(c)) continue;
-                if constexpr (!RAW) pin(acc[i][c]);
-                else if constexpr (DENSE) pin(iacc[i][c]);
-                else pin(racc[i][c]);
-            }
+                for (int c = 0; c < WN; ++c) {
+                    if (!has(c)) continue;
+                    if constexpr (!RAW) pin(acc[i][c]);
+                    else if constexpr (DENSE) pin(iacc[i][c]);
+                    else pin(racc[i][c]);
+                }
+        };
+        if constexpr (DENSE) {
+            rows(std::integral_constant<int, 0>{}, std::integral_constant<int, kSync>{});
+            wait_loads_and_sync();          // the only loads in flight are the next group's
+            issue(P);
+            read_ahead(Snext, H);
+            rows(std::integral_constant<int, kSync>{}, std::integral_constant<int, WM>{});
+        } else {
+            rows(std::integral_constant<int, 0>{}, std::integral_constant<int, WM>{});
+        }
     };
 
     // residual blocks of the groups one and two ahead (-1: none), per block row
     int p_cur[NBR], p_next[NBR], p_new[NBR];
-    issue_all(plan(gb, 0, p_cur));
-    issue_all(plan(gb + 1, 1, p_next));
+    issue(plan(gb, 0, p_cur));
+    issue(plan(gb + 1, 1, p_next));
     constexpr int kBR0 = (1 << kCPerBR) - 1;                // sub-tiles of block row 0
     wait_loads_and_sync();                                 // groups gb, gb + 1 landed
     Ahead H;
@@ -507,7 +515,7 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     for (int g = gb; g < ge; ++g) {
         // Group g's slot holds its operands (published by the barrier inside
         // the previous dense pass) and H its dense pass's first operands.  The
-        // dense pass carries the loads of group g + 2 into the slot of group
+        // dense pass issues the loads of group g + 2 into the slot of group
         // g - 1, which its barrier frees; then a residual pass per block row
         // with a block at this group: every wave multiplies its kCPerBR
         // sub-tiles of that block row.  (Passes rather than variants of the
@@ -517,7 +525,6 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         const Plan P = plan(g + 2, sfree, p_new);
         const Slot& S = ring[slot];
         phase(S, std::integral_constant<int, 0>{}, H, ring[snext], P);
-        issue_extras(P);
         if (p_cur[0] >= 0) phase(S, std::integral_constant<int, kBR0>{}, H, S, P);
         if constexpr (NBR == 2)
             if (p_cur[1] >= 0) phase(S, std::integral_constant<int, kBR0 << kCPerBR>{}, H, S, P);
@@ -528,8 +535,8 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         }
         slot = snext;
     }
-    // the loads issued for the two groups past the end read nothing, but
-    // they still write `spare` or a ring slot: let them finish first
+    // the X and W loads issued for the two groups past the end read nothing,
+    // but they still write a ring slot: let them finish first
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
     // epilogue: lane holds rows 4 * (lane / 16) + r of each sub-tile, column lane % 16
