@@ -75,9 +75,12 @@ typedef enum mq_variant {
     MQ_VARIANT_AUTO = 0,
     MQ_VARIANT_SKINNY = 1,   /* decode: split-K over the waves of a workgroup  */
     MQ_VARIANT_TILED = 2,    /* prefill: 128 x 128 output tiles, K-loop of groups */
-    MQ_VARIANT_TILED_LARGE = 3 /* prefill: 256 x 256 output tiles (N % 256 == 0,
-                                  else as TILED); AUTO takes it when every CU
-                                  gets at least one tile                     */
+    MQ_VARIANT_TILED_LARGE = 3, /* prefill: 256 x 256 output tiles (N % 256 == 0,
+                                   else as TILED); AUTO takes it when every CU
+                                   gets at least one tile                    */
+    MQ_VARIANT_MEDIUM = 4       /* 32 or 64 x 64 output tiles; AUTO takes it
+                                   when 128 x 128 tiles would be too few to
+                                   fill the chip                             */
 } mq_variant;
 
 /* Static string naming a status code.  Never NULL. */

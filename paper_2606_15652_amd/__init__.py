@@ -19,7 +19,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmq.so")
 
 MQ_OK = 0
-VARIANTS = {"auto": 0, "skinny": 1, "tiled": 2, "tiled_large": 3}
+VARIANTS = {"auto": 0, "skinny": 1, "tiled": 2, "tiled_large": 3, "medium": 4}
 BLOCK = 128
 
 _P = C.c_void_p

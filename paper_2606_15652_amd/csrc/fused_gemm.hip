@@ -16,16 +16,20 @@
 // already staged for the dense term and accumulated into the same output
 // registers.
 //
-// Two kernel families share that inner step:
-//  * tiled  (prefill):  a workgroup owns a 128 x 128 output tile; the packed X,
-//    W and (when present) R tiles of each group are copied by the LDS DMA into
-//    a 3-stage ring shared by its four waves.
+// Three kernel families share that inner step:
+//  * tiled  (prefill):  a workgroup owns a 256 x 256 (eight waves, one per CU)
+//    or 128 x 128 (four waves, two per CU) output tile; the packed X, W and
+//    (when present) R tiles of each group are copied by the LDS DMA into a
+//    3-stage ring.
+//  * medium (M of a few hundred): a workgroup owns a 64 x 64 or 32 x 64 tile;
+//    its eight waves split the K-loop in two halves over an 8-slot ring.
 //  * skinny (decode, small M): a workgroup owns 16 output columns and all M
 //    rows; its waves split the K-loop, each streaming a contiguous run of
 //    groups, and the fp32 partial tiles are reduced through LDS in wave order
 //    (deterministic).
 #include "mq_device.h"
 
+#include <stddef.h>
 #include <type_traits>
 
 namespace mq {
@@ -50,6 +54,11 @@ struct GemmArgs {
     int32_t* Tr;
     const uint16_t* X;       // fused-quantisation decode path: fp16 activations
     int ldx;
+    int nnzb;
+    // byte sizes of Xq, Wq, Rq, s_w, s_r (each below 2 GB) and buffer
+    // resources spanning each whole operand (set by launch())
+    uint32_t xq_bytes, wq_bytes, rq_bytes, sw_bytes, sr_bytes;
+    i32x4 rx, rw, rr, rsw, rsr;
 };
 
 // Keeps a value in registers at this point of the program: an empty volatile
@@ -214,6 +223,21 @@ __device__ __forceinline__ void static_for(F&& f) {
 // the workgroup.
 __device__ __forceinline__ void wait_loads_and_sync() {
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Waits until at most n (0 .. 15) of this wave's vector-memory loads are in
+// flight, then meets the other waves.  s_waitcnt takes an immediate, hence
+// one case per count (a larger n waits as for 15, i.e. longer).
+__device__ __forceinline__ void wait_vm_and_sync(int n) {
+#define MQ_WAIT_CASE(k) \
+    case k: asm volatile("s_waitcnt vmcnt(" #k ") lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
+    switch (n) {
+        MQ_WAIT_CASE(0) MQ_WAIT_CASE(1) MQ_WAIT_CASE(2) MQ_WAIT_CASE(3) MQ_WAIT_CASE(4) MQ_WAIT_CASE(5)
+        MQ_WAIT_CASE(6) MQ_WAIT_CASE(7) MQ_WAIT_CASE(8) MQ_WAIT_CASE(9) MQ_WAIT_CASE(10) MQ_WAIT_CASE(11)
+        MQ_WAIT_CASE(12) MQ_WAIT_CASE(13) MQ_WAIT_CASE(14)
+        default: asm volatile("s_waitcnt vmcnt(15) lgkmcnt(0)\n\ts_barrier" ::: "memory"); break;
+    }
+#undef MQ_WAIT_CASE
 }
 
 // Tile geometry: two waves along M of WMB 16-row sub-tiles each, WAVES_N
@@ -587,6 +611,241 @@ static int tiled_splits(int M, int N, int K) {
 }
 
 // --------------------------------------------------------------------------
+// Medium kernel (M from a few dozen to about a thousand rows): a workgroup owns
+// a TM x 64 output tile (TM = 32 WMB), small enough that the problem has
+// hundreds of tiles without split-K over workgroups.  Its eight waves form two
+// K-halves (waves 0-3 take the even groups, waves 4-7 the odd ones: two waves
+// per SIMD, each with a short dependency chain per group) of a 2 x 2 grid:
+// wave (wm, wn) of a half owns rows 16 WMB wm .. and columns 32 wn .., i.e.
+// WMB x 2 sub-tiles.  The halves' sums are added through LDS at the end (in
+// fixed order).  A 64-column tile is half of a residual block row: its R tile
+// is the matching 64 rows (4 KB) of the block, its residual scales the
+// matching 64 of the block's 128.  Per group the X, W (and R) tiles go by LDS
+// DMA into a ring of kStages slots, loaded by the half that computes the
+// group, three group pairs ahead.
+// --------------------------------------------------------------------------
+template <int WMB, bool RAW>
+__global__ __launch_bounds__(512) void gemm_medium_kernel(GemmArgs a) {
+    constexpr int TM = 32 * WMB, TN = 64, kRow = kGroupBytes, kStages = 8;
+    struct Slot {
+        uint8_t x[TM * kRow], w[TN * kRow], r[TN * kRow];
+        uint16_t sw[128], sr[128];                          // 64 used; 256 B per 64-lane dword DMA
+    };
+    __shared__ __attribute__((aligned(16))) Slot ring[kStages];
+
+    const int M = a.M, N = a.N, K = a.K;
+    const int G = K / kGroup;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    const int half = wave >> 2, w4 = wave & 3;
+    const int wm = w4 >> 1, wn = w4 & 1;
+    const int lrow = lane & 15, lq = lane >> 4;
+    const int tiles_m = (M + TM - 1) / TM, tiles_n = N / TN;
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * TM, n0 = tn * TN;
+    const int br = n0 / kTB, roff = n0 % kTB;               // residual block row, row offset inside it
+
+    // CSR walk of the block row (scalar; every wave walks it, so each knows
+    // which groups have a residual block; next block's group loaded ahead)
+    const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
+    int rp = 0, re = 0, nk = 0x7fffffff, nk2 = 0x7fffffff;  // groups of the next two blocks
+    if (a.rowptr) {
+        const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
+        rp = rowptr[br];
+        re = rowptr[br + 1];
+        if (rp < re) nk = res_kb[rp];
+        if (rp + 1 < re) nk2 = res_kb[rp + 1];
+    }
+
+    // DMA, by the half that computes the group: its wave w4 fills 1 KB block
+    // w4 (16 rows) of the W and R tiles and, when w4 < 2 WMB, of the X tile;
+    // wave w4 = 0 the weight scales, w4 = 1 the residual scales (64 lanes x
+    // 4 B, 128 B of them in use).  Lane l takes row 16 w4 + l / 4 and physical
+    // chunk l % 4 (swizzle as in the tiled kernel).  Every load goes through
+    // a resource spanning its whole operand (built by the host), so the
+    // per-group addressing is a vector offset.  A wave issues base_n loads for
+    // a group and res_n more when it has a residual block; it waits on that
+    // count.  X rows past M (last tile) read other bytes of the operand or the
+    // zero tail; they only feed output rows that are never written.
+    const int drow = 16 * w4 + (lane >> 2);
+    const uint32_t chunk = (uint32_t)(((lane & 3) ^ ((drow >> 1) & 3)) << 4);
+    const bool hx = w4 < 2 * WMB;
+    const int base_n = (hx ? 1 : 0) + 1 + ((!RAW && w4 == 0) ? 1 : 0);
+    const int res_n = 1 + ((!RAW && w4 == 1) ? 1 : 0);
+    const uint32_t vx0 = (uint32_t)(m0 + drow) * kRow + chunk;
+    const uint32_t vw0 = (uint32_t)(n0 + drow) * kRow + chunk;
+    const uint32_t vs0 = (uint32_t)n0 * 2 + (uint32_t)lane * 4;
+    const uint32_t vr0 = (uint32_t)(roff + drow) * kRow + chunk;              // + p * 8 KB
+    const uint32_t vsr0 = (uint32_t)roff * 2 + (uint32_t)lane * 4;           // + p * 256 B
+    const uint32_t ring0 = lds_addr(&ring[0]);
+    const uint32_t ox = (uint32_t)offsetof(Slot, x) + 1024u * w4;
+    const uint32_t ow = (uint32_t)offsetof(Slot, w) + 1024u * w4, orr = (uint32_t)offsetof(Slot, r) + 1024u * w4;
+    // group g's loads (by this wave; g < G); p: its residual block (-1: none)
+    auto issue = [&](int g, int p) {
+        const uint32_t sb = ring0 + (uint32_t)(g & (kStages - 1)) * (uint32_t)sizeof(Slot);
+        if (hx) dma16(a.rx, sb + ox, vx0 + (uint32_t)g * ((uint32_t)M * kRow));
+        dma16(a.rw, sb + ow, vw0 + (uint32_t)g * ((uint32_t)N * kRow));
+        if constexpr (!RAW)
+            if (w4 == 0) dma4(a.rsw, sb + (uint32_t)offsetof(Slot, sw), vs0 + (uint32_t)g * ((uint32_t)N * 2));
+        if (p >= 0) {
+            dma16(a.rr, sb + orr, vr0 + (uint32_t)p * (kTB * kRow));
+            if constexpr (!RAW)
+                if (w4 == 1) dma4(a.rsr, sb + (uint32_t)offsetof(Slot, sr), vsr0 + (uint32_t)p * (kTB * 2));
+        }
+    };
+    // the CSR walk, one group at a time (all waves, in group order); the
+    // entry after the next is loaded ahead, so a compare never waits for it
+    auto next_block = [&](int g) -> int {
+        int p = -1;
+        if (g < G && nk == g) {
+            p = rp++;
+            nk = nk2;
+            nk2 = rp + 1 < re ? res_kb[rp + 1] : 0x7fffffff;
+        }
+        return p;
+    };
+    // loads this wave issues for group g with residual flag r
+    auto loads = [&](int g, bool r) -> int { return g < G ? base_n + (r ? res_n : 0) : 0; };
+
+    f32x4 acc[WMB][2];
+    i32x4 iacc[WMB][2], racc[WMB][2];
+#pragma unroll
+    for (int i = 0; i < WMB; ++i)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+            iacc[i][c] = i32x4{0, 0, 0, 0};
+            racc[i][c] = i32x4{0, 0, 0, 0};
+        }
+    const int wrow = 16 * WMB * wm;
+
+    // one group (HAS_RES: with its residual block, sharing the A fragments)
+    auto compute = [&](const Slot& S, auto has_res) {
+        constexpr bool HR = decltype(has_res)::value;
+        i32x8 b[2], rb[2];
+        float bs[2], rs[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            const int col = 32 * wn + 16 * c + lrow;       // row of the W and R tiles
+            const int off = col * kRow + (swz(col, lq) << 4);
+            b[c] = unfold_codes(*reinterpret_cast<const uint4*>(&S.w[off]));
+            bs[c] = RAW ? 0.f : half_bits_to_float(S.sw[col]) * kCodeScale;
+            if constexpr (HR) {
+                rb[c] = unfold_codes(*reinterpret_cast<const uint4*>(&S.r[off]));
+                rs[c] = RAW ? 0.f : half_bits_to_float(S.sr[col]) * kCodeScale;
+            }
+        }
+        f32x4 t[WMB][2], tr[WMB][2];
+#pragma unroll
+        for (int i = 0; i < WMB; ++i) {
+            const int row = wrow + 16 * i + lrow;
+            const i32x8 av = unfold_codes(*reinterpret_cast<const uint4*>(&S.x[row * kRow + (swz(row, lq) << 4)]));
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                t[i][c] = mfma_codes(av, b[c], f32x4{0.f, 0.f, 0.f, 0.f});
+                if constexpr (HR) tr[i][c] = mfma_codes(av, rb[c], f32x4{0.f, 0.f, 0.f, 0.f});
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < WMB; ++i)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if constexpr (RAW) {
+                        iacc[i][c][r] += (int)(t[i][c][r] * kCodeScale);   // exact
+                        if constexpr (HR) racc[i][c][r] += (int)(tr[i][c][r] * kCodeScale);
+                    } else {
+                        acc[i][c][r] = __builtin_fmaf(bs[c], t[i][c][r], acc[i][c][r]);
+                        if constexpr (HR) acc[i][c][r] = __builtin_fmaf(rs[c], tr[i][c][r], acc[i][c][r]);
+                    }
+                }
+                // the group's epilogue completes inside this block (see pin)
+                if constexpr (!RAW) {
+                    pin(acc[i][c]);
+                } else {
+                    pin(iacc[i][c]);
+                    if constexpr (HR) pin(racc[i][c]);
+                }
+            }
+    };
+
+    // Group pairs: pair j is groups 2 j (half 0) and 2 j + 1 (half 1), in
+    // slots 2 j % kStages and the next.  `res` bit 2 j + h: group 2 j + h has a
+    // residual block (pairs in flight, relative to the current one).
+    static_assert(kStages == 8, "four pairs of slots");
+    uint32_t res = 0;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+        const int p0 = next_block(2 * j), p1 = next_block(2 * j + 1);
+        if (2 * j + half < G) issue(2 * j + half, half ? p1 : p0);
+        res |= ((p0 >= 0 ? 1u : 0u) | (p1 >= 0 ? 2u : 0u)) << (2 * j);
+    }
+    for (int g = 0; g < G; g += 2) {
+        // this wave's loads of pair g / 2 landed (those of the next two pairs
+        // may stay in flight); everyone finished the previous pair, whose
+        // slots are refilled next
+        const int gh = g + half;
+        wait_vm_and_sync(loads(gh + 2, (res >> (half + 2)) & 1u) + loads(gh + 4, (res >> (half + 4)) & 1u));
+        const int p0 = next_block(g + 6), p1 = next_block(g + 7);
+        if (gh + 6 < G) issue(gh + 6, half ? p1 : p0);
+        res |= ((p0 >= 0 ? 1u : 0u) | (p1 >= 0 ? 2u : 0u)) << 6;
+        if (gh < G) {
+            if ((res >> half) & 1u) compute(ring[gh & (kStages - 1)], std::true_type{});
+            else compute(ring[gh & (kStages - 1)], std::false_type{});
+        }
+        res >>= 2;
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+    // half 1 hands its sums to half 0 through LDS (the ring is free once
+    // everyone is past the loop); half 0 adds them (fixed order) and writes
+    constexpr int kVals = WMB * 2 * 4 * (RAW ? 2 : 1);     // values per lane
+    static_assert(4 * 64 * kVals * 4 <= (int)sizeof(ring), "exchange fits in the ring");
+    uint32_t* xch = reinterpret_cast<uint32_t*>(&ring[0]);
+    __syncthreads();
+    if (half == 1) {
+#pragma unroll
+        for (int i = 0; i < WMB; ++i)
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int v = (i * 2 + c) * 4 + r;
+                    if constexpr (RAW) {
+                        xch[((w4 * kVals) + 2 * v) * 64 + lane] = (uint32_t)iacc[i][c][r];
+                        xch[((w4 * kVals) + 2 * v + 1) * 64 + lane] = (uint32_t)racc[i][c][r];
+                    } else {
+                        xch[((w4 * kVals) + v) * 64 + lane] = __float_as_uint(acc[i][c][r]);
+                    }
+                }
+    }
+    __syncthreads();
+    if (half == 1) return;
+#pragma unroll
+    for (int i = 0; i < WMB; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int m = m0 + wrow + 16 * i + 4 * lq + r;
+            if (m >= M) continue;
+            const float sx = RAW ? 0.f : half_bits_to_float(a.s_x[m]);
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                const int n = n0 + 32 * wn + 16 * c + lrow;
+                const int v = (i * 2 + c) * 4 + r;
+                if constexpr (RAW) {
+                    a.Tb[(int64_t)m * N + n] = iacc[i][c][r] + (int32_t)xch[((w4 * kVals) + 2 * v) * 64 + lane];
+                    a.Tr[(int64_t)m * N + n] = racc[i][c][r] + (int32_t)xch[((w4 * kVals) + 2 * v + 1) * 64 + lane];
+                } else {
+                    const float sum = acc[i][c][r] + __uint_as_float(xch[((w4 * kVals) + v) * 64 + lane]);
+                    a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(sx * sum);
+                }
+            }
+        }
+}
+
+// --------------------------------------------------------------------------
 // Skinny kernel: 16 * WN output columns per workgroup, all M (<= 16 * WM)
 // rows, the K-loop split over NW waves.
 // --------------------------------------------------------------------------
@@ -889,15 +1148,64 @@ static bool large_tiles_fit(int M, int N) {
     return N % 256 == 0 && (int64_t)((M + 255) / 256) * (N / 256) >= kLargeTileMinTiles;
 }
 
+// Buffer resource words (as buf_desc), built on the host.
+static i32x4 host_buf_desc(const void* base, uint32_t bytes) {
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    return i32x4{(int)(uint32_t)b, (int)((uint32_t)(b >> 32) & 0xFFFFu), (int)bytes, 0x00020000};
+}
+
+// AUTO takes the medium kernel where the 128 x 128 tiles would need split-K
+// to give every CU two workgroups, as long as its 64 x 64 tiles fit on the
+// CUs in one round (one workgroup per CU: its ring takes most of the LDS).
+constexpr int kMediumTargetWGs = 512;
+constexpr int kCUs = 256;
+static bool medium_preferred(int M, int N) {
+    return (int64_t)((M + kTB - 1) / kTB) * (N / kTB) < kMediumTargetWGs &&
+           (int64_t)((M + 63) / 64) * (N / 64) <= kCUs;
+}
+
 template <bool RAW>
-static mq_status launch(mq_variant variant, const GemmArgs& a, void* workspace, size_t ws_bytes,
+static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspace, size_t ws_bytes,
                         hipStream_t stream) {
+    // whole-operand buffer resources take 32-bit offsets (and offsets from
+    // 2 GB up serve as "past the end")
+    GemmArgs a = args;
+    const uint64_t G = (uint64_t)(a.K / kGroup);
+    const uint64_t sizes[5] = {G * a.M * kGroupBytes, G * a.N * kGroupBytes, (uint64_t)a.nnzb * kTB * kGroupBytes,
+                               G * a.N * 2, (uint64_t)a.nnzb * kTB * 2};
+    for (uint64_t b : sizes)
+        if (b >= (1ull << 31)) return MQ_ERR_UNSUPPORTED_SHAPE;
+    a.xq_bytes = (uint32_t)sizes[0];
+    a.wq_bytes = (uint32_t)sizes[1];
+    a.rq_bytes = (uint32_t)sizes[2];
+    a.sw_bytes = RAW ? 0u : (uint32_t)sizes[3];
+    a.sr_bytes = RAW ? 0u : (uint32_t)sizes[4];
+    // a resource over an absent operand has a valid base and no bytes
+    auto desc = [&](const void* p, uint32_t bytes) {
+        return host_buf_desc(p ? p : (const void*)a.Wq, p ? bytes : 0u);
+    };
+    a.rx = desc(a.Xq, a.xq_bytes);
+    a.rw = desc(a.Wq, a.wq_bytes);
+    a.rr = desc(a.Rq, a.rq_bytes);
+    a.rsw = desc(a.s_w, a.sw_bytes);
+    a.rsr = desc(a.s_r, a.sr_bytes);
     if (variant == MQ_VARIANT_AUTO)
         variant = a.M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY
-                  : large_tiles_fit(a.M, a.N) ? MQ_VARIANT_TILED_LARGE : MQ_VARIANT_TILED;
+                  : large_tiles_fit(a.M, a.N) ? MQ_VARIANT_TILED_LARGE
+                  : medium_preferred(a.M, a.N) ? MQ_VARIANT_MEDIUM : MQ_VARIANT_TILED;
     if (variant == MQ_VARIANT_SKINNY && a.M > kSkinnyMaxM) variant = MQ_VARIANT_TILED;
     if (variant == MQ_VARIANT_TILED_LARGE && a.N % 256 != 0) variant = MQ_VARIANT_TILED;
-    if (variant == MQ_VARIANT_TILED_LARGE) {
+    if (variant == MQ_VARIANT_MEDIUM) {
+        // one workgroup per CU (its ring takes most of the LDS): 64-row tiles
+        // when they alone give every CU one, else 32-row ones
+        const int64_t t64 = (int64_t)((a.M + 63) / 64) * (a.N / 64);
+        const int64_t t32 = (int64_t)((a.M + 31) / 32) * (a.N / 64);
+        if (t32 > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
+        if (t64 >= kCUs)
+            hipLaunchKernelGGL((gemm_medium_kernel<2, RAW>), dim3((unsigned)t64), dim3(512), 0, stream, a);
+        else
+            hipLaunchKernelGGL((gemm_medium_kernel<1, RAW>), dim3((unsigned)t32), dim3(512), 0, stream, a);
+    } else if (variant == MQ_VARIANT_TILED_LARGE) {
         using TS = TileShape<8, 4>;
         const int64_t tiles = (int64_t)((a.M + TS::kTM - 1) / TS::kTM) * (a.N / TS::kTN);
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
@@ -967,7 +1275,7 @@ extern "C" mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int
                                            void* Y, int ldy,
                                            void* workspace, size_t ws_bytes, hipStream_t stream) {
     (void)workspace;
-    if (variant < MQ_VARIANT_AUTO || variant > MQ_VARIANT_TILED_LARGE) return MQ_ERR_INVALID_ARG;
+    if (variant < MQ_VARIANT_AUTO || variant > MQ_VARIANT_MEDIUM) return MQ_ERR_INVALID_ARG;
     mq_status st = check_common(M, N, K, Xq, Wq, res_rowptr, res_kb, nnzb, Rq);
     if (st != MQ_OK) return st;
     if (ldy < N || ldy % 8 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
@@ -980,6 +1288,7 @@ extern "C" mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int
     GemmArgs a{M, N, K, Xq, static_cast<const uint16_t*>(s_x), Wq, static_cast<const uint16_t*>(s_w),
                nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq, static_cast<const uint16_t*>(s_r),
                static_cast<uint16_t*>(Y), ldy, nullptr, nullptr};
+    a.nnzb = nnzb;
     return launch<false>(variant, a, workspace, ws_bytes, stream);
 }
 
@@ -1000,7 +1309,7 @@ extern "C" mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int
                                            const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
                                            const uint8_t* Rq,
                                            int32_t* Tb, int32_t* Tr, hipStream_t stream) {
-    if (variant < MQ_VARIANT_AUTO || variant > MQ_VARIANT_TILED_LARGE) return MQ_ERR_INVALID_ARG;
+    if (variant < MQ_VARIANT_AUTO || variant > MQ_VARIANT_MEDIUM) return MQ_ERR_INVALID_ARG;
     mq_status st = check_common(M, N, K, Xq, Wq, res_rowptr, res_kb, nnzb, Rq);
     if (st != MQ_OK) return st;
     if (M == 0) return MQ_OK;
@@ -1008,6 +1317,7 @@ extern "C" mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int
     if (!mq_host::aligned(Tb, 4) || !mq_host::aligned(Tr, 4)) return MQ_ERR_MISALIGNED;
     GemmArgs a{M, N, K, Xq, nullptr, Wq, nullptr, nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq,
                nullptr, nullptr, 0, Tb, Tr};
+    a.nnzb = nnzb;
     return launch<true>(variant, a, nullptr, 0, stream);
 }
 

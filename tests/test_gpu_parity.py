@@ -216,7 +216,7 @@ GEMM_CASES = [
 
 
 def _variants(M, N=128):
-    vs = ["skinny", "tiled", "auto"] if M <= 32 else ["tiled", "auto"]
+    vs = ["skinny", "tiled", "medium", "auto"] if M <= 32 else ["tiled", "medium", "auto"]
     if N % 256 == 0:
         vs.append("tiled_large")            # 256 x 256 tiles (AUTO takes them on large problems)
     return vs
@@ -277,7 +277,7 @@ def test_gemm_quantized_layer_matches_oracle(tc, mq, orc):
     pw = mq.prepare_weight(dev(tc, W), L.nnzb)
     Y = mq.linear(dev(tc, X), pw)
     Xq, s_x = mq.quantize_act(dev(tc, X))
-    for v in ("skinny", "tiled", "tiled_large"):
+    for v in ("skinny", "tiled", "tiled_large", "medium"):
         Tb, Tr = mq.fused_gemm_acc_i32(Xq, pw, variant=v)
         assert np.array_equal(host(Tb), Tb_ref) and np.array_equal(host(Tr), Tr_ref)
         assert maxabsrel(mq.fused_gemm(Xq, s_x, pw, variant=v), Y64) <= TIGHT
@@ -304,7 +304,7 @@ def test_gemm_extreme_codes_long_k(tc, mq, orc):
     Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
     assert np.abs(Tb_ref).max() == 49 * K
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
-    for v in ("skinny", "tiled", "tiled_large"):
+    for v in ("skinny", "tiled", "tiled_large", "medium"):
         Tb, Tr = mq.fused_gemm_acc_i32(dev_x(tc, Xq), pw, variant=v)
         Y = mq.fused_gemm(dev_x(tc, Xq), dev(tc, s_x).view(tc.float16), pw, variant=v)
         tc.cuda.synchronize()
@@ -320,7 +320,7 @@ def test_gemm_guard_bands_and_empty(tc, mq, orc):
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
     Xq_d, sx_d = dev_x(tc, Xq), dev(tc, s_x)        # kept alive across the launches
     lib = mq.load()
-    for v in (1, 2, 3):
+    for v in (1, 2, 3, 4):
         if v == 1 and M > 32:
             continue
         canary = 12345
@@ -352,7 +352,7 @@ def test_gemm_no_residual_null_pointers(tc, mq, orc):
     keep = [dev_x(tc, Xq), dev(tc, s_x), dev(tc, layout.block_rows(Wq, K)),
             dev(tc, layout.block_scales(s_w))]               # kept alive across the launches
     lib = mq.load()
-    for v in (1, 2, 3):
+    for v in (1, 2, 3, 4):
         st = lib.mq_fused_gemm_variant(v, M, N, K, *[t.data_ptr() for t in keep], None, None, 0,
                                        None, None, Y.data_ptr(), N, None, 0, None)
         tc.cuda.synchronize()
@@ -366,7 +366,7 @@ def test_gemm_deterministic_and_row_independent(tc, mq, orc):
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=21)
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
     sd = dev(tc, s_x).view(tc.float16)
-    for v in ("tiled", "tiled_large", "skinny"):
+    for v in ("tiled", "tiled_large", "medium", "skinny"):
         rows = M if v != "skinny" else 16
         Xd = dev_x(tc, Xq[:rows])
         Y1 = host(mq.fused_gemm(Xd, sd[:rows].contiguous(), pw, variant=v).view(tc.int16))
