@@ -5,10 +5,11 @@
 // One workgroup of 256 threads per token row.  Each thread owns 32-byte
 // chunks (16 fp16) of the row; the row maximum of |x| is taken on the fp16 bit
 // patterns with the sign cleared (an order-preserving integer max for finite
-// values), reduced across the wave with xor-shuffles and across the four waves
-// through LDS.  Codes are then formed from the registers (rows up to
-// CPT * 4096 elements) or by re-reading the row (longer rows), and written as
-// one folded 8-byte chunk per 16 codes (fold_codes) in the device group order
+// values, packed 16-bit maxima), reduced across the wave with xor-shuffles and
+// across the four waves through LDS.  Codes are then formed from the
+// registers (rows up to CPT * 4096 elements) or by re-reading the row (longer
+// rows), with the division-free exact rounding of quant_mag, and written as
+// one folded 8-byte chunk per 16 codes in the device group order
 // (piece_offset): coalesced 16-byte loads, 8-byte stores.
 #include "mq_device.h"
 
@@ -41,17 +42,15 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
             if (c < nchunks) {
                 v[i][0] = *reinterpret_cast<const uint4*>(row + 16 * c);
                 v[i][1] = *reinterpret_cast<const uint4*>(row + 16 * c + 8);
-                const uint32_t cm0 = chunk_absmax_bits(v[i][0]), cm1 = chunk_absmax_bits(v[i][1]);
-                amax = cm0 > amax ? cm0 : amax;
-                amax = cm1 > amax ? cm1 : amax;
+                const uint32_t cm = chunk_absmax_bits(v[i][0], v[i][1]);
+                amax = cm > amax ? cm : amax;
             }
         }
     } else {
         for (int c = t; c < nchunks; c += kActThreads) {
-            const uint32_t cm0 = chunk_absmax_bits(*reinterpret_cast<const uint4*>(row + 16 * c));
-            const uint32_t cm1 = chunk_absmax_bits(*reinterpret_cast<const uint4*>(row + 16 * c + 8));
-            amax = cm0 > amax ? cm0 : amax;
-            amax = cm1 > amax ? cm1 : amax;
+            const uint32_t cm = chunk_absmax_bits(*reinterpret_cast<const uint4*>(row + 16 * c),
+                                                  *reinterpret_cast<const uint4*>(row + 16 * c + 8));
+            amax = cm > amax ? cm : amax;
         }
     }
     amax = wave_max_u32(amax);

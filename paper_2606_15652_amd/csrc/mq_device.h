@@ -31,6 +31,22 @@ __device__ __forceinline__ uint16_t scale_bits_from_amax(float amax) {
     return float_to_half_bits(amax / (float)kQmax);
 }
 
+// |code| of an fp16 x for an fp16 scale s > 0 (the activation quantiser):
+// min(7, round_half_even(|x| / s)), given inv_s = the correctly rounded fp32
+// 1 / s.  x and s are fp16 values, so a
+// quotient that is not a tie lies at least 2^-14 from every half-integer
+// (2|x| - (2k+1) s is a non-zero multiple of the finer of the two exponents'
+// units).  q0 = |x| inv_s is within 2^-20 of |x| / s; one correction step
+// (r = |x| - q0 s is exact: on a tie q0 - (k + 1/2) is a few units of the
+// last place, times s representable) makes q1 exactly k + 1/2 on a tie and
+// keeps it within 2^-22 otherwise, so rint (ties to even) gives the code.
+__device__ __forceinline__ float quant_mag(float ax, float s, float inv_s) {
+    const float q0 = ax * inv_s;
+    const float r = __builtin_fmaf(-q0, s, ax);
+    const float q1 = __builtin_fmaf(r, inv_s, q0);
+    return fminf(rintf(q1), (float)kQmax);
+}
+
 // Code of x for scale s > 0 (inv_s = 1 / s, rounded any way):
 // clamp(round_half_even(x / s), -7, 7).
 // x is fp16 or fp32 and s is fp16, so the tie points t*s (t = k + 1/2) have at
@@ -109,31 +125,53 @@ constexpr float kCodeScale = 64.0f;
 
 // ------------------------------------------------- activation quantiser --
 // Largest |x| of 8 fp16 values, as fp16 bits with the sign cleared (an
-// order-preserving integer maximum for finite values).
+// order-preserving integer maximum for finite values): packed 16-bit maxima.
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u16x2 abs_bits2(uint32_t w) {
+    return __builtin_bit_cast(u16x2, w & 0x7FFF7FFFu);
+}
+__device__ __forceinline__ u16x2 chunk_absmax2(const uint4 v) {
+    return __builtin_elementwise_max(__builtin_elementwise_max(abs_bits2(v.x), abs_bits2(v.y)),
+                                     __builtin_elementwise_max(abs_bits2(v.z), abs_bits2(v.w)));
+}
 __device__ __forceinline__ uint32_t chunk_absmax_bits(const uint4 v) {
-    uint32_t m = 0;
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        uint32_t lo = w[i] & 0x7FFFu, hi = (w[i] >> 16) & 0x7FFFu;
-        m = lo > m ? lo : m;
-        m = hi > m ? hi : m;
-    }
-    return m;
+    const u16x2 m = chunk_absmax2(v);
+    return m.x > m.y ? m.x : m.y;
+}
+// the same over two 16-byte loads (16 fp16)
+__device__ __forceinline__ uint32_t chunk_absmax_bits(const uint4 v0, const uint4 v1) {
+    const u16x2 m = __builtin_elementwise_max(chunk_absmax2(v0), chunk_absmax2(v1));
+    return m.x > m.y ? m.x : m.y;
 }
 
 // 16 fp16 (two 16-byte loads) -> 16 codes for scale s (inv_s = 1 / s) -> one
-// folded chunk.
+// folded chunk.  Each 6-bit field is the code's magnitude with x's sign bit
+// at bit 5 when the code is not zero (as fold_codes writes it), laid out at
+// bit 6e of the 96-bit word and folded.
+__device__ __forceinline__ uint32_t code_field(uint32_t h16, float s, float inv_s) {
+    // quant_mag's steps on the signed value (every step is sign-symmetric);
+    // adding +0 turns a negative zero into +0, so the sign bit of q is set
+    // exactly for the negative codes
+    const float x = half_bits_to_float((uint16_t)h16);
+    const float q0 = x * inv_s;
+    const float r = __builtin_fmaf(-q0, s, x);
+    const float q = rintf(__builtin_fmaf(r, inv_s, q0)) + 0.0f;
+    const uint32_t m = min((uint32_t)fabsf(q), (uint32_t)kQmax);
+    return m | ((__float_as_uint(q) >> 31) << 5);
+}
 __device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, float s, float inv_s) {
     if (s == 0.0f) return make_uint2(0u, 0u);
     const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-    int q[16];
+    uint32_t f[16];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        q[2 * i] = quant_code(half_bits_to_float((uint16_t)(w[i] & 0xFFFFu)), s, inv_s);
-        q[2 * i + 1] = quant_code(half_bits_to_float((uint16_t)(w[i] >> 16)), s, inv_s);
+        f[2 * i] = code_field(w[i] & 0xFFFFu, s, inv_s);
+        f[2 * i + 1] = code_field(w[i] >> 16, s, inv_s);
     }
-    return fold_codes(q);
+    const uint32_t o0 = f[0] | (f[1] << 6) | (f[2] << 12) | (f[3] << 18) | (f[4] << 24) | (f[5] << 30);
+    const uint32_t o1 = (f[5] >> 2) | (f[6] << 4) | (f[7] << 10) | (f[8] << 16) | (f[9] << 22) | (f[10] << 28);
+    const uint32_t o2 = (f[10] >> 4) | (f[11] << 2) | (f[12] << 8) | (f[13] << 14) | (f[14] << 20) | (f[15] << 26);
+    return make_uint2(o0 | (o2 & kFoldA), o1 | (o2 & kFoldB));
 }
 
 // ----------------------------------------------------- device group order --

@@ -133,6 +133,33 @@ def test_act_quant_parity(tc, mq, orc, M, K):
     assert np.array_equal(orc.unblock_rows(host(Xq), K), Xq_ref)
 
 
+def test_act_quant_exact_ties(tc, mq, orc):
+    """Every tie (k + 1/2) s, k = 0..6, both signs, and its fp16 neighbours,
+    over 256 scales s = j 2^e with a 7-bit j (so (k + 1/2) s and 7 s are
+    halves): the codes are round-half-even, bit-exact against the oracle."""
+    rng = np.random.default_rng(77)
+    rows = []
+    for r in range(256):
+        j = int(rng.integers(1, 128))
+        e = int(rng.integers(-20, 6))
+        s = np.float16(j * 2.0 ** e)
+        if not np.isfinite(s) or s == 0 or np.float16(7 * float(s)) != 7 * float(s):
+            s = np.float16(0.125)
+        row = [np.float16(7 * float(s))]                       # the row maximum: scale s
+        for k in range(7):
+            t = np.float16((k + 0.5) * float(s))
+            assert float(t) == (k + 0.5) * float(s)
+            for v in (t, np.nextafter(t, np.float16(0)), np.nextafter(t, np.float16(np.inf))):
+                row += [v, -v]
+        row = np.array(row, np.float16)
+        rows.append(np.concatenate([row, np.zeros(128 - len(row), np.float16)]))
+    X = np.stack(rows)
+    Xq, s_x = mq.quantize_act(dev(tc, X))
+    Xq_ref, sx_ref = orc.quantize_act(X)
+    assert np.array_equal(half_bits(s_x), sx_ref)
+    assert np.array_equal(orc.unblock_rows(host(Xq), 128), Xq_ref)
+
+
 def test_act_quant_strided(tc, mq, orc):
     X = synth.gen_act(9, 640, 5)
     Xbig = np.zeros((9, 1024), np.float16)
