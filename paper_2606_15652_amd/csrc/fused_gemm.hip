@@ -110,32 +110,36 @@ __device__ __forceinline__ void group_row(const i32x8 a, const i32x8 (&w)[WN], c
 // --------------------------------------------------------------------------
 // Tiled kernel
 // --------------------------------------------------------------------------
-// Workgroup: 4 waves (2 along M x 2 along N) owning a 128 x 128 output tile,
-// i.e. exactly one 128-row block row of the residual; each wave owns 64 x 64
-// (4 x 4 sub-tiles of 16 x 16, 64 fp32 accumulators).  Two workgroups share a
-// CU, so one can compute while the other waits at its barrier.
+// Workgroup: 2 x WAVES_N waves owning a (32 WMB) x (64 WAVES_N) output tile:
+// <8, 4> is 256 x 256 with eight waves, one workgroup per CU; <4, 2> is
+// 128 x 128 with four waves, two per CU.  Wave (wm, wn) owns WMB sub-tile
+// rows of 16 and four 16-column sub-tiles at tile columns 16 (wn + WAVES_N c),
+// interleaved so that every wave has sub-tiles in each 128-column residual
+// block row of the tile.
 //
-// Per 128-K group the packed X tile (128 x 64 B), W tile (128 x 64 B), the
-// group's 128 weight scales and, when the block row has a residual block at
-// this group, the R tile and its 128 scales go by LDS DMA (buffer loads that
-// write LDS directly, no staging registers) into one slot of a 3-stage ring:
-// at iteration g the waves wait for group g's loads, meet at the barrier that
-// also frees the slot of group g-1, and compute g, issuing the loads of group
-// g+2 into that slot a few at a time between the MFMA rows (a wave that
-// issued all of them at once would stall at issue while the memory pipeline
-// drains).  The DMA does not raise the compiler's wait counters, so the
+// Per 128-K group the packed X tile, W tile, the group's weight scales and,
+// for block rows with a residual block at this group, the R tiles and their
+// scales go by LDS DMA (buffer loads that write LDS directly, no staging
+// registers) into one slot of a 3-stage ring.  One barrier per group, in the
+// middle of the dense pass: it publishes group g + 1 (each wave first waits
+// for its own loads) and frees the slot of group g - 1, into which the waves
+// with wm == 0 then issue the loads of group g + 2; every wave reads its next
+// group's W fragments, scales and first A fragment into registers right
+// after it.  The DMA does not raise the compiler's wait counters, so the
 // kernel waits on the vector-memory counter itself (wait_loads_and_sync).
 //
 // Loads use per-tile buffer resources over operands in device group order, so
-// each load instruction reads 1 KB of whole 64-byte rows, contiguous.  16-byte chunks are XOR-swizzled
-// by (row >> 1) & 3 inside 64-byte rows, which makes the 16-lane fragment
-// reads conflict-free (LDS serves 8 lanes of 16 B per 128-byte bank window).
+// each load instruction reads 1 KB of whole 64-byte rows, contiguous.  16-byte
+// chunks are XOR-swizzled by (row >> 1) & 3 inside 64-byte rows, which makes
+// the 16-lane fragment reads conflict-free (LDS serves 8 lanes of 16 B per
+// 128-byte bank window).
 //
-// The residual runs as a second straight-line phase of the same group: the
-// wave re-reads the staged X fragments and accumulates into the same
-// registers.  With split-K (SPLIT), workgroup z handles a contiguous run of
-// groups and writes fp32 partial sums; reduce_splits_kernel adds them in split
-// order (deterministic) and applies s_x.
+// After the dense pass, one residual pass per block row with a block at this
+// group: every wave re-reads the staged X fragments and multiplies its
+// sub-tiles of that block row, accumulating into the same registers.  With
+// split-K (SPLIT), workgroup z handles a contiguous run of groups and writes
+// fp32 partial sums; reduce_splits_kernel adds them in split order
+// (deterministic) and applies s_x.
 constexpr int kTB = 128;
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
