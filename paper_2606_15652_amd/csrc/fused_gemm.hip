@@ -724,32 +724,29 @@ __global__ __launch_bounds__(512) void gemm_medium_kernel(GemmArgs a) {
         }
     const int wrow = 16 * WMB * wm;
 
-    // one group (HAS_RES: with its residual block, sharing the A fragments)
-    auto compute = [&](const Slot& S, auto has_res) {
-        constexpr bool HR = decltype(has_res)::value;
-        i32x8 b[2], rb[2];
-        float bs[2], rs[2];
+    // One pass over a staged group: the dense pass (RES false) multiplies the
+    // X tile with the W tile, the residual pass (RES true) with the R tile.
+    // Passes rather than one variant with both: a single code path per pass
+    // keeps the accumulators in fixed registers.
+    auto compute = [&](const Slot& S, auto res) {
+        constexpr bool RES = decltype(res)::value;
+        const uint8_t* bt = RES ? S.r : S.w;
+        const uint16_t* st = RES ? S.sr : S.sw;
+        i32x8 b[2];
+        float bs[2];
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
             const int col = 32 * wn + 16 * c + lrow;       // row of the W and R tiles
-            const int off = col * kRow + (swz(col, lq) << 4);
-            b[c] = unfold_codes(*reinterpret_cast<const uint4*>(&S.w[off]));
-            bs[c] = RAW ? 0.f : half_bits_to_float(S.sw[col]) * kCodeScale;
-            if constexpr (HR) {
-                rb[c] = unfold_codes(*reinterpret_cast<const uint4*>(&S.r[off]));
-                rs[c] = RAW ? 0.f : half_bits_to_float(S.sr[col]) * kCodeScale;
-            }
+            b[c] = unfold_codes(*reinterpret_cast<const uint4*>(&bt[col * kRow + (swz(col, lq) << 4)]));
+            bs[c] = RAW ? 0.f : half_bits_to_float(st[col]) * kCodeScale;
         }
-        f32x4 t[WMB][2], tr[WMB][2];
+        f32x4 t[WMB][2];
 #pragma unroll
         for (int i = 0; i < WMB; ++i) {
             const int row = wrow + 16 * i + lrow;
             const i32x8 av = unfold_codes(*reinterpret_cast<const uint4*>(&S.x[row * kRow + (swz(row, lq) << 4)]));
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                t[i][c] = mfma_codes(av, b[c], f32x4{0.f, 0.f, 0.f, 0.f});
-                if constexpr (HR) tr[i][c] = mfma_codes(av, rb[c], f32x4{0.f, 0.f, 0.f, 0.f});
-            }
+            for (int c = 0; c < 2; ++c) t[i][c] = mfma_codes(av, b[c], f32x4{0.f, 0.f, 0.f, 0.f});
         }
 #pragma unroll
         for (int i = 0; i < WMB; ++i)
@@ -757,21 +754,14 @@ __global__ __launch_bounds__(512) void gemm_medium_kernel(GemmArgs a) {
             for (int c = 0; c < 2; ++c) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    if constexpr (RAW) {
-                        iacc[i][c][r] += (int)(t[i][c][r] * kCodeScale);   // exact
-                        if constexpr (HR) racc[i][c][r] += (int)(tr[i][c][r] * kCodeScale);
-                    } else {
-                        acc[i][c][r] = __builtin_fmaf(bs[c], t[i][c][r], acc[i][c][r]);
-                        if constexpr (HR) acc[i][c][r] = __builtin_fmaf(rs[c], tr[i][c][r], acc[i][c][r]);
-                    }
+                    if constexpr (!RAW) acc[i][c][r] = __builtin_fmaf(bs[c], t[i][c][r], acc[i][c][r]);
+                    else if constexpr (!RES) iacc[i][c][r] += (int)(t[i][c][r] * kCodeScale);   // exact
+                    else racc[i][c][r] += (int)(t[i][c][r] * kCodeScale);
                 }
-                // the group's epilogue completes inside this block (see pin)
-                if constexpr (!RAW) {
-                    pin(acc[i][c]);
-                } else {
-                    pin(iacc[i][c]);
-                    if constexpr (HR) pin(racc[i][c]);
-                }
+                // the pass's epilogue completes inside this block (see pin)
+                if constexpr (!RAW) pin(acc[i][c]);
+                else if constexpr (!RES) pin(iacc[i][c]);
+                else pin(racc[i][c]);
             }
     };
 
@@ -787,17 +777,18 @@ __global__ __launch_bounds__(512) void gemm_medium_kernel(GemmArgs a) {
         res |= ((p0 >= 0 ? 1u : 0u) | (p1 >= 0 ? 2u : 0u)) << (2 * j);
     }
     for (int g = 0; g < G; g += 2) {
-        // this wave's loads of pair g / 2 landed (those of the next two pairs
-        // may stay in flight); everyone finished the previous pair, whose
-        // slots are refilled next
+        // this wave's loads of pair g / 2 landed (its base loads of the next two
+        // pairs may stay in flight: counting only those is exact without
+        // residual blocks there and waits a little longer with them);
+        // everyone finished the previous pair, whose slots are refilled next
         const int gh = g + half;
-        wait_vm_and_sync(loads(gh + 2, (res >> (half + 2)) & 1u) + loads(gh + 4, (res >> (half + 4)) & 1u));
+        wait_vm_and_sync(loads(gh + 2, false) + loads(gh + 4, false));
         const int p0 = next_block(g + 6), p1 = next_block(g + 7);
         if (gh + 6 < G) issue(gh + 6, half ? p1 : p0);
         res |= ((p0 >= 0 ? 1u : 0u) | (p1 >= 0 ? 2u : 0u)) << 6;
         if (gh < G) {
+            compute(ring[gh & (kStages - 1)], std::false_type{});
             if ((res >> half) & 1u) compute(ring[gh & (kStages - 1)], std::true_type{});
-            else compute(ring[gh & (kStages - 1)], std::false_type{});
         }
         res >>= 2;
     }
