@@ -71,6 +71,9 @@ def parse():
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="fold the counter_collection.csv files of two --traffic runs (FETCH_SIZE, "
                          "WRITE_SIZE) into profiles/fused_gemm_traffic.json; needs no GPU")
+    ap.add_argument("--families", action="store_true",
+                    help="time the fused GEMM and the whole layer call on every layer of the other "
+                         "workload families (one JSON line per layer and M; not the headline line)")
     ap.add_argument("--traffic", action="store_true",
                     help="counter run: eager fused GEMM launches at the largest M, then a plain "
                          "256 MiB device copy as the scale reference for FETCH_SIZE / WRITE_SIZE")
@@ -137,6 +140,107 @@ def summarize_traffic(fetch_csv, write_csv, m):
     print(json.dumps(out))
 
 
+def graph_of(torch, fn, calls):
+    """Capture `calls` back-to-back invocations of fn in one HIP graph."""
+    fn()                                   # warm the libraries outside capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(calls):
+            fn()
+    torch.cuda.synchronize()
+    return g
+
+
+def timed(torch, fn, reps):
+    """Average microseconds per call of fn: reps calls replayed from a HIP
+    graph (no host launch overhead in the timed region), HIP events on the
+    replay stream."""
+    g = graph_of(torch, fn, reps)
+    g.replay()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    g.replay()
+    t1.record()
+    t1.synchronize()
+    return t0.elapsed_time(t1) * 1e3 / reps
+
+
+def families(args):
+    """Per-layer timings of the workload families other than the headline
+    layer: fused GEMM (AUTO variant), the whole layer call (mq_linear) and
+    hipBLASLt W16A16 on the same shape, weights rotating through more than
+    512 MB of copies (at least two).  One JSON line per layer and M."""
+    import torch
+
+    import paper_2606_15652_amd as mq
+    import synth
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    mq.load()
+    dev = torch.device("cuda:0")
+    wcache = {}
+    for layer in synth.workloads():
+        if layer.name == "c2_4096":
+            continue
+        K, N, nnzb = layer.K, layer.N, layer.nnzb
+        key = (K, N, layer.seed, layer.skewed)
+        if key not in wcache:            # the density sweep shares one weight per shape
+            wcache.clear()
+            wcache[key] = torch.from_numpy(layer.weight()).to(dev)
+        W = wcache[key]
+        pw0 = mq.prepare_weight(W, nnzb)
+        torch.cuda.synchronize()
+        ncopy = max(2, -(-ROTATE_BYTES // pw0.nbytes))
+        copies = [pw0] + [mq.PackedWeight(N, K, pw0.Wq.clone(), pw0.s_w.clone(), pw0.rowptr.clone(),
+                                          pw0.kb.clone(), pw0.Rq.clone(), pw0.s_r.clone())
+                          for _ in range(ncopy - 1)]
+        rot = [0]
+
+        def next_pw():
+            rot[0] = (rot[0] + 1) % ncopy
+            return copies[rot[0]]
+
+        nb = max(2, -(-ROTATE_BYTES // (N * K * 2)))
+        wbs = [W.to(torch.float16)] + [None] * (nb - 1)
+        for i in range(1, nb):
+            wbs[i] = wbs[0].clone()
+        rb = [0]
+
+        def next_wb():
+            rb[0] = (rb[0] + 1) % nb
+            return wbs[rb[0]]
+
+        for m in layer.ms:
+            X = torch.from_numpy(layer.act(m)).to(dev)
+            Xq = torch.empty((m, K // 2), dtype=torch.uint8, device=dev)
+            sx = torch.empty((m,), dtype=torch.float16, device=dev)
+            Y = torch.empty((m, N), dtype=torch.float16, device=dev)
+            ws = torch.empty(max(1, mq.linear_workspace_bytes(m, N, K)), dtype=torch.uint8, device=dev)
+            mq.quantize_act(X, out=(Xq, sx))
+            reps = max(5, min(args.reps, int(2e5 // max(1.0, m * N * K / 1e9))))
+            t_gemm = timed(torch, lambda: mq.fused_gemm(Xq, sx, next_pw(), out=Y), reps)
+            t_call = timed(torch, lambda: mq.linear(X, next_pw(), out=Y, workspace=ws), reps)
+            t_blas = None if args.no_blas else timed(torch, lambda: torch.nn.functional.linear(X, next_wb()), reps)
+            ops, byts = algorithmic(m, N, K, nnzb)
+            row = {"layer": layer.name, "K": K, "N": N, "M": m, "density_pct": layer.density_pct,
+                   "nnzb": nnzb, "skewed": layer.skewed, "us_gemm": round(t_gemm, 3),
+                   "us_call": round(t_call, 3),
+                   "eff_tops": round(2.0 * m * N * K / (t_gemm * 1e-6) / 1e12, 2),
+                   "int8_peak_frac": round(ops / (t_gemm * 1e-6) / 1e12 / PEAK_I8_TOPS, 4),
+                   "hbm_frac": round(byts / (t_gemm * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+            if t_blas is not None:
+                row["us_w16a16"] = round(t_blas, 3)
+                row["speedup_vs_w16a16"] = round(t_blas / t_call, 3)
+            print(json.dumps(row), flush=True)
+            del X, Xq, sx, Y, ws
+        del copies, pw0, wbs
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.summarize_traffic:
@@ -148,6 +252,9 @@ def main():
         sys.exit(2)
     if args.quick:
         args.steps, args.warmup, args.reps = 3, 1, 5
+    if args.families:
+        families(args)
+        return
 
     import numpy as np
     import torch
@@ -190,30 +297,6 @@ def main():
         for m in ms:
             mq.linear(Xs[m], next_pw(), out=Ys[m], workspace=Ws[m])
 
-    def graph_of(fn, calls):
-        """Capture `calls` back-to-back invocations of fn in one HIP graph."""
-        fn()                                   # warm the libraries outside capture
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for _ in range(calls):
-                fn()
-        torch.cuda.synchronize()
-        return g
-
-    def timed(fn, reps):
-        """Average microseconds per call of fn: reps calls replayed from a HIP
-        graph (no host launch overhead in the timed region), HIP events on the
-        replay stream."""
-        g = graph_of(fn, reps)
-        g.replay()
-        torch.cuda.synchronize()
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0.record()
-        g.replay()
-        t1.record()
-        t1.synchronize()
-        return t0.elapsed_time(t1) * 1e3 / reps
 
     if args.traffic:
         # For rocprofv3 --pmc: TRAFFIC_CALLS GEMM dispatches at the largest M,
@@ -235,10 +318,10 @@ def main():
 
     # ------------------------------------------------------------ timed steps
     # one graph replay = `steps` steps; warm-up replays of a separate graph
-    warm = graph_of(step, max(1, args.warmup))
+    warm = graph_of(torch, step, max(1, args.warmup))
     warm.replay()
     torch.cuda.synchronize()
-    main_graph = graph_of(step, args.steps)
+    main_graph = graph_of(torch, step, args.steps)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     wall0 = time.perf_counter()
@@ -256,9 +339,9 @@ def main():
     rows = []
     for m in ms:
         ops, byts = algorithmic(m, N, K, nnzb)
-        t_call = timed(lambda: mq.linear(Xs[m], next_pw(), out=Ys[m], workspace=Ws[m]), args.reps)
-        t_q = timed(lambda: mq.quantize_act(Xs[m], out=(Xqs[m], sxs[m])), args.reps)
-        t_gemm = timed(lambda: mq.fused_gemm(Xqs[m], sxs[m], next_pw(), out=Ys[m]), args.reps)
+        t_call = timed(torch, lambda: mq.linear(Xs[m], next_pw(), out=Ys[m], workspace=Ws[m]), args.reps)
+        t_q = timed(torch, lambda: mq.quantize_act(Xs[m], out=(Xqs[m], sxs[m])), args.reps)
+        t_gemm = timed(torch, lambda: mq.fused_gemm(Xqs[m], sxs[m], next_pw(), out=Ys[m]), args.reps)
         row = {"M": m, "us_call": round(t_call, 3), "us_gemm": round(t_gemm, 3), "us_quant": round(t_q, 3),
                "eff_tops": round(2.0 * m * N * K / (t_gemm * 1e-6) / 1e12, 2),
                "int8_peak_frac": round(ops / (t_gemm * 1e-6) / 1e12 / PEAK_I8_TOPS, 4),
@@ -280,7 +363,7 @@ def main():
         for row in rows:
             m = row["M"]
             x16 = Xs[m]
-            t = timed(lambda: torch.nn.functional.linear(x16, next_wb()), args.reps)
+            t = timed(torch, lambda: torch.nn.functional.linear(x16, next_wb()), args.reps)
             row["us_w16a16"] = round(t, 3)
             row["w16a16_tops"] = round(2.0 * m * N * K / (t * 1e-6) / 1e12, 2)
             row["speedup_vs_w16a16"] = round(t / row["us_call"], 3)
