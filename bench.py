@@ -56,6 +56,7 @@ COPY_BYTES = 256 << 20         # size of the reference copy in a --traffic run
 CPU_MIN_S = 10.0               # cpu_baseline repeats whole steps for at least this long
 CPU_MAX_STEPS = 8
 GEMM_SRC = os.path.join(ROOT, "paper_2606_15652_amd", "csrc", "fused_gemm.hip")
+XCDS, SIMDS = 8, 1024          # MI355X: 8 XCDs, 256 CUs x 4 SIMDs
 
 
 def parse():
@@ -74,6 +75,14 @@ def parse():
     ap.add_argument("--families", action="store_true",
                     help="time the fused GEMM and the whole layer call on every layer of the other "
                          "workload families (one JSON line per layer and M; not the headline line)")
+    ap.add_argument("--kernel-run", metavar="SPECS",
+                    help="counter / trace run: comma-separated layer:M[:variant] specs; per spec, "
+                         "--calls eager fused GEMM launches (rotating weight copies), then a "
+                         "plain 256 MiB elementwise kernel as the byte-counter reference")
+    ap.add_argument("--calls", type=int, default=8, help="GEMM launches per spec in --kernel-run")
+    ap.add_argument("--summarize-counters", nargs="+", metavar=("OUT_MD", "CSV"),
+                    help="fold the counter_collection.csv files of --kernel-run passes into a "
+                         "markdown table OUT_MD (needs no GPU); SPECS from --kernel-run")
     ap.add_argument("--traffic", action="store_true",
                     help="counter run: eager fused GEMM launches at the largest M, then a plain "
                          "256 MiB device copy as the scale reference for FETCH_SIZE / WRITE_SIZE")
@@ -138,6 +147,141 @@ def summarize_traffic(fetch_csv, write_csv, m):
         json.dump(out, f, indent=1)
         f.write("\n")
     print(json.dumps(out))
+
+
+def parse_specs(text):
+    out = []
+    for item in text.split(","):
+        f = item.strip().split(":")
+        out.append((f[0], int(f[1]), f[2] if len(f) > 2 else "auto"))
+    return out
+
+
+def kernel_run(args):
+    """Eager launches for rocprofv3 (--pmc or --kernel-trace): for each spec,
+    the layer's weights prepared on the GPU and copied until the copies exceed
+    ROTATE_BYTES, activations quantised, then args.calls fused GEMM launches,
+    each on the next copy (so the weights come from HBM, not the last-level
+    cache); finally TRAFFIC_CALLS elementwise kernels that read and write
+    COPY_BYTES each, the reference that scales the byte counters."""
+    import torch
+
+    import paper_2606_15652_amd as mq
+    import synth
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    mq.load()
+    dev = torch.device("cuda:0")
+    for name, m, variant in parse_specs(args.kernel_run):
+        layer = synth.workload(name)
+        K, N = layer.K, layer.N
+        pw0 = mq.prepare_weight(torch.from_numpy(layer.weight()).to(dev), layer.nnzb)
+        ncopy = max(2, -(-ROTATE_BYTES // pw0.nbytes))
+        copies = [pw0] + [mq.PackedWeight(N, K, pw0.Wq.clone(), pw0.s_w.clone(), pw0.rowptr.clone(),
+                                          pw0.kb.clone(), pw0.Rq.clone(), pw0.s_r.clone())
+                          for _ in range(ncopy - 1)]
+        Xq, sx = mq.quantize_act(torch.from_numpy(layer.act(m)).to(dev))
+        Y = torch.empty((m, N), dtype=torch.float16, device=dev)
+        ws = torch.empty(max(1, mq.load().mq_fused_gemm_workspace_size(m, N, K)), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        for i in range(args.calls):
+            mq.fused_gemm(Xq, sx, copies[(i + 1) % ncopy], out=Y, variant=variant, workspace=ws)
+        torch.cuda.synchronize()
+        print(json.dumps({"spec": f"{name}:{m}:{variant}", "K": K, "N": N, "M": m, "nnzb": layer.nnzb,
+                          "calls": args.calls}), flush=True)
+        del copies, pw0, Xq, sx, Y, ws
+        torch.cuda.empty_cache()
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(TRAFFIC_CALLS):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"reference": "neg", "bytes_read": COPY_BYTES, "bytes_written": COPY_BYTES,
+                      "calls": TRAFFIC_CALLS}), flush=True)
+
+
+def summarize_counters(args):
+    """Per spec of a --kernel-run: the median per dispatch of every counter
+    over its GEMM launches (dispatches of kernels named gemm_* / reduce_*,
+    grouped into consecutive runs, one run per spec), and derived figures:
+    matrix-core ops from SQ_INSTS_VALU_MFMA_MOPS_F6F4 (x 512), MFMA busy
+    fraction SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / XCDs x 1024 SIMDs),
+    VALU instructions other than MFMA per MFMA, and HBM bytes from FETCH_SIZE,
+    WRITE_SIZE and TCC_EA0_RDREQ_DRAM scaled by what the same counter reads
+    for the reference kernel of known bytes."""
+    import csv
+    import statistics
+
+    out_md, csvs = args.summarize_counters[0], args.summarize_counters[1:]
+    specs = parse_specs(args.kernel_run)
+    per = [dict() for _ in specs]       # spec index -> counter -> median per dispatch
+    ref = {}
+    for path in csvs:
+        disp = {}
+        for r in csv.DictReader(open(path)):
+            d = int(r["Dispatch_Id"])
+            e = disp.setdefault(d, {"name": r["Kernel_Name"], "grid": r.get("Grid_Size", ""), "c": {}})
+            e["c"][r["Counter_Name"]] = e["c"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        order = sorted(disp)
+        gemm = [d for d in order if "gemm_" in disp[d]["name"] or "reduce_splits" in disp[d]["name"]]
+        runs = []                           # maximal runs of consecutive GEMM dispatch ids
+        for d in gemm:
+            if runs and d == runs[-1][-1] + 1:
+                runs[-1].append(d)
+            else:
+                runs.append([d])
+        runs = [r for r in runs if len(r) >= args.calls]
+        if len(runs) != len(specs):
+            raise SystemExit(f"{path}: {len(runs)} GEMM dispatch runs for {len(specs)} specs")
+        for i, run in enumerate(runs):
+            per_launch = len(run) // args.calls          # 2 with a split-K reduction
+            launches = [run[j:j + per_launch] for j in range(0, per_launch * args.calls, per_launch)]
+            for cname in disp[run[0]]["c"]:
+                per[i][cname] = statistics.median(sum(disp[d]["c"].get(cname, 0.0) for d in L)
+                                                  for L in launches)
+            per[i]["kernel"] = disp[run[0]]["name"].split("(")[0].replace("void ", "")
+            per[i]["grid"] = disp[run[0]]["grid"]
+        refd = order[-TRAFFIC_CALLS:]
+        for cname in disp[refd[0]]["c"]:
+            ref[cname] = statistics.median(disp[d]["c"][cname] for d in refd)
+    lines = ["| spec | kernel | matrix ops / launch (counter) | algorithmic ops | MFMA busy | "
+             "VALU per MFMA | LDS bank-conflict cycles / LDS instr | FETCH bytes | WRITE bytes | "
+             "DRAM read bytes | algorithmic bytes |", "|" + "---|" * 11]
+    for (name, m, variant), c in zip(specs, per):
+        import synth
+        layer = synth.workload(name)
+        ops, byts = algorithmic(m, layer.N, layer.K, layer.nnzb)
+        f = lambda x: "-" if x is None else (f"{x:.3g}" if abs(x) < 1e4 else f"{x:.4g}")
+        mops = c.get("SQ_INSTS_VALU_MFMA_MOPS_F6F4")
+        busy = None
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in c and c.get("GRBM_GUI_ACTIVE"):
+            busy = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (c["GRBM_GUI_ACTIVE"] / XCDS * SIMDS)
+        vpm = None
+        if c.get("SQ_INSTS_MFMA"):
+            vpm = (c.get("SQ_INSTS_VALU", 0.0) - c["SQ_INSTS_MFMA"]) / c["SQ_INSTS_MFMA"]
+        lds = c["SQ_LDS_BANK_CONFLICT"] / c["SQ_INSTS_LDS"] if c.get("SQ_INSTS_LDS") else None
+
+        def scaled(cn, ref_bytes):
+            if cn in c and ref.get(cn):
+                return c[cn] / ref[cn] * ref_bytes
+            return None
+        fetch = scaled("FETCH_SIZE", COPY_BYTES)
+        write = scaled("WRITE_SIZE", COPY_BYTES)
+        dram = scaled("TCC_EA0_RDREQ_DRAM_sum", COPY_BYTES) or scaled("TCC_EA0_RDREQ_DRAM", COPY_BYTES)
+        lines.append(f"| {name} M={m} ({variant}) | `{c['kernel']}` grid {c['grid']} | "
+                     f"{f(None if mops is None else mops * 512)} | {f(ops)} | "
+                     f"{'-' if busy is None else f'{100 * busy:.1f} %'} | {f(vpm)} | {f(lds)} | "
+                     f"{f(fetch)} | {f(write)} | {f(dram)} | {f(byts)} |")
+    raw = ["", "Raw medians per launch (counter: value; reference kernel in the last column):", "",
+           "| counter | " + " | ".join(f"{n} M={m}" for n, m, _ in specs) + " | reference |",
+           "|" + "---|" * (len(specs) + 2)]
+    for cn in sorted(set().union(*[set(k for k in c if k not in ("kernel", "grid")) for c in per])):
+        raw.append(f"| {cn} | " + " | ".join(f"{c.get(cn, float('nan')):.6g}" for c in per)
+                   + f" | {ref.get(cn, float('nan')):.6g} |")
+    with open(out_md, "a") as fh:
+        fh.write("\n".join(lines + raw) + "\n")
+    print("\n".join(lines + raw))
 
 
 def graph_of(torch, fn, calls):
@@ -243,6 +387,9 @@ def families(args):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        summarize_counters(args)
+        return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, m=max(int(x) for x in args.ms.split(",")))
         return
@@ -254,6 +401,9 @@ def main():
         args.steps, args.warmup, args.reps = 3, 1, 5
     if args.families:
         families(args)
+        return
+    if args.kernel_run:
+        kernel_run(args)
         return
 
     import numpy as np

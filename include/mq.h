@@ -44,9 +44,16 @@
  * - Packed operand pointers (Xq, Wq, Rq) must be 16-byte aligned; fp16
  *   pointers 2-byte aligned; int32 pointers 4-byte aligned; fp32/fp64 arrays
  *   naturally aligned.  Violations return MQ_ERR_MISALIGNED.
+ * - Canonical interchange layout (mq_repack_*, mq_unpack_*): one
+ *   two's-complement 4-bit code per nibble, two per byte, the code of the
+ *   even k in the low nibble, a row of K codes as K/2 bytes in k order; Wq
+ *   [N][K/2], Xq [M][K/2], Rq [nnzb][128][64]; weight scales s_w [N][K/128].
+ *   A caller holding codes in that layout converts them once with
+ *   mq_repack_weights / mq_repack_act; every other call takes the library
+ *   layout above.
  * - Inputs must be finite.  Outputs must not alias inputs.
  * - Thread safety: every call may be made concurrently from several host
- *   threads; the only global state is a read-only per-device property cache.
+ *   threads; the library keeps no mutable global state.
  */
 #ifndef MQ_H
 #define MQ_H
@@ -149,10 +156,13 @@ mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int K,
                                 void* workspace, size_t ws_bytes, hipStream_t stream);
 
 /*
- * Same main loop, raw integer epilogue (for bit-exact testing):
+ * Same main loop (same kernel family, tiles and split-K ranges as the fp16
+ * call), raw integer epilogue (for bit-exact testing):
  *     Tb[m,n] = sum_g A_b[m,n,g],   Tr[m,n] = sum_g A_r[m,n,g]
  *   Tb, Tr : out, int32 [M, N] row-major.  Exact: |Tb|, |Tr| <= 49 K < 2^31
- *            for every supported K.
+ *            for every supported K.  Where the fp16 call splits K over
+ *            workgroups, the splits' integer sums are added atomically into
+ *            Tb, Tr (cleared first; integer addition is exact in any order).
  */
 mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int K,
                                 const uint8_t* Xq,
@@ -180,6 +190,73 @@ mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
                     const uint8_t* Rq, const void* s_r,
                     void* Y, int ldy,
                     void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Comparison baseline: the unfused pipeline the fused kernel replaces
+ * (Section 4.2 "Kernel Fusion", Fig. 3; Appendix "Kernel Profile"), three
+ * launches on `stream`:
+ *   1. the dense W4A4 GEMM (mq_fused_gemm with no residual blocks) -> fp16 Y;
+ *   2. a block-sparse residual GEMM that reads Xq again from memory and
+ *      writes fp32 partial sums P[m,n] = sum_g s_r[p][n%128] A_r[m,n,g] into
+ *      the workspace (block rows with residual blocks only);
+ *   3. a reduce-add Y[m,n] <- fp16(f32(Y[m,n]) + s_x[m] P[m,n]) on those
+ *      block rows.
+ * Same operands, layouts and checks as mq_fused_gemm; Y is rounded to fp16
+ * twice on block rows with residual blocks (within the output bar).
+ *   workspace : >= mq_unfused_workspace_size(M, N, K) bytes, 16-byte aligned
+ *               (never NULL for M > 0).  N/128 <= 65535.
+ */
+size_t mq_unfused_workspace_size(int M, int N, int K);
+mq_status mq_unfused_gemm(int M, int N, int K,
+                          const uint8_t* Xq, const void* s_x,
+                          const uint8_t* Wq, const void* s_w,
+                          const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                          const uint8_t* Rq, const void* s_r,
+                          void* Y, int ldy,
+                          void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* ======================================================================== */
+/* Layout conversion (offline; canonical <-> library layout)                 */
+/* ======================================================================== */
+
+/*
+ * Canonical int4 weights -> library layout (the paper fixes no bit layout;
+ * Section 4.2 fuses layout packing with quantisation).  The method's codes
+ * lie in [-7, 7] (Eq. (1) with q_max = 7): a nibble of -8 (0x8) is stored as
+ * -7 and counted.
+ *   Wq_c      : uint8 [N, K/2] canonical nibbles, 8-byte aligned.
+ *   s_w_c     : fp16 [N, K/128] (may be NULL together with s_w: no scales).
+ *   Rq_c      : uint8 [nnzb, 128, 64] canonical nibbles (block p, row r,
+ *               column c = code k of the block's 128), 8-byte aligned.
+ *   Wq, s_w, Rq : out, library layout (Wq group order, s_w [K/128][N],
+ *               Rq [nnzb, 128, 64] folded), 16-byte aligned packed outputs.
+ *   n_invalid : optional int32 device counter; the number of -8 nibbles is
+ *               added to it (atomically; the caller clears it).
+ * The residual scales s_r and the CSR need no conversion.
+ */
+mq_status mq_repack_weights(int N, int K, const uint8_t* Wq_c, const void* s_w_c, int nnzb,
+                            const uint8_t* Rq_c, uint8_t* Wq, void* s_w, uint8_t* Rq,
+                            int32_t* n_invalid, hipStream_t stream);
+
+/* Library layout -> canonical (the inverse of mq_repack_weights); pointer
+ * rules mirrored (library side 16-byte aligned). */
+mq_status mq_unpack_weights(int N, int K, const uint8_t* Wq, const void* s_w, int nnzb,
+                            const uint8_t* Rq, uint8_t* Wq_c, void* s_w_c, uint8_t* Rq_c,
+                            hipStream_t stream);
+
+/*
+ * Canonical int4 activation codes -> library layout (group order), e.g. for
+ * codes quantised elsewhere; -8 handled as for mq_repack_weights.
+ *   Xq_c : uint8 [M, ldq] canonical rows (ldq >= K/2, ldq % 8 == 0), 8-byte aligned.
+ *   Xq   : out, uint8 [M, K/2] library layout, 16-byte aligned.
+ */
+mq_status mq_repack_act(int M, int K, const uint8_t* Xq_c, int ldq, uint8_t* Xq,
+                        int32_t* n_invalid, hipStream_t stream);
+
+/* Library-layout activation codes (as mq_quantize_act writes them) ->
+ * canonical rows Xq_c [M, ldq]. */
+mq_status mq_unpack_act(int M, int K, const uint8_t* Xq, uint8_t* Xq_c, int ldq,
+                        hipStream_t stream);
 
 /* ======================================================================== */
 /* Offline weight preparation (not on the timed path)                        */

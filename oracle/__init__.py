@@ -52,6 +52,9 @@ def lib() -> C.CDLL:
             "orc_f32_to_f16_array": (None, [P, P, i64]),
             "orc_f16_to_f32_array": (None, [P, P, i64]),
             "orc_pack_codes": (None, [P, i, i, P]),
+            "orc_unpack_codes": (None, [P, i, i, P]),
+            "orc_pack_nibbles": (None, [P, i, i, P]),
+            "orc_unpack_nibbles": (None, [P, i, i, P]),
             "orc_unpack_code": (i, [P, i]),
             "orc_quantize_act": (None, [P, i, i, i, P, P]),
             "orc_quantize_weight": (None, [P, i, i, P, P, P]),
@@ -145,6 +148,43 @@ def pack_codes(codes: np.ndarray) -> np.ndarray:
     out = np.empty((q2.shape[0], q2.shape[1] // 2), np.uint8)
     lib().orc_pack_codes(_p(q2), q2.shape[0], q2.shape[1], _p(out))
     return out.reshape(*q.shape[:-1], q.shape[-1] // 2)
+
+
+def unpack_codes_c(packed: np.ndarray, K: int) -> np.ndarray:
+    """Signed int8 codes [rows, K] of folded packed rows [rows, K/2] (oracle C)."""
+    p = np.ascontiguousarray(packed, np.uint8).reshape(-1, K // 2)
+    out = np.empty((p.shape[0], K), np.int8)
+    lib().orc_unpack_codes(_p(p), p.shape[0], K, _p(out))
+    return out
+
+
+# ---------------------------------------------------- canonical nibbles ----
+# The interchange layout of the library's boundary: two's-complement 4-bit
+# codes, two per byte, even k in the low nibble, rows in k order.
+def pack_nibbles(codes: np.ndarray) -> np.ndarray:
+    """Canonical nibble rows [rows, K/2] of int codes [rows, K] in [-8, 7]."""
+    q = np.ascontiguousarray(codes, dtype=np.int8)
+    q2 = q.reshape(-1, q.shape[-1])
+    if q2.size and (q2.min() < -8 or q2.max() > 7):
+        raise ValueError("codes must lie in [-8, 7]")
+    out = np.empty((q2.shape[0], q2.shape[1] // 2), np.uint8)
+    lib().orc_pack_nibbles(_p(q2), q2.shape[0], q2.shape[1], _p(out))
+    return out.reshape(*q.shape[:-1], q.shape[-1] // 2)
+
+
+def unpack_nibbles(packed: np.ndarray, K: int) -> np.ndarray:
+    """Signed codes [rows, K] in [-8, 7] of canonical nibble rows [rows, K/2]."""
+    p = np.ascontiguousarray(packed, np.uint8).reshape(-1, K // 2)
+    out = np.empty((p.shape[0], K), np.int8)
+    lib().orc_unpack_nibbles(_p(p), p.shape[0], K, _p(out))
+    return out
+
+
+def folded_from_nibbles(packed: np.ndarray, K: int) -> np.ndarray:
+    """Canonical nibble rows -> the oracle's folded rows (row-major), codes
+    of -8 saturated to -7 (the codes the library's repacking produces)."""
+    q = np.maximum(unpack_nibbles(packed, K), -7)
+    return pack_codes(q).reshape(np.asarray(packed).shape)
 
 
 # ------------------------------------------------------- device layout ----

@@ -222,6 +222,33 @@ void orc_pack_codes(const int8_t* q, int rows, int K, uint8_t* out)
 {
     for (int r = 0; r < rows; ++r) pack_row(q + (int64_t)r * K, K, out + (int64_t)r * (K / 2));
 }
+void orc_unpack_codes(const uint8_t* packed, int rows, int K, int8_t* out)
+{
+    for (int r = 0; r < rows; ++r) unpack_row(packed + (int64_t)r * (K / 2), K, out + (int64_t)r * K);
+}
+
+/* ------------------------------------------------------------------------ */
+/* Canonical nibble layout (the interchange format of the library's          */
+/* boundary): one 4-bit two's-complement code per nibble, two per byte, the  */
+/* even k in the low nibble, rows of K/2 bytes in k order.  A nibble holds   */
+/* -8 .. 7; the method's codes are -7 .. 7 (Eq. (1) with q_max = 7).         */
+/* ------------------------------------------------------------------------ */
+void orc_pack_nibbles(const int8_t* q, int rows, int K, uint8_t* out)
+{
+    for (int64_t i = 0; i < (int64_t)rows * (K / 2); ++i) {
+        int lo = q[2 * i], hi = q[2 * i + 1];
+        out[i] = (uint8_t)(((unsigned)lo & 0xFu) | (((unsigned)hi & 0xFu) << 4));
+    }
+}
+
+void orc_unpack_nibbles(const uint8_t* in, int rows, int K, int8_t* q)
+{
+    for (int64_t i = 0; i < (int64_t)rows * (K / 2); ++i) {
+        int lo = in[i] & 0xF, hi = in[i] >> 4;
+        q[2 * i] = (int8_t)(lo >= 8 ? lo - 16 : lo);
+        q[2 * i + 1] = (int8_t)(hi >= 8 ? hi - 16 : hi);
+    }
+}
 
 /* ------------------------------------------------------------------------ */
 /* Per-token activation quantisation (Eq. 1 applied row by row).             */

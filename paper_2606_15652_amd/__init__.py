@@ -42,6 +42,13 @@ _SIG = {
     "mq_block_scores_dhessian": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _P]),
     "mq_select_blocks": (_I, [_P, _I, _I, _I, _P, _P, _P]),
     "mq_quantize_residual": (_I, [_P, _I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _P]),
+    "mq_unfused_workspace_size": (C.c_size_t, [_I, _I, _I]),
+    "mq_unfused_gemm": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P,
+                            C.c_size_t, _P]),
+    "mq_repack_weights": (_I, [_I, _I, _P, _P, _I, _P, _P, _P, _P, _P, _P]),
+    "mq_unpack_weights": (_I, [_I, _I, _P, _P, _I, _P, _P, _P, _P, _P]),
+    "mq_repack_act": (_I, [_I, _I, _P, _I, _P, _P, _P]),
+    "mq_unpack_act": (_I, [_I, _I, _P, _P, _I, _P]),
 }
 
 _lib: Optional[C.CDLL] = None
@@ -105,6 +112,32 @@ def _check(fn, status):
         raise MQError(fn, status)
 
 
+def _need_out(t, shape, dtype, name):
+    """A caller-provided output: CUDA, contiguous rows, the exact shape."""
+    _need(t, dtype, name, len(shape))
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _scratch(nbytes, device, stream, given=None, name="workspace"):
+    """Workspace for one launch on `stream`.  A caller-provided tensor is
+    checked for size; an allocated one is tied to `stream` when that is not
+    torch's current stream, so that the caching allocator does not hand it
+    out again while the launch still uses it."""
+    torch = _torch()
+    if nbytes == 0:
+        return None
+    if given is not None:
+        _need(given, torch.uint8, name)
+        if given.numel() < nbytes:
+            raise ValueError(f"{name} needs {nbytes} bytes, got {given.numel()}")
+        return given
+    buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if stream is not None and stream != torch.cuda.current_stream(device):
+        buf.record_stream(stream)
+    return buf
+
+
 # -------------------------------------------------------------- hot path --
 def quantize_act(X, out=None, stream=None):
     """Per-token INT4 quantisation of fp16 X [M, K] -> (Xq uint8 [M, K/2], s_x fp16 [M])."""
@@ -116,6 +149,8 @@ def quantize_act(X, out=None, stream=None):
         s_x = torch.empty((M,), dtype=torch.float16, device=X.device)
     else:
         Xq, s_x = out
+        _need_out(Xq, (M, K // 2), torch.uint8, "out[0] (Xq)")
+        _need_out(s_x, (M,), torch.float16, "out[1] (s_x)")
     _check("mq_quantize_act", load().mq_quantize_act(_ptr(X), M, K, X.stride(0), _ptr(Xq),
                                                      _ptr(s_x), _stream(stream)))
     return Xq, s_x
@@ -152,7 +187,8 @@ def _res_ptrs(pw: PackedWeight):
     return _ptr(pw.rowptr), _ptr(pw.kb), _ptr(pw.Rq), _ptr(pw.s_r)
 
 
-def fused_gemm(Xq, s_x, pw: PackedWeight, out=None, variant: str = "auto", stream=None):
+def fused_gemm(Xq, s_x, pw: PackedWeight, out=None, variant: str = "auto", stream=None,
+               workspace=None):
     """Y fp16 [M, N] = s_x * (Xq Wq^T scaled per group + sparse residual term)."""
     torch = _torch()
     _need(Xq, torch.uint8, "Xq", 2)
@@ -162,14 +198,36 @@ def fused_gemm(Xq, s_x, pw: PackedWeight, out=None, variant: str = "auto", strea
         raise ValueError("Xq / s_x shapes do not match the weight")
     Y = out if out is not None else torch.empty((M, pw.N), dtype=torch.float16, device=Xq.device)
     if out is not None:
-        _need(Y, torch.float16, "out", 2)
+        _need_out(Y, (M, pw.N), torch.float16, "out")
     rp, kb, rq, sr = _res_ptrs(pw)
     lib = load()
     ws = lib.mq_fused_gemm_workspace_size(M, pw.N, pw.K)
-    wbuf = torch.empty(ws, dtype=torch.uint8, device=Xq.device) if ws else None
+    wbuf = _scratch(ws, Xq.device, stream, workspace)
     _check("mq_fused_gemm", lib.mq_fused_gemm_variant(
         VARIANTS[variant], M, pw.N, pw.K, _ptr(Xq), _ptr(s_x), _ptr(pw.Wq), _ptr(pw.s_w),
         rp, kb, pw.nnzb, rq, sr, _ptr(Y), Y.stride(0), _ptr(wbuf), ws, _stream(stream)))
+    return Y
+
+
+def unfused_gemm(Xq, s_x, pw: PackedWeight, out=None, stream=None, workspace=None):
+    """The three-kernel baseline (dense GEMM, separate residual GEMM,
+    reduce-add) on the same operands as fused_gemm; Y fp16 [M, N]."""
+    torch = _torch()
+    _need(Xq, torch.uint8, "Xq", 2)
+    _need(s_x, torch.float16, "s_x", 1)
+    M = Xq.shape[0]
+    if Xq.shape[1] * 2 != pw.K or s_x.shape[0] != M:
+        raise ValueError("Xq / s_x shapes do not match the weight")
+    Y = out if out is not None else torch.empty((M, pw.N), dtype=torch.float16, device=Xq.device)
+    if out is not None:
+        _need_out(Y, (M, pw.N), torch.float16, "out")
+    rp, kb, rq, sr = _res_ptrs(pw)
+    lib = load()
+    ws = lib.mq_unfused_workspace_size(M, pw.N, pw.K)
+    wbuf = _scratch(ws, Xq.device, stream, workspace)
+    _check("mq_unfused_gemm", lib.mq_unfused_gemm(
+        M, pw.N, pw.K, _ptr(Xq), _ptr(s_x), _ptr(pw.Wq), _ptr(pw.s_w), rp, kb, pw.nnzb, rq, sr,
+        _ptr(Y), Y.stride(0), _ptr(wbuf), ws, _stream(stream)))
     return Y
 
 
@@ -201,19 +259,75 @@ def linear(X, pw: PackedWeight, out=None, workspace=None, stream=None):
         raise ValueError("X does not match the weight")
     Y = out if out is not None else torch.empty((M, pw.N), dtype=torch.float16, device=X.device)
     if out is not None:
-        _need(Y, torch.float16, "out", 2)
+        _need_out(Y, (M, pw.N), torch.float16, "out")
     rp, kb, rq, sr = _res_ptrs(pw)
     lib = load()
     ws = lib.mq_linear_workspace_size(M, pw.N, pw.K)
-    wbuf = None
-    if ws:
-        wbuf = workspace if workspace is not None else torch.empty(ws, dtype=torch.uint8, device=X.device)
-        if wbuf.numel() * wbuf.element_size() < ws:
-            raise ValueError(f"workspace needs {ws} bytes")
+    wbuf = _scratch(ws, X.device, stream, workspace)
     _check("mq_linear", lib.mq_linear(
         M, pw.N, pw.K, _ptr(X), X.stride(0), _ptr(pw.Wq), _ptr(pw.s_w), rp, kb, pw.nnzb, rq, sr,
         _ptr(Y), Y.stride(0), _ptr(wbuf), ws, _stream(stream)))
     return Y
+
+
+# ------------------------------------------------------ layout conversion --
+def repack_weights(Wq_c, s_w_c, rowptr, kb, Rq_c, s_r, n_invalid=None, stream=None) -> PackedWeight:
+    """Canonical int4 weights (two's-complement nibbles, even k low; Wq_c
+    uint8 [N, K/2], s_w_c fp16 [N, K/128], Rq_c uint8 [nnzb, 128, 64]) ->
+    a PackedWeight in the library layout.  ``n_invalid``: optional int32 [1]
+    device counter that receives the number of -8 nibbles (stored as -7)."""
+    torch = _torch()
+    _need(Wq_c, torch.uint8, "Wq_c", 2)
+    _need(s_w_c, torch.float16, "s_w_c", 2)
+    N, K = Wq_c.shape[0], Wq_c.shape[1] * 2
+    nnzb = int(kb.numel())
+    Wq = torch.empty((N, K // 2), dtype=torch.uint8, device=Wq_c.device)
+    s_w = torch.empty((N, K // BLOCK), dtype=torch.float16, device=Wq_c.device)
+    Rq = torch.empty((max(nnzb, 1), BLOCK, BLOCK // 2), dtype=torch.uint8, device=Wq_c.device)
+    if nnzb:
+        _need(Rq_c, torch.uint8, "Rq_c", 3)
+    if n_invalid is not None:
+        _need(n_invalid, torch.int32, "n_invalid", 1)
+    _check("mq_repack_weights", load().mq_repack_weights(
+        N, K, _ptr(Wq_c), _ptr(s_w_c), nnzb, _ptr(Rq_c) if nnzb else None, _ptr(Wq), _ptr(s_w),
+        _ptr(Rq) if nnzb else None, _ptr(n_invalid), _stream(stream)))
+    return PackedWeight(N, K, Wq, s_w, rowptr, kb, Rq[:nnzb], s_r)
+
+
+def unpack_weights(pw: PackedWeight, stream=None):
+    """Library layout -> canonical (Wq_c [N, K/2], s_w_c [N, K/128], Rq_c [nnzb, 128, 64])."""
+    torch = _torch()
+    dev = pw.Wq.device
+    Wq_c = torch.empty((pw.N, pw.K // 2), dtype=torch.uint8, device=dev)
+    s_w_c = torch.empty((pw.N, pw.K // BLOCK), dtype=torch.float16, device=dev)
+    Rq_c = torch.empty((max(pw.nnzb, 1), BLOCK, BLOCK // 2), dtype=torch.uint8, device=dev)
+    _check("mq_unpack_weights", load().mq_unpack_weights(
+        pw.N, pw.K, _ptr(pw.Wq), _ptr(pw.s_w), pw.nnzb, _ptr(pw.Rq) if pw.nnzb else None,
+        _ptr(Wq_c), _ptr(s_w_c), _ptr(Rq_c) if pw.nnzb else None, _stream(stream)))
+    return Wq_c, s_w_c, Rq_c[:pw.nnzb]
+
+
+def repack_act(Xq_c, n_invalid=None, stream=None):
+    """Canonical int4 activation rows uint8 [M, K/2] -> library layout."""
+    torch = _torch()
+    _need(Xq_c, torch.uint8, "Xq_c", 2)
+    M, K = Xq_c.shape[0], Xq_c.shape[1] * 2
+    Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=Xq_c.device)
+    if n_invalid is not None:
+        _need(n_invalid, torch.int32, "n_invalid", 1)
+    _check("mq_repack_act", load().mq_repack_act(M, K, _ptr(Xq_c), Xq_c.stride(0), _ptr(Xq),
+                                                 _ptr(n_invalid), _stream(stream)))
+    return Xq
+
+
+def unpack_act(Xq, stream=None):
+    """Library-layout activation codes uint8 [M, K/2] -> canonical rows."""
+    torch = _torch()
+    _need(Xq, torch.uint8, "Xq", 2)
+    M, K = Xq.shape[0], Xq.shape[1] * 2
+    Xq_c = torch.empty((M, K // 2), dtype=torch.uint8, device=Xq.device)
+    _check("mq_unpack_act", load().mq_unpack_act(M, K, _ptr(Xq), _ptr(Xq_c), K // 2, _stream(stream)))
+    return Xq_c
 
 
 # --------------------------------------------------- weight preparation --

@@ -578,7 +578,11 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
 #pragma unroll
             for (int c = 0; c < WN; ++c) {
                 const int n = n0 + 16 * (wn + WAVES_N * c) + lrow;
-                if constexpr (RAW) {
+                if constexpr (RAW && SPLIT) {
+                    // integer sums of a group range: added in any order, exact
+                    atomicAdd(&a.Tb[(int64_t)m * N + n], iacc[i][c][r]);
+                    atomicAdd(&a.Tr[(int64_t)m * N + n], racc[i][c][r]);
+                } else if constexpr (RAW) {
                     a.Tb[(int64_t)m * N + n] = iacc[i][c][r];
                     a.Tr[(int64_t)m * N + n] = racc[i][c][r];
                 } else if constexpr (SPLIT) {
@@ -602,6 +606,12 @@ __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restr
     float v = 0.f;
     for (int s = 0; s < splits; ++s) v += part[s * total + idx];
     Y[(int64_t)m * ldy + n] = float_to_half_bits(half_bits_to_float(s_x[m]) * v);
+}
+
+// Zero-fills n int32 (the raw split-K sums are accumulated into them).
+__global__ __launch_bounds__(256) void fill_zero_kernel(int32_t* __restrict__ p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0;
 }
 
 // Split-K factor for the tiled kernel: enough workgroups to give every CU two,
@@ -1216,10 +1226,21 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
     } else {
         const int64_t tiles = (int64_t)((a.M + kTB - 1) / kTB) * (a.N / kTB);
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
-        const int splits = RAW ? 1 : tiled_splits(a.M, a.N, a.K);
+        const int splits = tiled_splits(a.M, a.N, a.K);
         if (splits == 1) {
             hipLaunchKernelGGL((gemm_tiled_kernel<4, 2, RAW, false>), dim3((unsigned)tiles),
                                dim3(TileShape<4, 2>::kThreads), 0, stream, a, 0, (float*)nullptr);
+        } else if constexpr (RAW) {
+            // raw sums: every split adds its exact integer partial sums into Tb, Tr
+            const int64_t total = (int64_t)a.M * a.N;
+            hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                               a.Tb, total);
+            hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                               a.Tr, total);
+            const int G = a.K / kGroup;
+            const int gps = (G + splits - 1) / splits;
+            hipLaunchKernelGGL((gemm_tiled_kernel<4, 2, RAW, true>), dim3((unsigned)tiles, splits),
+                               dim3(TileShape<4, 2>::kThreads), 0, stream, a, gps, (float*)nullptr);
         } else {
             if (!workspace || ws_bytes < (size_t)splits * a.M * a.N * sizeof(float)) return MQ_ERR_WORKSPACE;
             const int G = a.K / kGroup;

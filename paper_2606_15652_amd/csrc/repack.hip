@@ -1,0 +1,155 @@
+// Conversion between the canonical 4-bit interchange layout and the
+// library's storage layout (both documented in mq.h).
+//
+// Canonical: one two's-complement code per nibble, two per byte, the even k
+// in the low nibble, rows of K/2 bytes in k order; weight scales [N][K/128].
+// Library: folded sign-magnitude chunks of 16 codes (the operand form of the
+// fp6 matrix instruction), packed rows (Xq, Wq) in group order, weight scales
+// [K/128][N]; residual blocks keep their [nnzb][128][64] order.
+//
+// The paper fixes no bit layout (Section 4.2 fuses layout packing with
+// quantisation); these conversions let a caller that holds plain int4 codes
+// use the fused layer, with the method's codes in [-7, 7] (Eq. (1) with
+// q_max = 7).  Offline work: one thread per 16-code chunk.
+#include "mq_device.h"
+
+namespace mq {
+
+// 8 canonical bytes (16 nibbles) -> 16 codes; -8 saturates to -7 and is counted
+__device__ __forceinline__ int nibbles_to_codes(uint2 v, int (&q)[16]) {
+    int bad = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const uint32_t w = e < 8 ? v.x : v.y;
+        const int nib = (int)((w >> (4 * (e & 7))) & 0xFu);
+        int c = nib >= 8 ? nib - 16 : nib;
+        if (c == -8) {
+            c = -kQmax;
+            ++bad;
+        }
+        q[e] = c;
+    }
+    return bad;
+}
+
+// folded chunk -> 8 canonical bytes
+__device__ __forceinline__ uint2 chunk_to_nibbles(uint2 ch) {
+    uint32_t lo = 0u, hi = 0u;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+        const uint32_t nib = (uint32_t)chunk_code(ch.x, ch.y, e) & 0xFu;
+        if (e < 8) lo |= nib << (4 * e);
+        else hi |= nib << (4 * (e - 8));
+    }
+    return make_uint2(lo, hi);
+}
+
+// Packed rows.  Chunk c of row r: canonical bytes 8c of row r (stride ld
+// bytes); library bytes piece_offset(rows, r, c / 8) + 8 (c % 8) when GROUPED,
+// else 8c of row r (stride K/2: residual blocks).
+template <bool TO_LIB, bool GROUPED>
+__global__ __launch_bounds__(256) void repack_rows_kernel(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                                          int rows, int K, int ld, int32_t* __restrict__ n_invalid) {
+    const int cpr = K / 16;                                   // chunks per row
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (int64_t)rows * cpr) return;
+    const int r = (int)(idx / cpr), c = (int)(idx % cpr);
+    const int64_t canon = (int64_t)r * ld + 8 * c;
+    const int64_t lib = GROUPED ? piece_offset(rows, r, c / 8) + 8 * (c % 8) : (int64_t)r * (K / 2) + 8 * c;
+    if constexpr (TO_LIB) {
+        int q[16];
+        const int bad = nibbles_to_codes(*reinterpret_cast<const uint2*>(src + canon), q);
+        *reinterpret_cast<uint2*>(dst + lib) = fold_codes(q);
+        if (bad && n_invalid) atomicAdd(n_invalid, bad);
+    } else {
+        *reinterpret_cast<uint2*>(dst + canon) = chunk_to_nibbles(*reinterpret_cast<const uint2*>(src + lib));
+    }
+}
+
+// Weight scales: canonical [N][G] <-> library [G][N]
+template <bool TO_LIB>
+__global__ __launch_bounds__(256) void repack_scales_kernel(const uint16_t* __restrict__ src,
+                                                            uint16_t* __restrict__ dst, int N, int G) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (int64_t)N * G) return;
+    const int n = (int)(idx / G), g = (int)(idx % G);
+    if constexpr (TO_LIB) dst[wscale_index(N, n, g)] = src[idx];
+    else dst[idx] = src[wscale_index(N, n, g)];
+}
+
+static unsigned blocks_for(int64_t n) { return (unsigned)((n + 255) / 256); }
+
+template <bool TO_LIB, bool GROUPED>
+static mq_status rows_launch(const uint8_t* src, uint8_t* dst, int rows, int K, int ld, int32_t* n_invalid,
+                             hipStream_t stream) {
+    const int64_t n = (int64_t)rows * (K / 16);
+    if (n == 0) return MQ_OK;
+    hipLaunchKernelGGL((repack_rows_kernel<TO_LIB, GROUPED>), dim3(blocks_for(n)), dim3(256), 0, stream, src, dst,
+                       rows, K, ld, n_invalid);
+    return mq_host::launch_status();
+}
+
+static bool k_ok(int K) { return K >= 128 && K % 128 == 0 && K <= (1 << 20); }
+
+template <bool TO_LIB>
+static mq_status weights(int N, int K, const uint8_t* Wsrc, const void* ssrc, int nnzb, const uint8_t* Rsrc,
+                         uint8_t* Wdst, void* sdst, uint8_t* Rdst, int32_t* n_invalid, hipStream_t stream) {
+    if (N < 0 || K < 0 || nnzb < 0) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::shape_ok(N, K)) return MQ_ERR_UNSUPPORTED_SHAPE;
+    if ((int64_t)nnzb > (int64_t)(N / kGroup) * (K / kGroup)) return MQ_ERR_INVALID_ARG;
+    if (!Wsrc || !Wdst || (ssrc == nullptr) != (sdst == nullptr) || (nnzb > 0 && (!Rsrc || !Rdst)))
+        return MQ_ERR_INVALID_ARG;
+    if (!mq_host::aligned(Wsrc, 8) || !mq_host::aligned(Wdst, 16) || (ssrc && !mq_host::aligned(ssrc, 2)) ||
+        (sdst && !mq_host::aligned(sdst, 2)) || (Rsrc && !mq_host::aligned(Rsrc, 8)) ||
+        (Rdst && !mq_host::aligned(Rdst, 16)) || (n_invalid && !mq_host::aligned(n_invalid, 4)))
+        return MQ_ERR_MISALIGNED;
+    // the library side must be 16-byte aligned, the canonical side 8-byte
+    if (!TO_LIB && (!mq_host::aligned(Wsrc, 16) || (Rsrc && !mq_host::aligned(Rsrc, 16)))) return MQ_ERR_MISALIGNED;
+    mq_status st = rows_launch<TO_LIB, true>(Wsrc, Wdst, N, K, K / 2, n_invalid, stream);
+    if (st != MQ_OK) return st;
+    if (ssrc) {
+        const int G = K / kGroup;
+        hipLaunchKernelGGL((repack_scales_kernel<TO_LIB>), dim3(blocks_for((int64_t)N * G)), dim3(256), 0, stream,
+                           static_cast<const uint16_t*>(ssrc), static_cast<uint16_t*>(sdst), N, G);
+        st = mq_host::launch_status();
+        if (st != MQ_OK) return st;
+    }
+    if (nnzb > 0) return rows_launch<TO_LIB, false>(Rsrc, Rdst, nnzb * kGroup, kGroup, kGroup / 2, n_invalid, stream);
+    return MQ_OK;
+}
+
+}  // namespace mq
+
+using namespace mq;
+
+extern "C" mq_status mq_repack_weights(int N, int K, const uint8_t* Wq_c, const void* s_w_c, int nnzb,
+                                       const uint8_t* Rq_c, uint8_t* Wq, void* s_w, uint8_t* Rq,
+                                       int32_t* n_invalid, hipStream_t stream) {
+    return weights<true>(N, K, Wq_c, s_w_c, nnzb, Rq_c, Wq, s_w, Rq, n_invalid, stream);
+}
+
+extern "C" mq_status mq_unpack_weights(int N, int K, const uint8_t* Wq, const void* s_w, int nnzb,
+                                       const uint8_t* Rq, uint8_t* Wq_c, void* s_w_c, uint8_t* Rq_c,
+                                       hipStream_t stream) {
+    return weights<false>(N, K, Wq, s_w, nnzb, Rq, Wq_c, s_w_c, Rq_c, nullptr, stream);
+}
+
+extern "C" mq_status mq_repack_act(int M, int K, const uint8_t* Xq_c, int ldq, uint8_t* Xq, int32_t* n_invalid,
+                                   hipStream_t stream) {
+    if (M < 0 || K < 0) return MQ_ERR_INVALID_ARG;
+    if (!k_ok(K) || M > (1 << 24) || ldq < K / 2 || ldq % 8 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
+    if (M == 0) return MQ_OK;
+    if (!Xq_c || !Xq) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::aligned(Xq_c, 8) || !mq_host::aligned(Xq, 16) || (n_invalid && !mq_host::aligned(n_invalid, 4)))
+        return MQ_ERR_MISALIGNED;
+    return rows_launch<true, true>(Xq_c, Xq, M, K, ldq, n_invalid, stream);
+}
+
+extern "C" mq_status mq_unpack_act(int M, int K, const uint8_t* Xq, uint8_t* Xq_c, int ldq, hipStream_t stream) {
+    if (M < 0 || K < 0) return MQ_ERR_INVALID_ARG;
+    if (!k_ok(K) || M > (1 << 24) || ldq < K / 2 || ldq % 8 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
+    if (M == 0) return MQ_OK;
+    if (!Xq_c || !Xq) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::aligned(Xq_c, 8) || !mq_host::aligned(Xq, 16)) return MQ_ERR_MISALIGNED;
+    return rows_launch<false, true>(Xq, Xq_c, M, K, ldq, nullptr, stream);
+}

@@ -129,3 +129,24 @@ def test_linear_validation(lib):
     assert _lin(lib, M=64, K=1024, ws=A, ws_bytes=need - 1) == WORKSPACE
     assert _lin(lib, M=64, K=1024, ws=None, ws_bytes=need) == INVALID
     assert _lin(lib, M=64, K=1024, ws=A + 8, ws_bytes=need) == MISALIGNED
+
+
+def test_repack_validation(lib):
+    rw, uw = lib.mq_repack_weights, lib.mq_unpack_weights
+    assert rw(256, 200, A, A, 0, None, A, A, None, None, None) == SHAPE
+    assert rw(-1, 256, A, A, 0, None, A, A, None, None, None) == INVALID
+    assert rw(256, 256, A, A, 5, A, A, A, A, None, None) == INVALID             # nnzb > NB * KB
+    assert rw(256, 256, A, A, 1, None, A, A, A, None, None) == INVALID          # residual source missing
+    assert rw(256, 256, A, None, 0, None, A, A, None, None, None) == INVALID    # scales: both or neither
+    assert rw(256, 256, A + 4, A, 0, None, A, A, None, None, None) == MISALIGNED
+    assert rw(256, 256, A, A, 0, None, A + 8, A, None, None, None) == MISALIGNED
+    assert rw(256, 256, A, A, 0, None, A, A, None, A + 2, None) == MISALIGNED
+    assert uw(256, 256, A + 8, A, 0, None, A, A, None, None) == MISALIGNED     # library side 16-byte
+    ra, ua = lib.mq_repack_act, lib.mq_unpack_act
+    assert ra(0, 256, A, 128, A, None, None) == OK
+    assert ra(4, 256, A, 120, A, None, None) == SHAPE                          # ldq < K/2
+    assert ra(4, 256, A, 132, A, None, None) == SHAPE                          # ldq % 8
+    assert ra(4, 256, None, 128, A, None, None) == INVALID
+    assert ra(4, 256, A, 128, A + 8, None, None) == MISALIGNED
+    assert ua(4, 256, A + 8, A, 128, None) == MISALIGNED
+    assert ua(-1, 256, A, A, 128, None) == INVALID

@@ -571,3 +571,146 @@ def test_planted_mistakes_are_caught(orc):
     assert not np.array_equal(xc @ wsw.T, Tb)
     # sign error on the residual
     assert not np.array_equal(xc @ (-rcodes).T, Tr)
+
+
+# ------------------------------------------ canonical nibbles, device order --
+def _read_pairs(name, last):
+    cases, cur = [], {}
+    for line in open(os.path.join(GOLDEN, name)):
+        line = line.split("#", 1)[0].strip()
+        if not line:
+            continue
+        key, val = line.split(":", 1)
+        cur[key] = val.split()
+        if key == last:
+            cases.append(cur)
+            cur = {}
+    return cases
+
+
+@pytest.mark.parametrize("case", _read_pairs("nibble_layout.txt", "bytes"),
+                         ids=lambda c: " ".join(c["codes"]))
+def test_nibble_layout_golden(orc, case):
+    """Hand-worked canonical bytes: packing gives them, unpacking gives the codes."""
+    codes = np.array([int(v) for v in case["codes"]], np.int8)[None, :]
+    want = bytes(int(b, 16) for b in case["bytes"])
+    assert orc.pack_nibbles(codes).tobytes() == want
+    assert orc.unpack_nibbles(np.frombuffer(want, np.uint8)[None, :], codes.shape[1]).tolist() == codes.tolist()
+
+
+def test_nibble_layout_invariants(orc):
+    """Round trips over every byte value; each code only moves its own nibble;
+    the folded and canonical layouts hold the same codes (-8 saturating)."""
+    allb = np.arange(256, dtype=np.uint8)[None, :]
+    codes = orc.unpack_nibbles(allb, 512)
+    assert codes.min() == -8 and codes.max() == 7
+    assert np.array_equal(orc.pack_nibbles(codes), allb)
+    # a byte's low nibble is k = 2j, its high nibble k = 2j + 1 (numpy restatement)
+    assert np.array_equal(codes[0, 0::2], ((allb[0] & 15).astype(np.int16) ^ 8) - 8)
+    assert np.array_equal(codes[0, 1::2], ((allb[0] >> 4).astype(np.int16) ^ 8) - 8)
+    for k in (0, 1, 2, 7, 126, 127):
+        one = np.zeros((1, 128), np.int8)
+        one[0, k] = -3
+        b = orc.pack_nibbles(one)
+        assert np.flatnonzero(b[0]).tolist() == [k // 2]
+        assert np.flatnonzero(orc.unpack_nibbles(b, 128)[0]).tolist() == [k]
+    rng = np.random.default_rng(3)
+    raw = rng.integers(0, 256, (5, 256), dtype=np.uint8)
+    fold = orc.folded_from_nibbles(raw, 512)
+    assert np.array_equal(orc.unpack_codes(fold, 512), np.maximum(orc.unpack_nibbles(raw, 512), -7))
+    assert np.array_equal(orc.unpack_codes_c(fold, 512), orc.unpack_codes(fold, 512))
+
+
+def _device_order_golden():
+    rows, pieces, scales = None, [], []
+    for line in open(os.path.join(GOLDEN, "device_order.txt")):
+        line = line.split("#", 1)[0].strip()
+        if not line:
+            continue
+        key, val = line.split(":", 1)
+        v = [int(x) for x in val.split()]
+        if key == "rows":
+            rows = v[0]
+        elif key == "K":
+            K = v[0]
+        elif key == "piece":
+            pieces.append(v)
+        elif key == "scale":
+            scales.append(v)
+    return rows, K, pieces, scales
+
+
+def test_device_order_golden(orc):
+    """block_rows / block_scales (the permutation every GPU parity test applies
+    at the boundary) against the hand-worked offsets of the documented
+    formulas, and their inverses."""
+    R, K, pieces, scales = _device_order_golden()
+    G = K // B
+    rm = np.zeros((R, K // 2), np.uint8)
+    for r in range(R):
+        for g in range(G):
+            rm[r, 64 * g:64 * (g + 1)] = 16 * (r + 1) + g + np.arange(64) % 2
+    dev = orc.block_rows(rm, K).reshape(-1)
+    assert len(pieces) == R * G
+    for r, g, off in pieces:
+        assert np.array_equal(dev[off:off + 64], rm[r, 64 * g:64 * (g + 1)]), (r, g, off)
+    assert np.array_equal(orc.unblock_rows(dev.reshape(R, K // 2), K), rm)
+    s = (np.arange(R * G, dtype=np.uint16) * 7 + 1).reshape(R, G)
+    ds = orc.block_scales(s).reshape(-1)
+    assert len(scales) == R * G
+    for n, g, el in scales:
+        assert ds[el] == s[n, g], (n, g, el)
+    assert np.array_equal(orc.unblock_scales(ds.reshape(R, G)), s)
+
+
+def test_device_order_formula_random(orc):
+    """The same formulas at larger, ragged sizes by direct indexing."""
+    rng = np.random.default_rng(8)
+    for R, K in ((37, 640), (130, 1024), (1, 128)):
+        rm = rng.integers(0, 256, (R, K // 2), dtype=np.uint8)
+        dev = orc.block_rows(rm, K).reshape(-1)
+        for _ in range(200):
+            r, g = int(rng.integers(R)), int(rng.integers(K // B))
+            off = (g * R + r) * 64
+            assert np.array_equal(dev[off:off + 64], rm[r, 64 * g:64 * g + 64])
+        s = rng.integers(0, 65536, (R, K // B)).astype(np.uint16)
+        ds = orc.block_scales(s).reshape(-1)
+        for _ in range(200):
+            n, g = int(rng.integers(R)), int(rng.integers(K // B))
+            assert ds[g * R + n] == s[n, g]
+
+
+def test_hessian_constant_against_exact_distortion(orc):
+    """App. A: the exact output distortion L(S) = (2/N) ||X E_S^T||_F^2 (its own
+    constant, computed by a matrix product) equals the diagonal surrogate
+    sum h_j E_ij^2 built from the oracle's h when the columns of X are
+    orthogonal, in absolute value; and L(0) - L(S) is the sum of the oracle's
+    Delta-Hessian scores of S.  A wrong factor in h (which the top-K ranking
+    cannot see) fails here."""
+    N, K = 256, 256
+    rng = np.random.default_rng(21)
+    W = synth.gen_weight(N, K, 44)
+    T = K
+    X = np.zeros((T, K), np.float16)
+    X[np.arange(K), np.arange(K)] = rng.uniform(0.2, 4.0, K).astype(np.float16)
+    Xd = X.astype(np.float64)
+    _, _, R = orc.quantize_weight(W)
+    h = orc.hessian_diag(X)
+    S = orc.block_scores_dhessian(R, h)
+    qr = _all_block_qr(R.astype(np.float64), orc)
+    KB = K // B
+
+    def err(sel):
+        E = R.astype(np.float64).copy()
+        for b in sel:
+            nb, kb = divmod(b, KB)
+            E[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B] -= qr[nb * B:(nb + 1) * B, kb * B:(kb + 1) * B]
+        return E
+
+    for sel in ((), (0,), (1, 2), (0, 1, 2, 3)):
+        E = err(sel)
+        exact = 2.0 / T * np.linalg.norm(Xd @ E.T) ** 2
+        surrogate = float((h[None, :] * E ** 2).sum())
+        assert surrogate == pytest.approx(exact, rel=1e-12)
+        gain = 2.0 / T * np.linalg.norm(Xd @ R.astype(np.float64).T) ** 2 - exact
+        assert gain == pytest.approx(sum(S.ravel()[b] for b in sel), rel=1e-9, abs=1e-15)
