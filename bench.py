@@ -75,6 +75,10 @@ def parse():
     ap.add_argument("--families", action="store_true",
                     help="time the fused GEMM and the whole layer call on every layer of the other "
                          "workload families (one JSON line per layer and M; not the headline line)")
+    ap.add_argument("--only", metavar="LAYERS", help="--families: comma-separated layer names (default: all)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="--families: also time the three-kernel baseline (dense GEMM, residual GEMM, "
+                         "reduce-add) and the dense-only GEMM on the same operands")
     ap.add_argument("--kernel-run", metavar="SPECS",
                     help="counter / trace run: comma-separated layer:M[:variant] specs; per spec, "
                          "--calls eager fused GEMM launches (rotating weight copies), then a "
@@ -326,8 +330,9 @@ def families(args):
     mq.load()
     dev = torch.device("cuda:0")
     wcache = {}
+    only = set(args.only.split(",")) if args.only else None
     for layer in synth.workloads():
-        if layer.name == "c2_4096":
+        if (only is None and layer.name == "c2_4096") or (only is not None and layer.name not in only):
             continue
         K, N, nnzb = layer.K, layer.N, layer.nnzb
         key = (K, N, layer.seed, layer.skewed)
@@ -378,6 +383,24 @@ def families(args):
             if t_blas is not None:
                 row["us_w16a16"] = round(t_blas, 3)
                 row["speedup_vs_w16a16"] = round(t_blas / t_call, 3)
+            if args.unfused:
+                wsu = torch.empty(max(1, mq.load().mq_unfused_workspace_size(m, N, K)), dtype=torch.uint8,
+                                  device=dev)
+                dense = [mq.PackedWeight(N, K, c.Wq, c.s_w, c.rowptr.new_zeros(N // 128 + 1), c.kb[:0],
+                                         c.Rq[:0], c.s_r[:0]) for c in copies]
+                rd = [0]
+
+                def next_dense():
+                    rd[0] = (rd[0] + 1) % ncopy
+                    return dense[rd[0]]
+                t_unf = timed(torch, lambda: mq.unfused_gemm(Xq, sx, next_pw(), out=Y, workspace=wsu), reps)
+                t_dense = timed(torch, lambda: mq.fused_gemm(Xq, sx, next_dense(), out=Y), reps)
+                row["us_unfused"] = round(t_unf, 3)
+                row["us_dense_only"] = round(t_dense, 3)
+                row["fused_speedup_vs_unfused"] = round(t_unf / t_gemm, 3)
+                row["residual_overhead_fused"] = round(t_gemm / t_dense - 1.0, 4)
+                row["residual_overhead_unfused"] = round(t_unf / t_dense - 1.0, 4)
+                del wsu, dense
             print(json.dumps(row), flush=True)
             del X, Xq, sx, Y, ws
         del copies, pw0, wbs

@@ -851,185 +851,210 @@ __global__ __launch_bounds__(512) void gemm_medium_kernel(GemmArgs a) {
 }
 
 // --------------------------------------------------------------------------
-// Skinny kernel: 16 * WN output columns per workgroup, all M (<= 16 * WM)
-// rows, the K-loop split over NW waves.
+// Decode kernel (M <= 32): a workgroup owns SPW adjacent 16-column strips
+// (16 SPW <= 64 columns, inside one 128-row block row) and all M rows.  Its
+// eight waves split the K groups into contiguous runs, and the block row's
+// residual blocks into contiguous runs of its CSR entries (by entry, not by
+// group: no search of the CSR, and hot block rows spread over all waves).
+// Each wave streams its groups and then its blocks as one sequence of items
+// through a ring of GD register stages (the loads of GD items in flight; the
+// SPW strips of an item are adjacent 1 KB pieces of Wq or of the block).
+// Partial sums are added through LDS in wave order (deterministic).  Every
+// stage issues a fixed number of loads (a dead slot reads past its resource:
+// zeros, no memory access), so the compiler's wait counts stay exact.
 // --------------------------------------------------------------------------
 // Fused activation quantisation (FQ): at most kFusedMaxM rows and
 // kFusedCPT 16-element chunks per thread; the workgroup quantises the rows
 // into LDS itself (same arithmetic as mq_quantize_act) instead of reading Xq.
 constexpr int kFusedMaxM = 4, kFusedCPT = 4;
+constexpr int kDecodeWaves = 8;
+constexpr uint32_t kPastEnd = 0x80000000u;   // buffer offset past every operand (< 2 GB): reads zero
 
-template <int WM, int WN, int NW, bool RAW, bool FQ = false>
-__global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
-    static_assert(WN * 16 <= 128 && 128 % (WN * 16) == 0, "workgroup columns must sit in one block row");
+// Items in flight per wave: about 96 registers of stages (a stage holds WM X
+// fragments, WN B fragments and WN scales).
+template <int WM, int WN>
+struct StreamDepth {
+    static constexpr int kStageRegs = 4 * WM + 4 * WN + WN;
+    static constexpr int GD = 96 / kStageRegs < 2 ? 2 : 96 / kStageRegs > 6 ? 6 : 96 / kStageRegs;
+};
+
+// bytes of dynamic LDS: the quantised rows (FQ) and, after the main loops,
+// the cross-wave partial sums
+template <int WM, int WN, bool RAW>
+constexpr size_t stream_red_bytes() {
+    return (size_t)kDecodeWaves * WM * WN * 4 * (RAW ? 2 : 1) * 64 * 4;
+}
+
+// The streaming kernel: eight waves = KS = 8 / (WGM WGN) splits of the K
+// loop x a WGM x WGN grid of waves, each wave WM x WN sub-tiles of 16 x 16:
+// a (16 WM WGM) x (16 WN WGN) output tile.  Decode: WGM = WGN = 1 (all M <=
+// 32 rows, 16 WN columns, K over eight waves); medium M: 64 x 64 tiles of
+// 2 x 2 waves and two K splits.
+template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ>
+__global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs a) {
+    static_assert(WN * WGN == 1 || WN * WGN == 2 || WN * WGN == 4, "tile columns inside one block row");
     static_assert(!(FQ && RAW), "fused quantisation feeds the fp16 path");
-    // reduction buffer: fp32 partials, or (raw mode) int32 base and residual sums
-    constexpr int kSlotsPerWave = WM * WN * 4 * (RAW ? 2 : 1);
-    __shared__ __attribute__((aligned(16))) uint32_t red[NW][kSlotsPerWave][64];
-    // FQ: packed codes of the M rows (M x K/2 bytes, row-major), row maxima, scales
-    extern __shared__ __attribute__((aligned(16))) uint8_t xs[];
+    static_assert(!FQ || (WGM == 1 && WGN == 1), "fused quantisation: one tile of all rows");
+    constexpr int NW = kDecodeWaves, WG2 = WGM * WGN, KS = NW / WG2;
+    static_assert(KS * WG2 == NW, "eight waves");
+    constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
+    constexpr int SPW = WN;
+    constexpr int GD = StreamDepth<WM, WN>::GD;
+    constexpr int kVals = WM * SPW * 4 * (RAW ? 2 : 1);          // partial sums per lane
+    // FQ: packed codes of the M rows (M x K/2 bytes, row-major); afterwards
+    // the partial sums red[wave][value][lane]
+    extern __shared__ __attribute__((aligned(16))) uint8_t dyn[];
     __shared__ uint32_t amax_sh[kFusedMaxM];
     __shared__ uint16_t sx_sh[kFusedMaxM];
+    uint8_t* xs = dyn;
+    uint32_t* red = reinterpret_cast<uint32_t*>(dyn);
 
-    const int M = a.M, K = a.K, N = a.N;
+    const int M = a.M, N = a.N, K = a.K;
     const int G = K / kGroup;
     const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int n0 = blockIdx.x * 16 * WN;
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int lrow = lane & 15, lq = lane >> 4;
+    const int split = wave / WG2, wpos = wave % WG2, wm = wpos / WGN, wn = wpos % WGN;
+    int tm, tn;
+    tile_coords(blockIdx.x, (M + TM - 1) / TM, N / TN, tm, tn);
+    const int m0 = tm * TM, n0 = tn * TN;
+    const int nb = n0 / kGroup, roff = n0 % kGroup;
+    const int mw = m0 + 16 * WM * wm;                            // the wave's first row
+    const int nw = 16 * WN * wn;                                 // its first column inside the tile
 
-    // contiguous run of groups for this wave
-    const int per = G / NW, extra = G % NW;
-    const int gb = wave * per + (wave < extra ? wave : extra);
-    const int ge = gb + per + (wave < extra ? 1 : 0);
+    // this split's run of groups
+    const int gper = G / KS, gextra = G % KS;
+    const int gb = split * gper + min(split, gextra);
+    const int ng = gper + (split < gextra ? 1 : 0);
 
-    // residual walk: first entry of the block row with column >= gb (scalar
-    // loads through the constant address space, off the vector-memory counter)
+    // this split's run of the block row's CSR entries (scalar loads through
+    // the constant address space: off the vector-memory counter)
     const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
-    int rp = 0, rend = 0;
+    int pb = 0, ne = 0;
     if (a.rowptr) {
         const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
-        const int nb = n0 / 128;
-        rp = rowptr[nb];
-        rend = rowptr[nb + 1];
-        while (rp < rend && res_kb[rp] < gb) ++rp;
+        const int rp = rowptr[nb], cnt = rowptr[nb + 1] - rp;
+        const int eper = cnt / KS, eextra = cnt % KS;
+        pb = rp + split * eper + min(split, eextra);
+        ne = eper + (split < eextra ? 1 : 0);
     }
-    const int rrow0 = n0 % 128;
 
-    f32x4 acc[WM][WN];
-    i32x4 iacc[WM][WN], racc[WM][WN];
+    // whole-operand resources (32-bit offsets; launch() checks every operand < 2 GB)
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(FQ ? a.Wq : a.Xq, FQ ? 0u : a.xq_bytes);
+    const uint32_t loff = (uint32_t)lrow * kGroupBytes + (uint32_t)lq * 16;   // lane's bytes of a 16-row piece
+
+    // X fragment of rows 16 i .. 16 i + 15 at group g: from the quantised rows
+    // in LDS (FQ; rows past M read 0) or from Xq (rows past M read other rows'
+    // bytes or zeros past the end: they only feed output rows never written)
+    auto x_offset = [&](int g, int i) -> uint32_t {
+        return ((uint32_t)g * (uint32_t)M + (uint32_t)mw + 16u * i) * kGroupBytes + loff;
+    };
+    auto x_lds = [&](int g, int i) -> uint4 {
+        const int row = mw + 16 * i + lrow;
+        uint4 v = make_uint4(0u, 0u, 0u, 0u);
+        if (row < M) v = *reinterpret_cast<const uint4*>(&xs[(int64_t)row * (K / 2) + g * kGroupBytes + lq * 16]);
+        return v;
+    };
+
+    f32x4 acc[WM][SPW];
+    i32x4 iacc[WM][SPW], racc[WM][SPW];
 #pragma unroll
     for (int i = 0; i < WM; ++i)
 #pragma unroll
-        for (int j = 0; j < WN; ++j) {
-            acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-            iacc[i][j] = i32x4{0, 0, 0, 0};
-            racc[i][j] = i32x4{0, 0, 0, 0};
+        for (int s = 0; s < SPW; ++s) {
+            acc[i][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+            iacc[i][s] = i32x4{0, 0, 0, 0};
+            racc[i][s] = i32x4{0, 0, 0, 0};
         }
-
-    // Operands of kChunk consecutive groups per stage; two stages alternate so
-    // that a wave keeps up to 2 * kChunk groups of loads in flight (decode is
-    // bound by how many bytes are in flight, not by the arithmetic).
-    constexpr int kChunk = 4;
-    struct Stage {
-        uint4 x[kChunk][WM], w[kChunk][WN], r[kChunk][WN];
-        uint16_t sw[kChunk][WN], sr[kChunk][WN];
-        int p[kChunk];
-    };
-    // Every load is issued unconditionally through a range-checked buffer
-    // resource (rows past M, absent residual blocks and groups past ge read
-    // zero from a resource that does not cover them), so each stage issues a
-    // fixed number of loads and the compiler's waits can leave the other
-    // stage in flight.
-    auto load = [&](int c0, Stage& S) {
-        // dense operands first: they do not wait for the scalar CSR walk
-#pragma unroll
-        for (int q = 0; q < kChunk; ++q) {
-            const int g = c0 + q;
-            const bool live = g < ge;
-            const __amdgpu_buffer_rsrc_t xr =
-                make_rsrc(a.Xq + (live ? piece_offset(M, 0, g) : 0), live ? (uint32_t)M * kGroupBytes : 0u);
-            const __amdgpu_buffer_rsrc_t wr =
-                make_rsrc(a.Wq + (live ? piece_offset(N, n0, g) : 0), live ? 16u * WN * kGroupBytes : 0u);
-            if constexpr (!FQ) {
-#pragma unroll
-                for (int i = 0; i < WM; ++i)
-                    S.x[q][i] = bload16(xr, (uint32_t)(i * 16 + lrow) * kGroupBytes + lq * 16, 0);
-            }
-#pragma unroll
-            for (int j = 0; j < WN; ++j)
-                S.w[q][j] = bload16(wr, (uint32_t)(16 * j + lrow) * kGroupBytes + lq * 16, 0);
-            if constexpr (!RAW) {
-                const __amdgpu_buffer_rsrc_t swr =
-                    make_rsrc(a.s_w + (live ? wscale_index(N, n0, g) : 0), live ? 32u * WN : 0u);
-#pragma unroll
-                for (int j = 0; j < WN; ++j)
-                    S.sw[q][j] = __builtin_amdgcn_raw_buffer_load_b16(swr, (uint32_t)(16 * j + lrow) * 2, 0, 0);
-            }
-        }
-#pragma unroll
-        for (int q = 0; q < kChunk; ++q) {
-            const int g = c0 + q;
-            int pr = -1;
-            if (g < ge && rp < rend && res_kb[rp] == g) pr = rp++;
-            S.p[q] = pr;
-            const bool hr = pr >= 0;
-            // (an absent block reads through a zero-size resource on the
-            // weight base: a.Rq may be null when there are no residual blocks)
-            const __amdgpu_buffer_rsrc_t rr = hr ? make_rsrc(a.Rq + ((int64_t)pr * 128 + rrow0) * kGroupBytes,
-                                                             16u * WN * kGroupBytes)
-                                                 : make_rsrc(a.Wq, 0u);
-#pragma unroll
-            for (int j = 0; j < WN; ++j)
-                S.r[q][j] = bload16(rr, (uint32_t)(16 * j + lrow) * kGroupBytes + lq * 16, 0);
-            if constexpr (!RAW) {
-                const __amdgpu_buffer_rsrc_t srr =
-                    hr ? make_rsrc(a.s_r + (int64_t)pr * 128 + rrow0, 32u * WN) : make_rsrc(a.Wq, 0u);
-#pragma unroll
-                for (int j = 0; j < WN; ++j)
-                    S.sr[q][j] = __builtin_amdgcn_raw_buffer_load_b16(srr, (uint32_t)(16 * j + lrow) * 2, 0, 0);
-            }
-        }
-    };
-    // each group's epilogue completes inside the block of its MFMAs (see pin)
     auto pin_all = [&]() {
 #pragma unroll
         for (int i = 0; i < WM; ++i)
 #pragma unroll
-            for (int j = 0; j < WN; ++j) {
-                if constexpr (RAW) { pin(iacc[i][j]); pin(racc[i][j]); }
-                else pin(acc[i][j]);
+            for (int s = 0; s < SPW; ++s) {
+                if constexpr (RAW) { pin(iacc[i][s]); pin(racc[i][s]); }
+                else pin(acc[i][s]);
             }
-    };
-    auto compute = [&](const Stage& S, int c0) {
-#pragma unroll
-        for (int q = 0; q < kChunk; ++q) {
-            if (c0 + q >= ge) continue;
-            const int p = S.p[q];
-            i32x8 av[WM], wv[WN], rv[WN];
-            float sw_f[WN], sr_f[WN];
-#pragma unroll
-            for (int i = 0; i < WM; ++i) {
-                if constexpr (FQ) {
-                    const int row = i * 16 + lrow;
-                    uint4 v = make_uint4(0, 0, 0, 0);
-                    if (row < M) v = *reinterpret_cast<const uint4*>(&xs[(int64_t)row * (K / 2) + (c0 + q) * kGroupBytes + lq * 16]);
-                    av[i] = unfold_codes(v);
-                } else {
-                    av[i] = unfold_codes(S.x[q][i]);
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < WN; ++j) {
-                wv[j] = unfold_codes(S.w[q][j]);
-                sw_f[j] = RAW ? 0.f : half_bits_to_float(S.sw[q][j]) * kCodeScale;
-                rv[j] = i32x8{0, 0, 0, 0, 0, 0, 0, 0};
-                sr_f[j] = 0.f;
-            }
-            if (p >= 0) {
-#pragma unroll
-                for (int j = 0; j < WN; ++j) {
-                    rv[j] = unfold_codes(S.r[q][j]);
-                    sr_f[j] = RAW ? 0.f : half_bits_to_float(S.sr[q][j]) * kCodeScale;
-                }
-#pragma unroll
-                for (int i = 0; i < WM; ++i)
-                    group_row<WN, RAW, true>(av[i], wv, rv, sw_f, sr_f, acc[i], iacc[i], racc[i]);
-                pin_all();
-            } else {
-#pragma unroll
-                for (int i = 0; i < WM; ++i)
-                    group_row<WN, RAW, false>(av[i], wv, rv, sw_f, sr_f, acc[i], iacc[i], racc[i]);
-                pin_all();
-            }
-        }
     };
 
-    // FQ, part 1: this thread's chunks of X (loaded first, so that they are
-    // the first loads to land) and their per-row maxima
+    // One stream of items per wave: its dense groups (item j < ng: group
+    // gb + j, B = the strips' W pieces, scales s_w), then its residual entries
+    // (item ng + e: block p = pb + e at group res_kb[p], B = the strips' R
+    // pieces, scales s_r), through one ring of GD register stages, so the
+    // residual blocks continue the pipeline without a bubble.
+    struct Stage {
+        uint4 x[WM], b[SPW];
+        uint16_t sc[SPW];
+        int g;
+        bool res;
+    };
+    const int nitems = ng + ne;
+    // group of the next residual entry to issue (scalar, loaded one entry ahead)
+    int kb_next = (ne > 0) ? (int)res_kb[pb] : 0;
+    auto load_item = [&](Stage& S, int j) {
+        const bool live = j < nitems;
+        // past the last item every offset gets bit 31: past every resource
+        // (arithmetic rather than a select, which the compiler turns into
+        // branches that reorder the ring's loads)
+        const uint32_t dead = (uint32_t)(nitems - 1 - j) & kPastEnd;
+        const bool res = j >= ng;                        // uniform
+        const int p = pb + (j - ng);
+        int g = gb + j;
+        if (res && live) {
+            g = kb_next;
+            if (j + 1 - ng < ne) kb_next = (int)res_kb[p + 1];
+        }
+        S.g = g;
+        S.res = res;
+        if constexpr (!FQ) {
+#pragma unroll
+            for (int i = 0; i < WM; ++i) S.x[i] = bload16(rx, x_offset(g, i) | dead, 0);
+        }
+        // resources built from the selected base (a select of scalars, not of
+        // two descriptors, which the compiler would turn into branches)
+        const bool use_r = res && a.Rq != nullptr;
+        const __amdgpu_buffer_rsrc_t rb =
+            make_rsrc(use_r ? (const void*)a.Rq : (const void*)a.Wq, use_r ? a.rq_bytes : a.wq_bytes);
+        const uint32_t row0 = (res ? (uint32_t)p * kGroup + (uint32_t)roff : (uint32_t)g * (uint32_t)N + (uint32_t)n0) +
+                              (uint32_t)nw;
+#pragma unroll
+        for (int s = 0; s < SPW; ++s)
+            S.b[s] = bload16(rb, ((row0 + 16u * s) * kGroupBytes + loff) | dead, 0);
+        if constexpr (!RAW) {
+            const bool use_sr = res && a.s_r != nullptr;
+            const __amdgpu_buffer_rsrc_t rs =
+                make_rsrc(use_sr ? (const void*)a.s_r : (const void*)a.s_w, use_sr ? a.sr_bytes : a.sw_bytes);
+#pragma unroll
+            for (int s = 0; s < SPW; ++s)
+                S.sc[s] = __builtin_amdgcn_raw_buffer_load_b16(rs, ((row0 + 16u * s + (uint32_t)lrow) * 2u) | dead, 0, 0);
+        }
+    };
+    auto compute_item = [&](const Stage& S, auto res_c) {
+        constexpr bool RES = decltype(res_c)::value;
+        i32x8 av[WM];
+#pragma unroll
+        for (int i = 0; i < WM; ++i) av[i] = unfold_codes(FQ ? x_lds(S.g, i) : S.x[i]);
+#pragma unroll
+        for (int s = 0; s < SPW; ++s) {
+            const i32x8 bv = unfold_codes(S.b[s]);
+            const float sc = RAW ? 0.f : half_bits_to_float(S.sc[s]) * kCodeScale;
+#pragma unroll
+            for (int i = 0; i < WM; ++i) {
+                const f32x4 t = mfma_codes(av[i], bv, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if constexpr (!RAW) acc[i][s][r] = __builtin_fmaf(sc, t[r], acc[i][s][r]);
+                    else if constexpr (RES) racc[i][s][r] += (int)(t[r] * kCodeScale);
+                    else iacc[i][s][r] += (int)(t[r] * kCodeScale);   // exact integer
+                }
+            }
+        }
+        pin_all();
+    };
+
+    // FQ, part 1: this thread's chunks of X, loaded first so that they are
+    // the first loads to land
     const int nxc = K / 16;
     uint4 xv[FQ ? kFusedCPT : 1][2];
-    // row of chunk index idx (M <= kFusedMaxM rows of nxc chunks)
     auto row_of = [&](int idx) { return (idx >= nxc) + (idx >= 2 * nxc) + (idx >= 3 * nxc); };
     if constexpr (FQ) {
         if (threadIdx.x < kFusedMaxM) amax_sh[threadIdx.x] = 0u;
@@ -1046,9 +1071,15 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
         }
     }
 
-    Stage SA, SB;
-    int c0 = gb;
-    if (c0 < ge) load(c0, SA);
+    // (the scheduling barriers keep each stage's loads together and the
+    // stages in ring order, so the wait for a stage counts exactly the
+    // stages issued after it)
+    Stage St[GD];
+    static_for<GD>([&](auto dc) {
+        constexpr int d = decltype(dc)::value;
+        load_item(St[d], d);
+        __builtin_amdgcn_sched_barrier(0);
+    });
 
     if constexpr (FQ) {
         // FQ, part 2: row maxima across the workgroup (LDS atomic max on the
@@ -1083,59 +1114,60 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
         __syncthreads();
     }
 
-    while (c0 < ge) {
-        if (c0 + kChunk < ge) load(c0 + kChunk, SB);
-        compute(SA, c0);
-        c0 += kChunk;
-        if (c0 >= ge) break;
-        if (c0 + kChunk < ge) load(c0 + kChunk, SA);
-        compute(SB, c0);
-        c0 += kChunk;
+    for (int j0 = 0; j0 < nitems; j0 += GD) {
+        static_for<GD>([&](auto dc) {
+            constexpr int d = decltype(dc)::value;
+            const int j = j0 + d;
+            if (j < nitems) {
+                if (RAW && St[d].res) compute_item(St[d], std::true_type{});
+                else compute_item(St[d], std::false_type{});
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            load_item(St[d], j + GD);
+            __builtin_amdgcn_sched_barrier(0);
+        });
     }
 
-    // cross-wave reduction in wave order
-    if constexpr (RAW) {
+    // cross-wave reduction in wave order (the LDS rows of FQ are free once
+    // every wave is past its loops)
+    if constexpr (FQ) __syncthreads();
 #pragma unroll
-        for (int i = 0; i < WM; ++i)
+    for (int i = 0; i < WM; ++i)
 #pragma unroll
-            for (int j = 0; j < WN; ++j)
+        for (int s = 0; s < SPW; ++s)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    red[wave][((i * WN + j) * 4 + r) * 2 + 0][lane] = (uint32_t)iacc[i][j][r];
-                    red[wave][((i * WN + j) * 4 + r) * 2 + 1][lane] = (uint32_t)racc[i][j][r];
+            for (int r = 0; r < 4; ++r) {
+                const int v = (i * SPW + s) * 4 + r;
+                if constexpr (RAW) {
+                    red[((wave * kVals) + 2 * v) * 64 + lane] = (uint32_t)iacc[i][s][r];
+                    red[((wave * kVals) + 2 * v + 1) * 64 + lane] = (uint32_t)racc[i][s][r];
+                } else {
+                    red[((wave * kVals) + v) * 64 + lane] = __float_as_uint(acc[i][s][r]);
                 }
-    } else {
-#pragma unroll
-        for (int i = 0; i < WM; ++i)
-#pragma unroll
-            for (int j = 0; j < WN; ++j)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    red[wave][(i * WN + j) * 4 + r][lane] = __float_as_uint(acc[i][j][r]);
-    }
+            }
     __syncthreads();
-    // each thread finishes (slot, lane) pairs
-    constexpr int kSlots = WM * WN * 4;
-    for (int e = threadIdx.x; e < kSlots * 64; e += 64 * NW) {
-        const int slot = e / 64, l = e % 64;
-        const int ij = slot / 4, r = slot % 4;
-        const int i = ij / WN, j = ij % WN;
-        const int m = i * 16 + 4 * (l >> 4) + r;
-        const int n = n0 + j * 16 + (l & 15);
+    constexpr int kSlots = WM * SPW * 4;
+    for (int e = threadIdx.x; e < WG2 * kSlots * 64; e += 64 * NW) {
+        const int wp = e / (kSlots * 64), v = (e / 64) % kSlots, l = e % 64;
+        const int is = v / 4, r = v % 4;
+        const int i = is / SPW, s = is % SPW;
+        const int m = m0 + 16 * (WM * (wp / WGN) + i) + 4 * (l >> 4) + r;
+        const int n = n0 + 16 * (WN * (wp % WGN) + s) + (l & 15);
         if (m >= M) continue;
         if constexpr (RAW) {
             int32_t tb = 0, tr = 0;
-            for (int w = 0; w < NW; ++w) {
-                tb += (int32_t)red[w][slot * 2 + 0][l];
-                tr += (int32_t)red[w][slot * 2 + 1][l];
+            for (int k = 0; k < KS; ++k) {
+                const int w = k * WG2 + wp;
+                tb += (int32_t)red[((w * kVals) + 2 * v) * 64 + l];
+                tr += (int32_t)red[((w * kVals) + 2 * v + 1) * 64 + l];
             }
             a.Tb[(int64_t)m * N + n] = tb;
             a.Tr[(int64_t)m * N + n] = tr;
         } else {
-            float v = 0.f;
-            for (int w = 0; w < NW; ++w) v += __uint_as_float(red[w][slot][l]);
+            float sum = 0.f;
+            for (int k = 0; k < KS; ++k) sum += __uint_as_float(red[(((k * WG2 + wp) * kVals) + v) * 64 + l]);
             const uint16_t sxb = FQ ? sx_sh[m] : a.s_x[m];
-            a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * v);
+            a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * sum);
         }
     }
 }
@@ -1145,6 +1177,40 @@ __global__ __launch_bounds__(64 * NW) void gemm_skinny_kernel(GemmArgs a) {
 // --------------------------------------------------------------------------
 constexpr int kSkinnyMaxM = 32;
 constexpr int kSkinnyAutoM = 32;   // AUTO picks the skinny kernel up to this M
+
+// Strips per decode workgroup: the most that still give every CU a
+// workgroup (a workgroup's adjacent strips share DRAM pages and the block
+// row's CSR entries); two at most for 17 to 32 rows (register and LDS budget).
+constexpr int kCUs = 256;
+static int decode_spw(int M, int N) {
+    const int S = N / 16;
+    if (M <= 16 && S / 4 >= kCUs) return 4;
+    if (S / 2 >= kCUs) return 2;
+    return 1;
+}
+
+template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ>
+static void launch_stream(const GemmArgs& a, size_t xs_bytes, hipStream_t stream) {
+    const size_t red = stream_red_bytes<WM, WN, RAW>();
+    const int64_t tiles = (int64_t)((a.M + 16 * WM * WGM - 1) / (16 * WM * WGM)) * (a.N / (16 * WN * WGN));
+    hipLaunchKernelGGL((gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ>), dim3((unsigned)tiles),
+                       dim3(64 * kDecodeWaves), xs_bytes > red ? xs_bytes : red, stream, a);
+}
+
+template <int WM, int SPW, bool RAW, bool FQ>
+static void launch_decode_spw(const GemmArgs& a, size_t xs_bytes, hipStream_t stream) {
+    launch_stream<WM, SPW, 1, 1, RAW, FQ>(a, xs_bytes, stream);
+}
+
+// xs_bytes: LDS for the quantised rows (fused quantisation), 0 otherwise
+template <int WM, bool RAW, bool FQ>
+static void launch_decode(const GemmArgs& a, int spw, size_t xs_bytes, hipStream_t stream) {
+    if constexpr (WM == 1) {
+        if (spw == 4) return launch_decode_spw<WM, 4, RAW, FQ>(a, xs_bytes, stream);
+    }
+    if (spw >= 2) return launch_decode_spw<WM, 2, RAW, FQ>(a, xs_bytes, stream);
+    launch_decode_spw<WM, 1, RAW, FQ>(a, xs_bytes, stream);
+}
 
 // The 256 x 256 tile is used when every CU gets at least one tile; smaller
 // problems keep the 128 x 128 tile (and split-K when even those are few).
@@ -1163,18 +1229,16 @@ static i32x4 host_buf_desc(const void* base, uint32_t bytes) {
 // to give every CU two workgroups, as long as its 64 x 64 tiles fit on the
 // CUs in one round (one workgroup per CU: its ring takes most of the LDS).
 constexpr int kMediumTargetWGs = 512;
-constexpr int kCUs = 256;
 static bool medium_preferred(int M, int N) {
     return (int64_t)((M + kTB - 1) / kTB) * (N / kTB) < kMediumTargetWGs &&
            (int64_t)((M + 63) / 64) * (N / 64) <= kCUs;
 }
 
+// Byte sizes of the operands and buffer resources spanning each of them.
+// Whole-operand resources take 32-bit offsets (and offsets from 2 GB up serve
+// as "past the end"), so every operand must stay below 2 GB.
 template <bool RAW>
-static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspace, size_t ws_bytes,
-                        hipStream_t stream) {
-    // whole-operand buffer resources take 32-bit offsets (and offsets from
-    // 2 GB up serve as "past the end")
-    GemmArgs a = args;
+static mq_status operand_resources(GemmArgs& a) {
     const uint64_t G = (uint64_t)(a.K / kGroup);
     const uint64_t sizes[5] = {G * a.M * kGroupBytes, G * a.N * kGroupBytes, (uint64_t)a.nnzb * kTB * kGroupBytes,
                                G * a.N * 2, (uint64_t)a.nnzb * kTB * 2};
@@ -1194,6 +1258,15 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
     a.rr = desc(a.Rq, a.rq_bytes);
     a.rsw = desc(a.s_w, a.sw_bytes);
     a.rsr = desc(a.s_r, a.sr_bytes);
+    return MQ_OK;
+}
+
+template <bool RAW>
+static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspace, size_t ws_bytes,
+                        hipStream_t stream) {
+    GemmArgs a = args;
+    const mq_status rs = operand_resources<RAW>(a);
+    if (rs != MQ_OK) return rs;
     if (variant == MQ_VARIANT_AUTO)
         variant = a.M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY
                   : large_tiles_fit(a.M, a.N) ? MQ_VARIANT_TILED_LARGE
@@ -1217,12 +1290,8 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
         hipLaunchKernelGGL((gemm_tiled_kernel<8, 4, RAW, false>), dim3((unsigned)tiles), dim3(TS::kThreads), 0,
                            stream, a, 0, (float*)nullptr);
     } else if (variant == MQ_VARIANT_SKINNY) {
-        constexpr int NW = 8;
-        const dim3 grid(a.N / 16), block(64 * NW);
-        if (a.M <= 16)
-            hipLaunchKernelGGL((gemm_skinny_kernel<1, 1, NW, RAW>), grid, block, 0, stream, a);
-        else
-            hipLaunchKernelGGL((gemm_skinny_kernel<2, 1, NW, RAW>), grid, block, 0, stream, a);
+        if (a.M <= 16) launch_decode<1, RAW, false>(a, decode_spw(a.M, a.N), 0, stream);
+        else launch_decode<2, RAW, false>(a, decode_spw(a.M, a.N), 0, stream);
     } else {
         const int64_t tiles = (int64_t)((a.M + kTB - 1) / kTB) * (a.N / kTB);
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
@@ -1373,9 +1442,10 @@ extern "C" mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
         GemmArgs a{M, N, K, nullptr, nullptr, Wq, static_cast<const uint16_t*>(s_w),
                    nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq, static_cast<const uint16_t*>(s_r),
                    static_cast<uint16_t*>(Y), ldy, nullptr, nullptr, static_cast<const uint16_t*>(X), ldx};
-        constexpr int NW = 8;
-        hipLaunchKernelGGL((gemm_skinny_kernel<1, 1, NW, false, true>), dim3(N / 16), dim3(64 * NW),
-                           (size_t)M * (K / 2), stream, a);
+        a.nnzb = nnzb;
+        st = operand_resources<false>(a);
+        if (st != MQ_OK) return st;
+        launch_decode<1, false, true>(a, decode_spw(M, N), (size_t)M * (K / 2), stream);
         return mq_host::launch_status();
     }
     // quantise into the workspace, then the fused GEMM

@@ -12,52 +12,91 @@
 
 namespace mq {
 
-// Residual kernel: a workgroup of four waves owns a 64 x 128 tile (64 rows of
-// the output, one 128-column block row); wave w owns rows 16 w .. 16 w + 15
-// as eight 16 x 16 sub-tiles.  For each residual block (nb, kb) of the block
-// row it multiplies the X rows' group kb (from memory) with the block's R
-// tile (from memory, shared through L2), scales each block row's sums by s_r
-// and accumulates in fp32.
-__global__ __launch_bounds__(256) void residual_only_kernel(int M, int N, const uint8_t* __restrict__ Xq,
+// Residual kernel: a workgroup of eight waves owns a (16 WGMR) x 128 tile (one
+// 128-column block row); WGMR waves along M, each with 16 rows and the eight
+// 16-column sub-tiles, and 8 / WGMR splits of the block row's CSR entries
+// (contiguous runs).  Each wave streams its blocks through a two-stage
+// register ring (X fragment of the block's group and R fragments, read from
+// memory), scales each block row's sums by s_r, and the splits are added
+// through LDS in split order.  WGMR = 1 for M <= 16, else 4.
+template <int WGMR>
+__global__ __launch_bounds__(512) void gemm_residual_kernel(int M, int N, const uint8_t* __restrict__ Xq,
                                                             const int32_t* __restrict__ rowptr,
                                                             const int32_t* __restrict__ res_kb,
                                                             const uint8_t* __restrict__ Rq,
                                                             const uint16_t* __restrict__ s_r,
                                                             float* __restrict__ P) {
+    constexpr int KS = 8 / WGMR;
+    __shared__ __attribute__((aligned(16))) float red[8][32][64];
     const int nb = blockIdx.y;
-    const int rp = rowptr[nb], re = rowptr[nb + 1];
-    if (rp == re) return;
+    const int rp = rowptr[nb], cnt = rowptr[nb + 1] - rp;
+    if (cnt == 0) return;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave % WGMR, split = wave / WGMR;
     const int lrow = lane & 15, lq = lane >> 4;
-    const int m0 = blockIdx.x * 64 + 16 * wave;
+    const int m0 = blockIdx.x * 16 * WGMR + 16 * wm;
     const int xr = m0 + lrow;
-    f32x4 acc[8];
-#pragma unroll
-    for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int p = rp; p < re; ++p) {
+    const int per = cnt / KS, extra = cnt % KS;
+    const int pb = rp + split * per + min(split, extra);
+    const int ne = per + (split < extra ? 1 : 0);
+
+    struct Stage {
+        uint4 x, r[8];
+        uint16_t s[8];
+    };
+    auto load = [&](Stage& S, int e) {
+        S.x = make_uint4(0u, 0u, 0u, 0u);
+        if (e >= ne) return;
+        const int p = pb + e;
         const int g = res_kb[p];
-        uint4 xa = make_uint4(0u, 0u, 0u, 0u);
-        if (xr < M) xa = ldg16(Xq + piece_offset(M, xr, g) + 16 * lq);
-        const i32x8 av = unfold_codes(xa);
+        if (xr < M) S.x = ldg16(Xq + piece_offset(M, xr, g) + 16 * lq);
         const uint8_t* rt = Rq + (int64_t)p * kGroup * kGroupBytes;
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
-            const int row = 16 * c + lrow;                       // row of the R tile
-            const i32x8 bv = unfold_codes(ldg16(rt + row * kGroupBytes + 16 * lq));
-            const f32x4 t = mfma_codes(av, bv, f32x4{0.f, 0.f, 0.f, 0.f});
-            const float sr = half_bits_to_float(s_r[(int64_t)p * kGroup + row]) * kCodeScale;
+            S.r[c] = ldg16(rt + (16 * c + lrow) * kGroupBytes + 16 * lq);
+            S.s[c] = s_r[(int64_t)p * kGroup + 16 * c + lrow];
+        }
+    };
+    f32x4 acc[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](const Stage& S) {
+        const i32x8 av = unfold_codes(S.x);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            const f32x4 t = mfma_codes(av, unfold_codes(S.r[c]), f32x4{0.f, 0.f, 0.f, 0.f});
+            const float sr = half_bits_to_float(S.s[c]) * kCodeScale;
 #pragma unroll
             for (int r = 0; r < 4; ++r) acc[c][r] = __builtin_fmaf(sr, t[r], acc[c][r]);
         }
+#pragma unroll
+        for (int c = 0; c < 8; ++c) asm volatile("" : "+v"(acc[c]));   // epilogue completes in this block
+    };
+    Stage S0, S1;
+    load(S0, 0);
+    load(S1, 1);
+    for (int e = 0; e < ne; e += 2) {
+        compute(S0);
+        load(S0, e + 2);
+        if (e + 1 < ne) compute(S1);
+        load(S1, e + 3);
     }
     // lane holds rows 4 (lane / 16) + r of each sub-tile, column lane % 16
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int m = m0 + 4 * lq + r;
-        if (m >= M) continue;
+    for (int c = 0; c < 8; ++c)
 #pragma unroll
-        for (int c = 0; c < 8; ++c) P[(int64_t)m * N + nb * kGroup + 16 * c + lrow] = acc[c][r];
-    }
+        for (int r = 0; r < 4; ++r) red[wave][c * 4 + r][lane] = acc[c][r];
+    __syncthreads();
+    if (split != 0) return;
+#pragma unroll
+    for (int c = 0; c < 8; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int m = m0 + 4 * lq + r;
+            float v = 0.f;
+            for (int k = 0; k < KS; ++k) v += red[k * WGMR + wm][c * 4 + r][lane];
+            if (m < M) P[(int64_t)m * N + nb * kGroup + 16 * c + lrow] = v;
+        }
 }
 
 // Y[m, n] <- fp16(f32(Y[m, n]) + s_x[m] P[m, n]) on block rows with blocks.
@@ -110,8 +149,12 @@ extern "C" mq_status mq_unfused_gemm(int M, int N, int K, const uint8_t* Xq, con
     if (st != MQ_OK || nnzb == 0) return st;
     // 2. sparse residual GEMM into P
     const int NB = N / kGroup;
-    hipLaunchKernelGGL(residual_only_kernel, dim3((unsigned)((M + 63) / 64), (unsigned)NB), dim3(256), 0, stream, M,
-                       N, Xq, res_rowptr, res_kb, Rq, static_cast<const uint16_t*>(s_r), P);
+    if (M <= 16)
+        hipLaunchKernelGGL((gemm_residual_kernel<1>), dim3(1u, (unsigned)NB), dim3(512), 0, stream, M, N, Xq,
+                           res_rowptr, res_kb, Rq, static_cast<const uint16_t*>(s_r), P);
+    else
+        hipLaunchKernelGGL((gemm_residual_kernel<4>), dim3((unsigned)((M + 63) / 64), (unsigned)NB), dim3(512), 0,
+                           stream, M, N, Xq, res_rowptr, res_kb, Rq, static_cast<const uint16_t*>(s_r), P);
     st = mq_host::launch_status();
     if (st != MQ_OK) return st;
     // 3. reduce-add

@@ -244,3 +244,60 @@ def test_unfused_baseline_matches_oracle(tc, mq, orc, M, N, K, nnzb):
     empty = np.flatnonzero(np.diff(rowptr) == 0)
     cols = (empty[:, None] * B + np.arange(B)[None, :]).ravel()
     assert np.array_equal(host(Y.view(tc.int16))[:, cols], host(Yd.view(tc.int16))[:, cols])
+
+
+# ------------------------------------------------------------ decode kernel --
+DECODE = [(1, 16384, 1024, "full"), (16, 16384, 512, "rand"), (3, 8192, 1280, "full"),
+          (17, 8192, 640, "rand"), (32, 16384, 384, "full"), (5, 4096, 128, "full"),
+          (1, 4096, 896, "none"), (32, 1024, 2048, "full"), (9, 2048, 28672, "rand")]
+
+
+def decode_csr(N, K, kind, rng):
+    """CSR with every block of some block rows (so each wave of a workgroup
+    gets entries, and rows with fewer entries than waves occur), random
+    blocks elsewhere; or random only; or none."""
+    NB, KB = N // B, K // B
+    sel = np.zeros((NB, KB), bool)
+    if kind == "full":
+        sel[rng.choice(NB, max(1, NB // 8), replace=False)] = True
+        sel |= rng.random((NB, KB)) < 0.05
+    elif kind == "rand":
+        sel = rng.random((NB, KB)) < 0.1
+    rowptr = np.zeros(NB + 1, np.int32)
+    rowptr[1:] = np.cumsum(sel.sum(1))
+    kb = np.concatenate([np.flatnonzero(r) for r in sel]).astype(np.int32) if sel.any() else np.zeros(0, np.int32)
+    return rowptr, kb, sel
+
+
+@pytest.mark.parametrize("M,N,K,kind", DECODE, ids=[f"M{m}_N{n}_K{k}_{c}" for m, n, k, c in DECODE])
+def test_decode_kernel_every_output(tc, mq, orc, M, N, K, kind):
+    """The decode kernel over its strip counts (1, 2, 4 strips of 16 columns
+    per workgroup), row tiles (M <= 16, <= 32), K with fewer groups than
+    waves, full and empty block rows: Tb, Tr bit-exact, Y within the bar,
+    and mq_linear's one-kernel path (quantisation inside) at M <= 4."""
+    from gpu_util import gpu_pw, orc_pw, dev_x
+    rng = np.random.default_rng(M * 31 + N + K)
+    rowptr, kb, sel = decode_csr(N, K, kind, rng)
+    nnzb = int(rowptr[-1])
+    Xq = rng.integers(0, 256, (M, K // 2), dtype=np.uint8)
+    s_x = rng.uniform(0.01, 2.0, M).astype(np.float16).view(np.uint16)
+    Wq = rng.integers(0, 256, (N, K // 2), dtype=np.uint8)
+    s_w = rng.uniform(1e-3, 0.05, (N, K // B)).astype(np.float16).view(np.uint16)
+    Rq = rng.integers(0, 256, (nnzb, B, B // 2), dtype=np.uint8)
+    s_r = rng.uniform(1e-4, 5e-3, (nnzb, B)).astype(np.float16).view(np.uint16)
+    Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    Xd = dev_x(tc, Xq)
+    Tb, Tr = mq.fused_gemm_acc_i32(Xd, pw, variant="skinny")
+    Y = mq.fused_gemm(Xd, dev(tc, s_x).view(tc.float16), pw, variant="skinny")
+    tc.cuda.synchronize()
+    assert np.array_equal(host(Tb), Tb_ref) and np.array_equal(host(Tr), Tr_ref)
+    assert maxabsrel(Y, Y64) <= TIGHT
+    if M <= 4 and M * K // 2 <= 65536:
+        X = synth.gen_act(M, K, 11 + M + K)
+        Xq_r, sx_r = orc.quantize_act(X)
+        _, _, Y64x = orc.linear(Xq_r, sx_r, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+        assert mq.linear_workspace_bytes(M, N, K) == 0
+        Yl = mq.linear(dev(tc, X), pw)
+        tc.cuda.synchronize()
+        assert maxabsrel(Yl, Y64x) <= TIGHT
