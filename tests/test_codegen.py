@@ -101,7 +101,7 @@ def asm():
 
 def test_gemm_kernels_have_mfma(asm):
     names = [k for k in asm if "gemm" in k]
-    assert any("tiled" in k for k in names) and any("decode" in k for k in names)
+    assert any("tiled" in k for k in names) and any("stream" in k for k in names)
     for k in names:
         assert any("v_mfma_f32_16x16x128_f8f6f4" in l for l in asm[k]), k
 
