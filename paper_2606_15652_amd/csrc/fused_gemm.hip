@@ -16,20 +16,22 @@
 // already staged for the dense term and accumulated into the same output
 // registers.
 //
-// Three kernel families share that inner step:
+// Two kernel families share that inner step:
 //  * tiled  (prefill):  a workgroup owns a 256 x 256 (eight waves, one per CU)
 //    or 128 x 128 (four waves, two per CU) output tile; the packed X, W and
 //    (when present) R tiles of each group are copied by the LDS DMA into a
 //    3-stage ring.
-//  * medium (M of a few hundred): a workgroup owns a 64 x 64 or 32 x 64 tile;
-//    its eight waves split the K-loop in two halves over an 8-slot ring.
-//  * skinny (decode, small M): a workgroup owns 16 output columns and all M
-//    rows; its waves split the K-loop, each streaming a contiguous run of
-//    groups, and the fp32 partial tiles are reduced through LDS in wave order
-//    (deterministic).
+//  * streaming (decode and medium M): the eight waves of a workgroup split
+//    the K groups, and the tile's residual blocks, into contiguous runs; each
+//    wave streams its run through a ring of register stages (no LDS staging,
+//    no barrier until the end), and the partial tiles are added through LDS
+//    in wave order (deterministic).  Decode (M <= 32): all rows, 16, 32 or 64
+//    columns.  Medium M: 64 x 64 (or 32 x 64) tiles, each wave the whole tile
+//    over an eighth of K, so every operand piece is read once per workgroup.
 #include "mq_device.h"
 
 #include <stddef.h>
+
 #include <type_traits>
 
 namespace mq {
@@ -625,232 +627,6 @@ static int tiled_splits(int M, int N, int K) {
 }
 
 // --------------------------------------------------------------------------
-// Medium kernel (M from a few dozen to about a thousand rows): a workgroup owns
-// a TM x 64 output tile (TM = 32 WMB), small enough that the problem has
-// hundreds of tiles without split-K over workgroups.  Its eight waves form two
-// K-halves (waves 0-3 take the even groups, waves 4-7 the odd ones: two waves
-// per SIMD, each with a short dependency chain per group) of a 2 x 2 grid:
-// wave (wm, wn) of a half owns rows 16 WMB wm .. and columns 32 wn .., i.e.
-// WMB x 2 sub-tiles.  The halves' sums are added through LDS at the end (in
-// fixed order).  A 64-column tile is half of a residual block row: its R tile
-// is the matching 64 rows (4 KB) of the block, its residual scales the
-// matching 64 of the block's 128.  Per group the X, W (and R) tiles go by LDS
-// DMA into a ring of kStages slots, loaded by the half that computes the
-// group, three group pairs ahead.
-// --------------------------------------------------------------------------
-template <int WMB, bool RAW>
-__global__ __launch_bounds__(512) void gemm_medium_kernel(GemmArgs a) {
-    constexpr int TM = 32 * WMB, TN = 64, kRow = kGroupBytes, kStages = 8;
-    struct Slot {
-        uint8_t x[TM * kRow], w[TN * kRow], r[TN * kRow];
-        uint16_t sw[128], sr[128];                          // 64 used; 256 B per 64-lane dword DMA
-    };
-    __shared__ __attribute__((aligned(16))) Slot ring[kStages];
-
-    const int M = a.M, N = a.N, K = a.K;
-    const int G = K / kGroup;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
-    const int half = wave >> 2, w4 = wave & 3;
-    const int wm = w4 >> 1, wn = w4 & 1;
-    const int lrow = lane & 15, lq = lane >> 4;
-    const int tiles_m = (M + TM - 1) / TM, tiles_n = N / TN;
-    int tm, tn;
-    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * TM, n0 = tn * TN;
-    const int br = n0 / kTB, roff = n0 % kTB;               // residual block row, row offset inside it
-
-    // CSR walk of the block row (scalar; every wave walks it, so each knows
-    // which groups have a residual block; next block's group loaded ahead)
-    const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
-    int rp = 0, re = 0, nk = 0x7fffffff, nk2 = 0x7fffffff;  // groups of the next two blocks
-    if (a.rowptr) {
-        const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
-        rp = rowptr[br];
-        re = rowptr[br + 1];
-        if (rp < re) nk = res_kb[rp];
-        if (rp + 1 < re) nk2 = res_kb[rp + 1];
-    }
-
-    // DMA, by the half that computes the group: its wave w4 fills 1 KB block
-    // w4 (16 rows) of the W and R tiles and, when w4 < 2 WMB, of the X tile;
-    // wave w4 = 0 the weight scales, w4 = 1 the residual scales (64 lanes x
-    // 4 B, 128 B of them in use).  Lane l takes row 16 w4 + l / 4 and physical
-    // chunk l % 4 (swizzle as in the tiled kernel).  Every load goes through
-    // a resource spanning its whole operand (built by the host), so the
-    // per-group addressing is a vector offset.  A wave issues base_n loads for
-    // a group and res_n more when it has a residual block; it waits on that
-    // count.  X rows past M (last tile) read other bytes of the operand or the
-    // zero tail; they only feed output rows that are never written.
-    const int drow = 16 * w4 + (lane >> 2);
-    const uint32_t chunk = (uint32_t)(((lane & 3) ^ ((drow >> 1) & 3)) << 4);
-    const bool hx = w4 < 2 * WMB;
-    const int base_n = (hx ? 1 : 0) + 1 + ((!RAW && w4 == 0) ? 1 : 0);
-    const int res_n = 1 + ((!RAW && w4 == 1) ? 1 : 0);
-    const uint32_t vx0 = (uint32_t)(m0 + drow) * kRow + chunk;
-    const uint32_t vw0 = (uint32_t)(n0 + drow) * kRow + chunk;
-    const uint32_t vs0 = (uint32_t)n0 * 2 + (uint32_t)lane * 4;
-    const uint32_t vr0 = (uint32_t)(roff + drow) * kRow + chunk;              // + p * 8 KB
-    const uint32_t vsr0 = (uint32_t)roff * 2 + (uint32_t)lane * 4;           // + p * 256 B
-    const uint32_t ring0 = lds_addr(&ring[0]);
-    const uint32_t ox = (uint32_t)offsetof(Slot, x) + 1024u * w4;
-    const uint32_t ow = (uint32_t)offsetof(Slot, w) + 1024u * w4, orr = (uint32_t)offsetof(Slot, r) + 1024u * w4;
-    // group g's loads (by this wave; g < G); p: its residual block (-1: none)
-    auto issue = [&](int g, int p) {
-        const uint32_t sb = ring0 + (uint32_t)(g & (kStages - 1)) * (uint32_t)sizeof(Slot);
-        if (hx) dma16(a.rx, sb + ox, vx0 + (uint32_t)g * ((uint32_t)M * kRow));
-        dma16(a.rw, sb + ow, vw0 + (uint32_t)g * ((uint32_t)N * kRow));
-        if constexpr (!RAW)
-            if (w4 == 0) dma4(a.rsw, sb + (uint32_t)offsetof(Slot, sw), vs0 + (uint32_t)g * ((uint32_t)N * 2));
-        if (p >= 0) {
-            dma16(a.rr, sb + orr, vr0 + (uint32_t)p * (kTB * kRow));
-            if constexpr (!RAW)
-                if (w4 == 1) dma4(a.rsr, sb + (uint32_t)offsetof(Slot, sr), vsr0 + (uint32_t)p * (kTB * 2));
-        }
-    };
-    // the CSR walk, one group at a time (all waves, in group order); the
-    // entry after the next is loaded ahead, so a compare never waits for it
-    auto next_block = [&](int g) -> int {
-        int p = -1;
-        if (g < G && nk == g) {
-            p = rp++;
-            nk = nk2;
-            nk2 = rp + 1 < re ? res_kb[rp + 1] : 0x7fffffff;
-        }
-        return p;
-    };
-    // loads this wave issues for group g with residual flag r
-    auto loads = [&](int g, bool r) -> int { return g < G ? base_n + (r ? res_n : 0) : 0; };
-
-    f32x4 acc[WMB][2];
-    i32x4 iacc[WMB][2], racc[WMB][2];
-#pragma unroll
-    for (int i = 0; i < WMB; ++i)
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            acc[i][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-            iacc[i][c] = i32x4{0, 0, 0, 0};
-            racc[i][c] = i32x4{0, 0, 0, 0};
-        }
-    const int wrow = 16 * WMB * wm;
-
-    // One pass over a staged group: the dense pass (RES false) multiplies the
-    // X tile with the W tile, the residual pass (RES true) with the R tile.
-    // Passes rather than one variant with both: a single code path per pass
-    // keeps the accumulators in fixed registers.
-    auto compute = [&](const Slot& S, auto res) {
-        constexpr bool RES = decltype(res)::value;
-        const uint8_t* bt = RES ? S.r : S.w;
-        const uint16_t* st = RES ? S.sr : S.sw;
-        i32x8 b[2];
-        float bs[2];
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            const int col = 32 * wn + 16 * c + lrow;       // row of the W and R tiles
-            b[c] = unfold_codes(*reinterpret_cast<const uint4*>(&bt[col * kRow + (swz(col, lq) << 4)]));
-            bs[c] = RAW ? 0.f : half_bits_to_float(st[col]) * kCodeScale;
-        }
-        f32x4 t[WMB][2];
-#pragma unroll
-        for (int i = 0; i < WMB; ++i) {
-            const int row = wrow + 16 * i + lrow;
-            const i32x8 av = unfold_codes(*reinterpret_cast<const uint4*>(&S.x[row * kRow + (swz(row, lq) << 4)]));
-#pragma unroll
-            for (int c = 0; c < 2; ++c) t[i][c] = mfma_codes(av, b[c], f32x4{0.f, 0.f, 0.f, 0.f});
-        }
-#pragma unroll
-        for (int i = 0; i < WMB; ++i)
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    if constexpr (!RAW) acc[i][c][r] = __builtin_fmaf(bs[c], t[i][c][r], acc[i][c][r]);
-                    else if constexpr (!RES) iacc[i][c][r] += (int)(t[i][c][r] * kCodeScale);   // exact
-                    else racc[i][c][r] += (int)(t[i][c][r] * kCodeScale);
-                }
-                // the pass's epilogue completes inside this block (see pin)
-                if constexpr (!RAW) pin(acc[i][c]);
-                else if constexpr (!RES) pin(iacc[i][c]);
-                else pin(racc[i][c]);
-            }
-    };
-
-    // Group pairs: pair j is groups 2 j (half 0) and 2 j + 1 (half 1), in
-    // slots 2 j % kStages and the next.  `res` bit 2 j + h: group 2 j + h has a
-    // residual block (pairs in flight, relative to the current one).
-    static_assert(kStages == 8, "four pairs of slots");
-    uint32_t res = 0;
-#pragma unroll
-    for (int j = 0; j < 3; ++j) {
-        const int p0 = next_block(2 * j), p1 = next_block(2 * j + 1);
-        if (2 * j + half < G) issue(2 * j + half, half ? p1 : p0);
-        res |= ((p0 >= 0 ? 1u : 0u) | (p1 >= 0 ? 2u : 0u)) << (2 * j);
-    }
-    for (int g = 0; g < G; g += 2) {
-        // this wave's loads of pair g / 2 landed (its base loads of the next two
-        // pairs may stay in flight: counting only those is exact without
-        // residual blocks there and waits a little longer with them);
-        // everyone finished the previous pair, whose slots are refilled next
-        const int gh = g + half;
-        wait_vm_and_sync(loads(gh + 2, false) + loads(gh + 4, false));
-        const int p0 = next_block(g + 6), p1 = next_block(g + 7);
-        if (gh + 6 < G) issue(gh + 6, half ? p1 : p0);
-        res |= ((p0 >= 0 ? 1u : 0u) | (p1 >= 0 ? 2u : 0u)) << 6;
-        if (gh < G) {
-            compute(ring[gh & (kStages - 1)], std::false_type{});
-            if ((res >> half) & 1u) compute(ring[gh & (kStages - 1)], std::true_type{});
-        }
-        res >>= 2;
-    }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-    // half 1 hands its sums to half 0 through LDS (the ring is free once
-    // everyone is past the loop); half 0 adds them (fixed order) and writes
-    constexpr int kVals = WMB * 2 * 4 * (RAW ? 2 : 1);     // values per lane
-    static_assert(4 * 64 * kVals * 4 <= (int)sizeof(ring), "exchange fits in the ring");
-    uint32_t* xch = reinterpret_cast<uint32_t*>(&ring[0]);
-    __syncthreads();
-    if (half == 1) {
-#pragma unroll
-        for (int i = 0; i < WMB; ++i)
-#pragma unroll
-            for (int c = 0; c < 2; ++c)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int v = (i * 2 + c) * 4 + r;
-                    if constexpr (RAW) {
-                        xch[((w4 * kVals) + 2 * v) * 64 + lane] = (uint32_t)iacc[i][c][r];
-                        xch[((w4 * kVals) + 2 * v + 1) * 64 + lane] = (uint32_t)racc[i][c][r];
-                    } else {
-                        xch[((w4 * kVals) + v) * 64 + lane] = __float_as_uint(acc[i][c][r]);
-                    }
-                }
-    }
-    __syncthreads();
-    if (half == 1) return;
-#pragma unroll
-    for (int i = 0; i < WMB; ++i)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int m = m0 + wrow + 16 * i + 4 * lq + r;
-            if (m >= M) continue;
-            const float sx = RAW ? 0.f : half_bits_to_float(a.s_x[m]);
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                const int n = n0 + 32 * wn + 16 * c + lrow;
-                const int v = (i * 2 + c) * 4 + r;
-                if constexpr (RAW) {
-                    a.Tb[(int64_t)m * N + n] = iacc[i][c][r] + (int32_t)xch[((w4 * kVals) + 2 * v) * 64 + lane];
-                    a.Tr[(int64_t)m * N + n] = racc[i][c][r] + (int32_t)xch[((w4 * kVals) + 2 * v + 1) * 64 + lane];
-                } else {
-                    const float sum = acc[i][c][r] + __uint_as_float(xch[((w4 * kVals) + v) * 64 + lane]);
-                    a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(sx * sum);
-                }
-            }
-        }
-}
-
-// --------------------------------------------------------------------------
 // Decode kernel (M <= 32): a workgroup owns SPW adjacent 16-column strips
 // (16 SPW <= 64 columns, inside one 128-row block row) and all M rows.  Its
 // eight waves split the K groups into contiguous runs, and the block row's
@@ -878,21 +654,15 @@ struct StreamDepth {
     static constexpr int GD = 96 / kStageRegs < 2 ? 2 : 96 / kStageRegs > 6 ? 6 : 96 / kStageRegs;
 };
 
-// bytes of dynamic LDS: the quantised rows (FQ) and, after the main loops,
-// the cross-wave partial sums
-template <int WM, int WN, bool RAW>
-constexpr size_t stream_red_bytes() {
-    return (size_t)kDecodeWaves * WM * WN * 4 * (RAW ? 2 : 1) * 64 * 4;
-}
-
 // The streaming kernel: eight waves = KS = 8 / (WGM WGN) splits of the K
 // loop x a WGM x WGN grid of waves, each wave WM x WN sub-tiles of 16 x 16:
-// a (16 WM WGM) x (16 WN WGN) output tile.  Decode: WGM = WGN = 1 (all M <=
-// 32 rows, 16 WN columns, K over eight waves); medium M: 64 x 64 tiles of
-// 2 x 2 waves and two K splits.
+// a (16 WM WGM) x (16 WN WGN) output tile.  Decode: WM <= 2, WN = 1, 2 or 4
+// (all M <= 32 rows, K over eight waves); medium M: WM = 2 or 4, WN = 4 (the
+// whole 32 x 64 or 64 x 64 tile per wave, K over eight waves).
 template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ>
 __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs a) {
-    static_assert(WN * WGN == 1 || WN * WGN == 2 || WN * WGN == 4, "tile columns inside one block row");
+    static_assert(WN * WGN == 1 || WN * WGN == 2 || WN * WGN == 4 || WN * WGN == 8,
+                  "tile columns inside one block row");
     static_assert(!(FQ && RAW), "fused quantisation feeds the fp16 path");
     static_assert(!FQ || (WGM == 1 && WGN == 1), "fused quantisation: one tile of all rows");
     constexpr int NW = kDecodeWaves, WG2 = WGM * WGN, KS = NW / WG2;
@@ -900,14 +670,15 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
     constexpr int SPW = WN;
     constexpr int GD = StreamDepth<WM, WN>::GD;
-    constexpr int kVals = WM * SPW * 4 * (RAW ? 2 : 1);          // partial sums per lane
-    // FQ: packed codes of the M rows (M x K/2 bytes, row-major); afterwards
-    // the partial sums red[wave][value][lane]
+    constexpr int kAcc = WM * SPW * 4;                           // sums per lane and accumulator
+    // cross-wave partial sums red[wave][value][lane] (one accumulator per
+    // round: raw mode adds the base and then the residual sums); FQ: packed
+    // codes of the M rows (M x K/2 bytes, row-major) in dynamic LDS
+    __shared__ __attribute__((aligned(16))) uint32_t red[NW][kAcc][64];
     extern __shared__ __attribute__((aligned(16))) uint8_t dyn[];
     __shared__ uint32_t amax_sh[kFusedMaxM];
     __shared__ uint16_t sx_sh[kFusedMaxM];
     uint8_t* xs = dyn;
-    uint32_t* red = reinterpret_cast<uint32_t*>(dyn);
 
     const int M = a.M, N = a.N, K = a.K;
     const int G = K / kGroup;
@@ -1128,46 +899,41 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         });
     }
 
-    // cross-wave reduction in wave order (the LDS rows of FQ are free once
-    // every wave is past its loops)
-    if constexpr (FQ) __syncthreads();
+    // cross-wave reduction, splits added in split order (deterministic)
+    constexpr int kRounds = RAW ? 2 : 1;
 #pragma unroll
-    for (int i = 0; i < WM; ++i)
+    for (int round = 0; round < kRounds; ++round) {
+        if (round > 0) __syncthreads();                     // the previous round is read
 #pragma unroll
-        for (int s = 0; s < SPW; ++s)
+        for (int i = 0; i < WM; ++i)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int v = (i * SPW + s) * 4 + r;
-                if constexpr (RAW) {
-                    red[((wave * kVals) + 2 * v) * 64 + lane] = (uint32_t)iacc[i][s][r];
-                    red[((wave * kVals) + 2 * v + 1) * 64 + lane] = (uint32_t)racc[i][s][r];
-                } else {
-                    red[((wave * kVals) + v) * 64 + lane] = __float_as_uint(acc[i][s][r]);
+            for (int s = 0; s < SPW; ++s)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int v = (i * SPW + s) * 4 + r;
+                    uint32_t x;
+                    if constexpr (RAW) x = (uint32_t)(round == 0 ? iacc[i][s][r] : racc[i][s][r]);
+                    else x = __float_as_uint(acc[i][s][r]);
+                    red[wave][v][lane] = x;
                 }
+        __syncthreads();
+        for (int e = threadIdx.x; e < WG2 * kAcc * 64; e += 64 * NW) {
+            const int wp = e / (kAcc * 64), v = (e / 64) % kAcc, l = e % 64;
+            const int is = v / 4, r = v % 4;
+            const int i = is / SPW, s = is % SPW;
+            const int m = m0 + 16 * (WM * (wp / WGN) + i) + 4 * (l >> 4) + r;
+            const int n = n0 + 16 * (WN * (wp % WGN) + s) + (l & 15);
+            if (m >= M) continue;
+            if constexpr (RAW) {
+                int32_t t = 0;
+                for (int k = 0; k < KS; ++k) t += (int32_t)red[k * WG2 + wp][v][l];
+                (round == 0 ? a.Tb : a.Tr)[(int64_t)m * N + n] = t;
+            } else {
+                float sum = 0.f;
+                for (int k = 0; k < KS; ++k) sum += __uint_as_float(red[k * WG2 + wp][v][l]);
+                const uint16_t sxb = FQ ? sx_sh[m] : a.s_x[m];
+                a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * sum);
             }
-    __syncthreads();
-    constexpr int kSlots = WM * SPW * 4;
-    for (int e = threadIdx.x; e < WG2 * kSlots * 64; e += 64 * NW) {
-        const int wp = e / (kSlots * 64), v = (e / 64) % kSlots, l = e % 64;
-        const int is = v / 4, r = v % 4;
-        const int i = is / SPW, s = is % SPW;
-        const int m = m0 + 16 * (WM * (wp / WGN) + i) + 4 * (l >> 4) + r;
-        const int n = n0 + 16 * (WN * (wp % WGN) + s) + (l & 15);
-        if (m >= M) continue;
-        if constexpr (RAW) {
-            int32_t tb = 0, tr = 0;
-            for (int k = 0; k < KS; ++k) {
-                const int w = k * WG2 + wp;
-                tb += (int32_t)red[((w * kVals) + 2 * v) * 64 + l];
-                tr += (int32_t)red[((w * kVals) + 2 * v + 1) * 64 + l];
-            }
-            a.Tb[(int64_t)m * N + n] = tb;
-            a.Tr[(int64_t)m * N + n] = tr;
-        } else {
-            float sum = 0.f;
-            for (int k = 0; k < KS; ++k) sum += __uint_as_float(red[(((k * WG2 + wp) * kVals) + v) * 64 + l]);
-            const uint16_t sxb = FQ ? sx_sh[m] : a.s_x[m];
-            a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * sum);
         }
     }
 }
@@ -1191,10 +957,9 @@ static int decode_spw(int M, int N) {
 
 template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ>
 static void launch_stream(const GemmArgs& a, size_t xs_bytes, hipStream_t stream) {
-    const size_t red = stream_red_bytes<WM, WN, RAW>();
     const int64_t tiles = (int64_t)((a.M + 16 * WM * WGM - 1) / (16 * WM * WGM)) * (a.N / (16 * WN * WGN));
     hipLaunchKernelGGL((gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ>), dim3((unsigned)tiles),
-                       dim3(64 * kDecodeWaves), xs_bytes > red ? xs_bytes : red, stream, a);
+                       dim3(64 * kDecodeWaves), xs_bytes, stream, a);
 }
 
 template <int WM, int SPW, bool RAW, bool FQ>
@@ -1225,9 +990,10 @@ static i32x4 host_buf_desc(const void* base, uint32_t bytes) {
     return i32x4{(int)(uint32_t)b, (int)((uint32_t)(b >> 32) & 0xFFFFu), (int)bytes, 0x00020000};
 }
 
-// AUTO takes the medium kernel where the 128 x 128 tiles would need split-K
-// to give every CU two workgroups, as long as its 64 x 64 tiles fit on the
-// CUs in one round (one workgroup per CU: its ring takes most of the LDS).
+// AUTO takes the medium (streaming) kernel where the 128 x 128 tiles would
+// need split-K to give every CU two workgroups, as long as its 64 x 64 tiles
+// fit on the CUs in one round (one workgroup per CU: its partial-sum exchange
+// takes most of the LDS).
 constexpr int kMediumTargetWGs = 512;
 static bool medium_preferred(int M, int N) {
     return (int64_t)((M + kTB - 1) / kTB) * (N / kTB) < kMediumTargetWGs &&
@@ -1279,10 +1045,8 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
         const int64_t t64 = (int64_t)((a.M + 63) / 64) * (a.N / 64);
         const int64_t t32 = (int64_t)((a.M + 31) / 32) * (a.N / 64);
         if (t32 > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
-        if (t64 >= kCUs)
-            hipLaunchKernelGGL((gemm_medium_kernel<2, RAW>), dim3((unsigned)t64), dim3(512), 0, stream, a);
-        else
-            hipLaunchKernelGGL((gemm_medium_kernel<1, RAW>), dim3((unsigned)t32), dim3(512), 0, stream, a);
+        if (t64 >= kCUs) launch_stream<4, 4, 1, 1, RAW, false>(a, 0, stream);
+        else launch_stream<2, 4, 1, 1, RAW, false>(a, 0, stream);
     } else if (variant == MQ_VARIANT_TILED_LARGE) {
         using TS = TileShape<8, 4>;
         const int64_t tiles = (int64_t)((a.M + TS::kTM - 1) / TS::kTM) * (a.N / TS::kTN);
@@ -1422,12 +1186,12 @@ extern "C" size_t mq_linear_workspace_size(int M, int N, int K) {
            align256((size_t)2 * M);
 }
 
-extern "C" mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
-                               const uint8_t* Wq, const void* s_w,
-                               const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
-                               const uint8_t* Rq, const void* s_r,
-                               void* Y, int ldy,
-                               void* workspace, size_t ws_bytes, hipStream_t stream) {
+static mq_status linear_impl(int M, int N, int K, const void* X, int ldx,
+                             const uint8_t* Wq, const void* s_w,
+                             const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                             const uint8_t* Rq, const void* s_r,
+                             void* Y, int ldy,
+                             void* workspace, size_t ws_bytes, hipStream_t stream) {
     mq_status st = check_common(M, N, K, static_cast<const uint8_t*>(X), Wq, res_rowptr, res_kb, nnzb, Rq);
     if (st != MQ_OK) return st;
     if (ldx < K || ldx % 8 != 0 || ldy < N || ldy % 8 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
@@ -1457,4 +1221,14 @@ extern "C" mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
     if (st != MQ_OK) return st;
     return mq_fused_gemm(M, N, K, Xq, sx, Wq, s_w, res_rowptr, res_kb, nnzb, Rq, s_r, Y, ldy,
                          gws > 0 ? ws : nullptr, gws, stream);
+}
+
+extern "C" mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
+                               const uint8_t* Wq, const void* s_w,
+                               const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                               const uint8_t* Rq, const void* s_r,
+                               void* Y, int ldy,
+                               void* workspace, size_t ws_bytes, hipStream_t stream) {
+    return linear_impl(M, N, K, X, ldx, Wq, s_w, res_rowptr, res_kb, nnzb, Rq, s_r, Y, ldy, workspace, ws_bytes,
+                       stream);
 }

@@ -150,3 +150,4 @@ def test_repack_validation(lib):
     assert ra(4, 256, A, 128, A + 8, None, None) == MISALIGNED
     assert ua(4, 256, A + 8, A, 128, None) == MISALIGNED
     assert ua(-1, 256, A, A, 128, None) == INVALID
+
