@@ -74,7 +74,9 @@ typedef enum mq_status {
                                       leading dimension too small / unaligned  */
     MQ_ERR_MISALIGNED = -3,        /* pointer alignment rule violated          */
     MQ_ERR_WORKSPACE = -4,         /* workspace smaller than required          */
-    MQ_ERR_HIP = -5                /* the HIP runtime reported a launch error  */
+    MQ_ERR_HIP = -5,               /* the HIP runtime reported a launch error  */
+    MQ_ERR_SCRATCH_LIMIT = -6      /* a scratch-free call needs more scratch than
+                                      the library holds (mq_scratch_bytes)      */
 } mq_status;
 
 /* Kernel family selection (testing and A/B timing).  AUTO picks by M. */
@@ -257,6 +259,28 @@ mq_status mq_repack_act(int M, int K, const uint8_t* Xq_c, int ldq, uint8_t* Xq,
  * canonical rows Xq_c [M, ldq]. */
 mq_status mq_unpack_act(int M, int K, const uint8_t* Xq, uint8_t* Xq_c, int ldq,
                         hipStream_t stream);
+
+/*
+ * mq_linear without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The workspace mq_linear would take (the
+ * quantised rows, their scales, split-K partial sums) lives in a file-scope
+ * device array of mq_scratch_bytes() bytes (128 MiB) that the library holds on
+ * every GPU it runs on until the process ends.  The call allocates nothing.
+ *   Same operands, results and checks as mq_linear.
+ *   Returns MQ_ERR_SCRATCH_LIMIT, launching nothing, when
+ *   mq_linear_workspace_size(M, N, K) > mq_scratch_bytes().
+ *   Calls on one GPU share its array: calls that overlap in time on one GPU
+ *   (other streams, other host threads) race and must be serialised by the
+ *   caller.  Each call writes every scratch byte it reads; nothing needs
+ *   clearing between calls.
+ */
+size_t mq_scratch_bytes(void);
+mq_status mq_linear_noalloc(int M, int N, int K, const void* X, int ldx,
+                            const uint8_t* Wq, const void* s_w,
+                            const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                            const uint8_t* Rq, const void* s_r,
+                            void* Y, int ldy, hipStream_t stream);
 
 /* ======================================================================== */
 /* Offline weight preparation (not on the timed path)                        */

@@ -45,6 +45,8 @@ _SIG = {
     "mq_unfused_workspace_size": (C.c_size_t, [_I, _I, _I]),
     "mq_unfused_gemm": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P,
                             C.c_size_t, _P]),
+    "mq_scratch_bytes": (C.c_size_t, []),
+    "mq_linear_noalloc": (_I, [_I, _I, _I, _P, _I, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P]),
     "mq_repack_weights": (_I, [_I, _I, _P, _P, _I, _P, _P, _P, _P, _P, _P]),
     "mq_unpack_weights": (_I, [_I, _I, _P, _P, _I, _P, _P, _P, _P, _P]),
     "mq_repack_act": (_I, [_I, _I, _P, _I, _P, _P, _P]),

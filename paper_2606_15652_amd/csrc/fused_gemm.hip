@@ -32,6 +32,7 @@
 
 #include <stddef.h>
 
+#include <mutex>
 #include <type_traits>
 
 namespace mq {
@@ -1231,4 +1232,49 @@ extern "C" mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
                                void* workspace, size_t ws_bytes, hipStream_t stream) {
     return linear_impl(M, N, K, X, ldx, Wq, s_w, res_rowptr, res_kb, nnzb, Rq, s_r, Y, ldy, workspace, ws_bytes,
                        stream);
+}
+
+// ---------------------------------------------------------------------------
+// Scratch-free whole layer: mq_linear's workspace (the quantised rows, their
+// scales and any split-K partial sums) in a file-scope device array instead
+// of caller memory, for callers that cannot allocate.  Every GPU the library
+// runs on holds its own copy until the process ends; calls on one GPU share
+// it.  Nothing in it needs clearing: each call writes every byte it reads.
+// ---------------------------------------------------------------------------
+constexpr size_t kScratchBytes = (size_t)128 << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mutex;
+static void* g_scratch_ptr[kMaxDevices];
+
+// this device's address of the scratch array (looked up once per device,
+// with the device current); nullptr on failure
+static void* device_scratch() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
+extern "C" size_t mq_scratch_bytes(void) { return kScratchBytes; }
+
+extern "C" mq_status mq_linear_noalloc(int M, int N, int K, const void* X, int ldx,
+                                       const uint8_t* Wq, const void* s_w,
+                                       const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                                       const uint8_t* Rq, const void* s_r,
+                                       void* Y, int ldy, hipStream_t stream) {
+    const size_t need = mq_linear_workspace_size(M, N, K);
+    if (need > kScratchBytes) return MQ_ERR_SCRATCH_LIMIT;
+    void* ws = nullptr;
+    if (need > 0) {
+        ws = device_scratch();
+        if (!ws) return MQ_ERR_HIP;
+    }
+    return linear_impl(M, N, K, X, ldx, Wq, s_w, res_rowptr, res_kb, nnzb, Rq, s_r, Y, ldy, ws, need, stream);
 }

@@ -9,6 +9,7 @@ extern "C" const char* mq_status_string(mq_status s) {
         case MQ_ERR_MISALIGNED: return "MQ_ERR_MISALIGNED: pointer alignment rule violated";
         case MQ_ERR_WORKSPACE: return "MQ_ERR_WORKSPACE: workspace too small";
         case MQ_ERR_HIP: return "MQ_ERR_HIP: the HIP runtime reported an error";
+        case MQ_ERR_SCRATCH_LIMIT: return "MQ_ERR_SCRATCH_LIMIT: the scratch-free call needs more than the library's 128 MiB scratch array";
     }
     return "MQ_ERR_UNKNOWN";
 }

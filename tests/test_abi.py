@@ -151,3 +151,10 @@ def test_repack_validation(lib):
     assert ua(4, 256, A + 8, A, 128, None) == MISALIGNED
     assert ua(-1, 256, A, A, 128, None) == INVALID
 
+
+def test_noalloc_validation(lib):
+    assert lib.mq_scratch_bytes() == 128 << 20
+    f = lib.mq_linear_noalloc
+    assert f(0, 256, 256, A, 256, A, A, A, A, 1, A, A, A, 256, None) == OK        # empty: no scratch used
+    assert f(4, 256, 200, A, 256, A, A, A, A, 1, A, A, A, 256, None) == SHAPE     # K not a multiple of 128
+    assert f(65536, 256, 8192, A, 8192, A, A, None, None, 0, None, None, A, 256, None) == -6   # beyond scratch
