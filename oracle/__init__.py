@@ -66,6 +66,10 @@ def lib() -> C.CDLL:
             "orc_linear": (i64, [i, i, i, P, P, P, P, P, P, i, P, P, P, P, P]),
             "orc_linear_sampled": (i64, [i, i, i, P, P, P, P, P, P, i, P, P,
                                          i64, P, P, P, P, P]),
+            "orc_quantize_act8": (None, [P, i, i, i, P, P]),
+            "orc_linear_a8": (i64, [i, i, i, P, P, P, P, P, P, i, P, P, P, P, P]),
+            "orc_linear_a8_sampled": (i64, [i, i, i, P, P, P, P, P, P, i, P, P,
+                                            i64, P, P, P, P, P]),
         }
         for name, (res, args) in sig.items():
             f = getattr(_lib, name)
@@ -375,6 +379,49 @@ def linear_sampled(Xq: np.ndarray, s_x: np.ndarray, pw: PackedWeight,
     ovf = lib().orc_linear_sampled(M, pw.N, pw.K, *[_p(a) for a in k[:6]], nnzb,
                                    _p(k[6]), _p(k[7]), cnt, _p(ms), _p(ns),
                                    _p(Tb), _p(Tr), _p(Y))
+    if ovf:
+        raise OverflowError(f"{ovf} accumulators exceed int32")
+    return Tb, Tr, Y
+
+
+# ---------------------------------------------------------- W4A8 layer ----
+def quantize_act8(X: np.ndarray):
+    """Per-token INT8 of fp16 X [M, K] (q_max = 127) -> (codes int8 [M, K], s_x bits [M])."""
+    X = np.ascontiguousarray(X, dtype=np.float16)
+    M, K = X.shape
+    q = np.empty((M, K), np.int8)
+    s_x = np.empty(M, np.uint16)
+    lib().orc_quantize_act8(_p(X.view(np.uint16)), M, K, K, _p(q), _p(s_x))
+    return q, s_x
+
+
+def linear_a8(Xq8: np.ndarray, s_x: np.ndarray, pw: PackedWeight):
+    """W4A8 layer from int8 activation codes -> (Tb int64, Tr int64, Y64 fp64) [M, N]."""
+    Xq8 = np.ascontiguousarray(Xq8, np.int8)
+    M, k, nnzb = _lin_args(np.zeros((Xq8.shape[0], 1), np.uint8), s_x, pw)
+    N, K = pw.N, pw.K
+    Tb = np.empty((M, N), np.int64)
+    Tr = np.empty((M, N), np.int64)
+    Y = np.empty((M, N), np.float64)
+    ovf = lib().orc_linear_a8(M, N, K, _p(Xq8), *[_p(a) for a in k[1:6]], nnzb, _p(k[6]), _p(k[7]),
+                              _p(Tb), _p(Tr), _p(Y))
+    if ovf:
+        raise OverflowError(f"{ovf} accumulators exceed int32")
+    return Tb, Tr, Y
+
+
+def linear_a8_sampled(Xq8: np.ndarray, s_x: np.ndarray, pw: PackedWeight,
+                      ms: np.ndarray, ns: np.ndarray):
+    Xq8 = np.ascontiguousarray(Xq8, np.int8)
+    M, k, nnzb = _lin_args(np.zeros((Xq8.shape[0], 1), np.uint8), s_x, pw)
+    ms = np.ascontiguousarray(ms, np.int32)
+    ns = np.ascontiguousarray(ns, np.int32)
+    cnt = ms.size
+    Tb = np.empty(cnt, np.int64)
+    Tr = np.empty(cnt, np.int64)
+    Y = np.empty(cnt, np.float64)
+    ovf = lib().orc_linear_a8_sampled(M, pw.N, pw.K, _p(Xq8), *[_p(a) for a in k[1:6]], nnzb,
+                                      _p(k[6]), _p(k[7]), cnt, _p(ms), _p(ns), _p(Tb), _p(Tr), _p(Y))
     if ovf:
         raise OverflowError(f"{ovf} accumulators exceed int32")
     return Tb, Tr, Y

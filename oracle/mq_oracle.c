@@ -28,6 +28,8 @@
  *   residual: 128x128 blocks aligned with the groups, one fp16 scale per row
  *   inside each selected block;
  *   top-K ties: lower linear block index (nb * KB + kb) wins;
+ *   W4A8 (appendix "Implementation Details": per-token dynamic activation
+ *   quantisation): the same quantiser with q_max = 127, codes in [-127, 127];
  *   packed layout (the paper fixes no bit layout; its Section 4.2 fuses the
  *   layout packing with quantisation): 4 bits per code in 8-byte chunks of
  *   16 codes, sign-magnitude, folded as described at pack_chunk() below.
@@ -101,28 +103,35 @@ void orc_f16_to_f32_array(const uint16_t* h, float* x, int64_t n)
 }
 
 /* ------------------------------------------------------------------------ */
-/* Eq. (1): symmetric 4-bit quantisation of one vector.                      */
+/* Eq. (1): symmetric b-bit quantisation of one vector, q_max = 2^(b-1) - 1. */
 /* ------------------------------------------------------------------------ */
 
-/* Quantise v[0..n) (stride 1).  Writes the fp16 scale bits and the codes. */
-static void quant_sym4(const float* v, int n, uint16_t* s_bits, int8_t* q)
+/* Quantise v[0..n) (stride 1) with q_max = qmax.  Writes the fp16 scale bits
+ * and the codes. */
+static void quant_sym(const float* v, int n, int qmax, uint16_t* s_bits, int8_t* q)
 {
     float amax = 0.0f;
     for (int i = 0; i < n; ++i) {
         float a = fabsf(v[i]);
         if (a > amax) amax = a;
     }
-    float ratio = amax / (float)ORC_QMAX;     /* fp32, correctly rounded */
+    float ratio = amax / (float)qmax;         /* fp32, correctly rounded */
     uint16_t sb = orc_f32_to_f16(ratio);
     float s = orc_f16_to_f32(sb);
     *s_bits = sb;
     for (int i = 0; i < n; ++i) {
         if (s == 0.0f) { q[i] = 0; continue; }
         float r = rintf(v[i] / s);            /* fp32 quotient, ties to even */
-        if (r > ORC_QMAX) r = ORC_QMAX;
-        if (r < -ORC_QMAX) r = -ORC_QMAX;
+        if (r > qmax) r = (float)qmax;
+        if (r < -qmax) r = (float)-qmax;
         q[i] = (int8_t)r;
     }
+}
+
+/* the 4-bit quantiser of the method (q_max = 7) */
+static void quant_sym4(const float* v, int n, uint16_t* s_bits, int8_t* q)
+{
+    quant_sym(v, n, ORC_QMAX, s_bits, q);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -265,6 +274,22 @@ void orc_quantize_act(const uint16_t* X, int M, int K, int ldx,
         pack_row(q, K, Xq + (int64_t)m * (K / 2));
         free(v);
         free(q);
+    }
+}
+
+/* Per-token symmetric INT8 activation quantisation (the W4A8 setting of the
+ * appendix "Implementation Details": per-token dynamic activation
+ * quantisation; Eq. (1) with q_max = 127, -128 never produced).  Codes are
+ * plain int8 [M, K] row-major. */
+void orc_quantize_act8(const uint16_t* X, int M, int K, int ldx,
+                       int8_t* Xq8, uint16_t* s_x)
+{
+    #pragma omp parallel for schedule(static)
+    for (int m = 0; m < M; ++m) {
+        float* v = (float*)malloc(sizeof(float) * (size_t)K);
+        for (int k = 0; k < K; ++k) v[k] = orc_f16_to_f32(X[(int64_t)m * ldx + k]);
+        quant_sym(v, K, 127, &s_x[m], Xq8 + (int64_t)m * K);
+        free(v);
     }
 }
 
@@ -566,6 +591,70 @@ int64_t orc_linear_sampled(int M, int N, int K,
         if (Tr) Tr[i] = tr;
         if (Y64) Y64[i] = y;
         free(xrow);
+        free(wrow);
+    }
+    layer_free(&L);
+    return overflow;
+}
+
+/* W4A8 layer: as orc_linear, with the activations given as int8 codes
+ * [M, K] (orc_quantize_act8) instead of packed 4-bit rows.  The group sums
+ * and the epilogue are those of Eq. (4) and Eq. (2) unchanged. */
+int64_t orc_linear_a8(int M, int N, int K,
+                      const int8_t* Xq8, const uint16_t* s_x,
+                      const uint8_t* Wq, const uint16_t* s_w,
+                      const int32_t* rowptr, const int32_t* kb_idx, int nnzb,
+                      const uint8_t* Rq, const uint16_t* s_r,
+                      int64_t* Tb, int64_t* Tr, double* Y64)
+{
+    orc_layer L;
+    layer_init(&L, M, N, K, NULL, s_x, Wq, s_w, nnzb > 0 ? rowptr : NULL, kb_idx, Rq, s_r);
+    int8_t* wun = (int8_t*)malloc((size_t)N * K);
+    #pragma omp parallel for schedule(static)
+    for (int n = 0; n < N; ++n) unpack_row(Wq + (int64_t)n * (K / 2), K, wun + (int64_t)n * K);
+    int64_t overflow = 0;
+    #pragma omp parallel for schedule(dynamic, 1) reduction(+ : overflow)
+    for (int m = 0; m < M; ++m) {
+        const int8_t* xrow = Xq8 + (int64_t)m * K;
+        for (int n = 0; n < N; ++n) {
+            int64_t tb, tr;
+            double y;
+            layer_elem(&L, xrow, wun + (int64_t)n * K, m, n, &tb, &tr, &y);
+            if (tb > INT32_MAX || tb < INT32_MIN || tr > INT32_MAX || tr < INT32_MIN) ++overflow;
+            int64_t o = (int64_t)m * N + n;
+            if (Tb) Tb[o] = tb;
+            if (Tr) Tr[o] = tr;
+            if (Y64) Y64[o] = y;
+        }
+    }
+    free(wun);
+    layer_free(&L);
+    return overflow;
+}
+
+/* Selected outputs of the W4A8 layer: (ms[i], ns[i]) for i < count. */
+int64_t orc_linear_a8_sampled(int M, int N, int K,
+                              const int8_t* Xq8, const uint16_t* s_x,
+                              const uint8_t* Wq, const uint16_t* s_w,
+                              const int32_t* rowptr, const int32_t* kb_idx, int nnzb,
+                              const uint8_t* Rq, const uint16_t* s_r,
+                              int64_t count, const int32_t* ms, const int32_t* ns,
+                              int64_t* Tb, int64_t* Tr, double* Y64)
+{
+    orc_layer L;
+    layer_init(&L, M, N, K, NULL, s_x, Wq, s_w, nnzb > 0 ? rowptr : NULL, kb_idx, Rq, s_r);
+    int64_t overflow = 0;
+    #pragma omp parallel for schedule(dynamic, 16) reduction(+ : overflow)
+    for (int64_t i = 0; i < count; ++i) {
+        int8_t* wrow = (int8_t*)malloc((size_t)K);
+        unpack_row(Wq + (int64_t)ns[i] * (K / 2), K, wrow);
+        int64_t tb, tr;
+        double y;
+        layer_elem(&L, Xq8 + (int64_t)ms[i] * K, wrow, ms[i], ns[i], &tb, &tr, &y);
+        if (tb > INT32_MAX || tb < INT32_MIN || tr > INT32_MAX || tr < INT32_MIN) ++overflow;
+        if (Tb) Tb[i] = tb;
+        if (Tr) Tr[i] = tr;
+        if (Y64) Y64[i] = y;
         free(wrow);
     }
     layer_free(&L);

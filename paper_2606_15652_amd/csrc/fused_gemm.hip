@@ -647,12 +647,15 @@ constexpr int kFusedMaxM = 4, kFusedCPT = 4;
 constexpr int kDecodeWaves = 8;
 constexpr uint32_t kPastEnd = 0x80000000u;   // buffer offset past every operand (< 2 GB): reads zero
 
-// Items in flight per wave: about 96 registers of stages (a stage holds WM X
-// fragments, WN B fragments and WN scales).
-template <int WM, int WN>
+// Items in flight per wave: stages of WM X fragments, WN B fragments and WN
+// scales filling about 96 registers for the decode tiles (which keep two
+// workgroups per CU) and 144 for the medium tiles (one workgroup per CU;
+// 72 in raw mode, whose two integer accumulators take the rest).
+template <int WM, int WN, bool RAW>
 struct StreamDepth {
     static constexpr int kStageRegs = 4 * WM + 4 * WN + WN;
-    static constexpr int GD = 96 / kStageRegs < 2 ? 2 : 96 / kStageRegs > 6 ? 6 : 96 / kStageRegs;
+    static constexpr int kBudget = (WM >= 2 && WN == 4) ? (RAW ? 72 : 144) : 96;
+    static constexpr int GD = kBudget / kStageRegs < 2 ? 2 : kBudget / kStageRegs > 6 ? 6 : kBudget / kStageRegs;
 };
 
 // The streaming kernel: eight waves = KS = 8 / (WGM WGN) splits of the K
@@ -670,7 +673,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     static_assert(KS * WG2 == NW, "eight waves");
     constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
     constexpr int SPW = WN;
-    constexpr int GD = StreamDepth<WM, WN>::GD;
+    constexpr int GD = StreamDepth<WM, WN, RAW>::GD;
     constexpr int kAcc = WM * SPW * 4;                           // sums per lane and accumulator
     // cross-wave partial sums red[wave][value][lane] (one accumulator per
     // round: raw mode adds the base and then the residual sums); FQ: packed

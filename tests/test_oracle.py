@@ -714,3 +714,80 @@ def test_hessian_constant_against_exact_distortion(orc):
         assert surrogate == pytest.approx(exact, rel=1e-12)
         gain = 2.0 / T * np.linalg.norm(Xd @ R.astype(np.float64).T) ** 2 - exact
         assert gain == pytest.approx(sum(S.ravel()[b] for b in sel), rel=1e-9, abs=1e-15)
+
+
+# ------------------------------------------------------------ W4A8 layer --
+def test_quant8_golden_ties(orc):
+    """Hand-worked INT8 codes (q_max = 127, round half to even)."""
+    for case in _read_pairs("quant8_ties.txt", "q"):
+        x = np.array([float(v) for v in case["x"]], np.float16)
+        want = [int(v) for v in case["q"]]
+        X = np.zeros((1, 128), np.float16)
+        X[0, :len(x)] = x
+        q, s = orc.quantize_act8(X)
+        assert q[0, :len(x)].tolist() == want
+        assert not q[0, len(x):].any()
+
+
+def test_quant8_exact_rational(orc):
+    """Every INT8 code equals round-half-even of the exact quotient x / s by the
+    stored fp16 scale (Python Fraction), with s = fp16(fp32(max|x|) / 127)."""
+    rng = np.random.default_rng(12)
+    X = (rng.standard_normal((6, 256)) * rng.uniform(0.01, 50, (6, 1))).astype(np.float16)
+    X[1, :7] = [0.5, 1.5, 2.5, 3.5, -0.5, -1.5, -2.5]
+    X[1, 7] = 127
+    X[2] = 0
+    q, s = orc.quantize_act8(X)
+    for m in range(X.shape[0]):
+        amax = float(np.abs(X[m].astype(np.float32)).max())
+        sf = float(np.float16(np.float32(amax) / np.float32(127)))
+        assert f16(s[m]) == sf
+        for k in range(X.shape[1]):
+            want = 0 if sf == 0 else max(-127, min(127, exact_round_half_even(
+                Fraction(float(X[m, k])) / Fraction(sf))))
+            assert q[m, k] == want, (m, k, float(X[m, k]), sf)
+
+
+def test_linear_a8_vs_bruteforce(orc):
+    """W4A8 layer: int64 sums and the fp64 epilogue against a numpy product of
+    the dequantised operands."""
+    W = synth.gen_weight(256, 384, 8)
+    pw = orc.prepare_weight(W, 3)
+    X = synth.gen_act(9, 384, 8)
+    q, s = orc.quantize_act8(X)
+    Tb, Tr, Y = orc.linear_a8(q, s, pw)
+    xc = q.astype(np.int64)
+    wc = orc.unpack_codes(pw.Wq, 384).astype(np.int64)
+    rcodes, rdeq = dense_residual(pw, orc)
+    assert np.array_equal(Tb, xc @ wc.T)
+    assert np.array_equal(Tr, xc @ rcodes.T)
+    Yref = (xc * f16(s)[:, None]) @ (dequant_base(pw, orc) + rdeq).T
+    assert np.abs(Y - Yref).max() <= 1e-12 * np.abs(Yref).max()
+    assert np.abs(q).max() == 127
+
+
+def test_linear_a8_reduces_to_a4_on_4bit_codes(orc):
+    """With activation codes inside [-7, 7], the W4A8 layer computes exactly
+    what the W4A4 layer computes on the same codes (packed 4-bit)."""
+    W = synth.gen_weight(256, 512, 21)
+    pw = orc.prepare_weight(W, 4)
+    rng = np.random.default_rng(2)
+    codes = rng.integers(-7, 8, (5, 512)).astype(np.int8)
+    s = np.full(5, np.float16(0.25).view(np.uint16))
+    a8 = orc.linear_a8(codes, s, pw)
+    a4 = orc.linear(orc.pack_codes(codes), s, pw)
+    for u, v in zip(a8, a4):
+        assert np.array_equal(u, v)
+
+
+def test_linear_a8_int32_range(orc):
+    """+-127 x +-7 over K = 28672 stays inside int32 (|T| = 889 K)."""
+    K, N = 28672, 128
+    codes = np.full((2, K), 127, np.int8)
+    codes[1] = -127
+    wc = np.full((N, K), -7, np.int8)
+    pw = orc.PackedWeight(N, K, orc.pack_codes(wc), np.full((N, K // B), 0x3c00, np.uint16),
+                          np.zeros(N // B + 1, np.int32), np.zeros(0, np.int32),
+                          np.zeros((0, B, B // 2), np.uint8), np.zeros((0, B), np.uint16), None, None)
+    Tb, _, _ = orc.linear_a8(codes, np.full(2, 0x3c00, np.uint16), pw)
+    assert Tb[0, 0] == -889 * K and Tb[1, 0] == 889 * K
