@@ -76,6 +76,10 @@ def parse():
                     help="time the fused GEMM and the whole layer call on every layer of the other "
                          "workload families (one JSON line per layer and M; not the headline line)")
     ap.add_argument("--only", metavar="LAYERS", help="--families: comma-separated layer names (default: all)")
+    ap.add_argument("--table5", action="store_true",
+                    help="--families: the Qwen3-8B concatenated-output operators (qkv, o, gate_up, down) "
+                         "at decode and prefill batch sizes instead of the workload families")
+    ap.add_argument("--max-m", type=int, default=None, help="--families: skip token counts above this")
     ap.add_argument("--unfused", action="store_true",
                     help="--families: also time the three-kernel baseline (dense GEMM, residual GEMM, "
                          "reduce-add) and the dense-only GEMM on the same operands")
@@ -331,7 +335,7 @@ def families(args):
     dev = torch.device("cuda:0")
     wcache = {}
     only = set(args.only.split(",")) if args.only else None
-    for layer in synth.workloads():
+    for layer in (synth.table5_workloads() if args.table5 else synth.workloads()):
         if (only is None and layer.name == "c2_4096") or (only is not None and layer.name not in only):
             continue
         K, N, nnzb = layer.K, layer.N, layer.nnzb
@@ -363,6 +367,8 @@ def families(args):
             return wbs[rb[0]]
 
         for m in layer.ms:
+            if args.max_m is not None and m > args.max_m:
+                continue
             X = torch.from_numpy(layer.act(m)).to(dev)
             Xq = torch.empty((m, K // 2), dtype=torch.uint8, device=dev)
             sx = torch.empty((m,), dtype=torch.float16, device=dev)
@@ -515,7 +521,14 @@ def main():
         t_call = timed(torch, lambda: mq.linear(Xs[m], next_pw(), out=Ys[m], workspace=Ws[m]), args.reps)
         t_q = timed(torch, lambda: mq.quantize_act(Xs[m], out=(Xqs[m], sxs[m])), args.reps)
         t_gemm = timed(torch, lambda: mq.fused_gemm(Xqs[m], sxs[m], next_pw(), out=Ys[m]), args.reps)
+        # the W4A8 variant (INT8 activations) on the same layer
+        xq8 = torch.empty((m, 3 * K // 2), dtype=torch.uint8, device=dev)
+        sx8 = torch.empty((m,), dtype=torch.float16, device=dev)
+        t_q8 = timed(torch, lambda: mq.quantize_act8(Xs[m], out=(xq8, sx8)), args.reps)
+        t_g8 = timed(torch, lambda: mq.fused_gemm_a8(xq8, sx8, next_pw(), out=Ys[m]), args.reps)
+        del xq8, sx8
         row = {"M": m, "us_call": round(t_call, 3), "us_gemm": round(t_gemm, 3), "us_quant": round(t_q, 3),
+               "us_gemm_w4a8": round(t_g8, 3), "us_quant_w4a8": round(t_q8, 3),
                "eff_tops": round(2.0 * m * N * K / (t_gemm * 1e-6) / 1e12, 2),
                "int8_peak_frac": round(ops / (t_gemm * 1e-6) / 1e12 / PEAK_I8_TOPS, 4),
                "hbm_frac": round(byts / (t_gemm * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),

@@ -193,6 +193,60 @@ mq_status mq_linear(int M, int N, int K, const void* X, int ldx,
                     void* Y, int ldy,
                     void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* ======================================================================== */
+/* W4A8 variant (per-token INT8 activations)                                 */
+/* ======================================================================== */
+
+/*
+ * Per-token symmetric INT8 activation quantisation (the W4A8 setting of the
+ * paper's appendix "Implementation Details": per-token dynamic activation
+ * quantisation; Eq. (1) with q_max = 127):
+ *     s_x[m] = fp16_rn(fp32(max_k |X[m,k]|) / 127),
+ *     x = clamp(round_half_even(X[m,k] / s_x[m]), -127, 127)   (0 if s == 0)
+ *   X   : fp16 [M, ldx], as for mq_quantize_act.
+ *   Xq8 : out, uint8 [M * K * 3 / 2] in the library's A8 layout: each code as
+ *         x = 8 h + l, h = floor(x / 8) in [-16, 15], l in [0, 7]; bytes
+ *         [0, M K): the fp8 e4m3 byte of h, piece (row m, group g) of 128
+ *         bytes at (g M + m) 128, its 16-code chunk c (codes 16c .. 16c+15 of
+ *         the group, in k order) at byte 32 (c mod 4) + 16 (c div 4) of the
+ *         piece (the operand order of the matrix instruction); [M K, 3 M K / 2):
+ *         the codes l as 4-bit codes in the W4A4 layout (folded chunks,
+ *         group order).  16-byte aligned.
+ *   s_x : out, fp16 [M].
+ */
+mq_status mq_quantize_act8(const void* X, int M, int K, int ldx,
+                           uint8_t* Xq8, void* s_x, hipStream_t stream);
+
+/*
+ * W4A8 layer: as mq_fused_gemm (same weights, residual blocks, epilogue of
+ * Section 3 Eq. (4) and Eq. (2)) with INT8 activation codes Xq8 (layout of
+ * mq_quantize_act8).  Exact integer group sums (|sum| <= 127 * 7 * 128).
+ * Every M runs on the streaming kernels (no workspace).
+ */
+mq_status mq_fused_gemm_a8(int M, int N, int K,
+                           const uint8_t* Xq8, const void* s_x,
+                           const uint8_t* Wq, const void* s_w,
+                           const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                           const uint8_t* Rq, const void* s_r,
+                           void* Y, int ldy, hipStream_t stream);
+
+/* Raw integer sums of the W4A8 layer (testing): Tb, Tr int32 [M, N];
+ * |Tb|, |Tr| <= 889 K < 2^31. */
+mq_status mq_fused_gemm_a8_acc_i32(int M, int N, int K,
+                                   const uint8_t* Xq8,
+                                   const uint8_t* Wq,
+                                   const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                                   const uint8_t* Rq,
+                                   int32_t* Tb, int32_t* Tr, hipStream_t stream);
+
+/* INT8 codes: canonical int8 rows Xc [M, ldq] (ldq >= K, ldq % 16 == 0,
+ * 16-byte aligned) <-> the A8 layout.  -128 (outside the method's range) is
+ * stored as -127 and counted into the optional device counter n_invalid. */
+mq_status mq_repack_act8(int M, int K, const int8_t* Xc, int ldq, uint8_t* Xq8,
+                         int32_t* n_invalid, hipStream_t stream);
+mq_status mq_unpack_act8(int M, int K, const uint8_t* Xq8, int8_t* Xc, int ldq,
+                         hipStream_t stream);
+
 /*
  * Comparison baseline: the unfused pipeline the fused kernel replaces
  * (Section 4.2 "Kernel Fusion", Fig. 3; Appendix "Kernel Profile"), three

@@ -45,6 +45,11 @@ _SIG = {
     "mq_unfused_workspace_size": (C.c_size_t, [_I, _I, _I]),
     "mq_unfused_gemm": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P,
                             C.c_size_t, _P]),
+    "mq_quantize_act8": (_I, [_P, _I, _I, _I, _P, _P, _P]),
+    "mq_fused_gemm_a8": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P]),
+    "mq_fused_gemm_a8_acc_i32": (_I, [_I, _I, _I, _P, _P, _P, _P, _I, _P, _P, _P, _P]),
+    "mq_repack_act8": (_I, [_I, _I, _P, _I, _P, _P, _P]),
+    "mq_unpack_act8": (_I, [_I, _I, _P, _P, _I, _P]),
     "mq_scratch_bytes": (C.c_size_t, []),
     "mq_linear_noalloc": (_I, [_I, _I, _I, _P, _I, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P]),
     "mq_repack_weights": (_I, [_I, _I, _P, _P, _I, _P, _P, _P, _P, _P, _P]),
@@ -245,6 +250,78 @@ def fused_gemm_acc_i32(Xq, pw: PackedWeight, variant: str = "auto", stream=None)
         VARIANTS[variant], M, pw.N, pw.K, _ptr(Xq), _ptr(pw.Wq), rp, kb, pw.nnzb, rq,
         _ptr(Tb), _ptr(Tr), _stream(stream)))
     return Tb, Tr
+
+
+# ------------------------------------------------------- W4A8 variant --
+def quantize_act8(X, out=None, stream=None):
+    """Per-token INT8 quantisation of fp16 X [M, K] -> (Xq8 uint8 [M, 3K/2] in
+    the A8 layout, s_x fp16 [M])."""
+    torch = _torch()
+    _need(X, torch.float16, "X", 2)
+    M, K = X.shape
+    if out is None:
+        Xq8 = torch.empty((M, 3 * K // 2), dtype=torch.uint8, device=X.device)
+        s_x = torch.empty((M,), dtype=torch.float16, device=X.device)
+    else:
+        Xq8, s_x = out
+        _need_out(Xq8, (M, 3 * K // 2), torch.uint8, "out[0] (Xq8)")
+        _need_out(s_x, (M,), torch.float16, "out[1] (s_x)")
+    _check("mq_quantize_act8", load().mq_quantize_act8(_ptr(X), M, K, X.stride(0), _ptr(Xq8),
+                                                       _ptr(s_x), _stream(stream)))
+    return Xq8, s_x
+
+
+def fused_gemm_a8(Xq8, s_x, pw: PackedWeight, out=None, stream=None):
+    """W4A8 layer: Y fp16 [M, N] from INT8 activation codes (A8 layout)."""
+    torch = _torch()
+    _need(Xq8, torch.uint8, "Xq8", 2)
+    _need(s_x, torch.float16, "s_x", 1)
+    M = Xq8.shape[0]
+    if Xq8.shape[1] * 2 != 3 * pw.K or s_x.shape[0] != M:
+        raise ValueError("Xq8 / s_x shapes do not match the weight")
+    Y = out if out is not None else torch.empty((M, pw.N), dtype=torch.float16, device=Xq8.device)
+    if out is not None:
+        _need_out(Y, (M, pw.N), torch.float16, "out")
+    rp, kb, rq, sr = _res_ptrs(pw)
+    _check("mq_fused_gemm_a8", load().mq_fused_gemm_a8(
+        M, pw.N, pw.K, _ptr(Xq8), _ptr(s_x), _ptr(pw.Wq), _ptr(pw.s_w), rp, kb, pw.nnzb, rq, sr,
+        _ptr(Y), Y.stride(0), _stream(stream)))
+    return Y
+
+
+def fused_gemm_a8_acc_i32(Xq8, pw: PackedWeight, stream=None):
+    torch = _torch()
+    _need(Xq8, torch.uint8, "Xq8", 2)
+    M = Xq8.shape[0]
+    Tb = torch.empty((M, pw.N), dtype=torch.int32, device=Xq8.device)
+    Tr = torch.empty((M, pw.N), dtype=torch.int32, device=Xq8.device)
+    rp, kb, rq, _ = _res_ptrs(pw)
+    _check("mq_fused_gemm_a8_acc_i32", load().mq_fused_gemm_a8_acc_i32(
+        M, pw.N, pw.K, _ptr(Xq8), _ptr(pw.Wq), rp, kb, pw.nnzb, rq, _ptr(Tb), _ptr(Tr), _stream(stream)))
+    return Tb, Tr
+
+
+def unpack_act8(Xq8, stream=None):
+    """A8 layout -> canonical int8 codes [M, K]."""
+    torch = _torch()
+    _need(Xq8, torch.uint8, "Xq8", 2)
+    M, K = Xq8.shape[0], Xq8.shape[1] * 2 // 3
+    Xc = torch.empty((M, K), dtype=torch.int8, device=Xq8.device)
+    _check("mq_unpack_act8", load().mq_unpack_act8(M, K, _ptr(Xq8), _ptr(Xc), K, _stream(stream)))
+    return Xc
+
+
+def repack_act8(Xc, n_invalid=None, stream=None):
+    """Canonical int8 codes [M, K] -> A8 layout."""
+    torch = _torch()
+    _need(Xc, torch.int8, "Xc", 2)
+    M, K = Xc.shape
+    Xq8 = torch.empty((M, 3 * K // 2), dtype=torch.uint8, device=Xc.device)
+    if n_invalid is not None:
+        _need(n_invalid, torch.int32, "n_invalid", 1)
+    _check("mq_repack_act8", load().mq_repack_act8(M, K, _ptr(Xc), Xc.stride(0), _ptr(Xq8),
+                                                   _ptr(n_invalid), _stream(stream)))
+    return Xq8
 
 
 def linear_workspace_bytes(M: int, N: int, K: int) -> int:

@@ -648,13 +648,12 @@ constexpr int kDecodeWaves = 8;
 constexpr uint32_t kPastEnd = 0x80000000u;   // buffer offset past every operand (< 2 GB): reads zero
 
 // Items in flight per wave: stages of WM X fragments, WN B fragments and WN
-// scales filling about 96 registers for the decode tiles (which keep two
-// workgroups per CU) and 144 for the medium tiles (one workgroup per CU;
-// 72 in raw mode, whose two integer accumulators take the rest).
-template <int WM, int WN, bool RAW>
+// scales filling about 96 registers (measured: a deeper ring of the 64 x 64
+// medium tile, 144 registers, ran slower).
+template <int WM, int WN, bool RAW, bool A8 = false>
 struct StreamDepth {
-    static constexpr int kStageRegs = 4 * WM + 4 * WN + WN;
-    static constexpr int kBudget = (WM >= 2 && WN == 4) ? (RAW ? 72 : 144) : 96;
+    static constexpr int kStageRegs = (A8 ? 12 : 4) * WM + 4 * WN + WN;
+    static constexpr int kBudget = 96;
     static constexpr int GD = kBudget / kStageRegs < 2 ? 2 : kBudget / kStageRegs > 6 ? 6 : kBudget / kStageRegs;
 };
 
@@ -663,17 +662,22 @@ struct StreamDepth {
 // a (16 WM WGM) x (16 WN WGN) output tile.  Decode: WM <= 2, WN = 1, 2 or 4
 // (all M <= 32 rows, K over eight waves); medium M: WM = 2 or 4, WN = 4 (the
 // whole 32 x 64 or 64 x 64 tile per wave, K over eight waves).
-template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ>
+// A8 (the W4A8 variant): the activation operand is INT8, stored as an e4m3
+// high plane and a folded 4-bit low plane (mq_quantize_act8); each product
+// takes the low-plane MFMA and the fp8 x fp6 MFMA of the high plane chained
+// on its result (both exact), the rest is unchanged.
+template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false>
 __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs a) {
     static_assert(WN * WGN == 1 || WN * WGN == 2 || WN * WGN == 4 || WN * WGN == 8,
                   "tile columns inside one block row");
     static_assert(!(FQ && RAW), "fused quantisation feeds the fp16 path");
     static_assert(!FQ || (WGM == 1 && WGN == 1), "fused quantisation: one tile of all rows");
+    static_assert(!(FQ && A8), "fused quantisation is the W4A4 decode path");
     constexpr int NW = kDecodeWaves, WG2 = WGM * WGN, KS = NW / WG2;
     static_assert(KS * WG2 == NW, "eight waves");
     constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
     constexpr int SPW = WN;
-    constexpr int GD = StreamDepth<WM, WN, RAW>::GD;
+    constexpr int GD = StreamDepth<WM, WN, RAW, A8>::GD;
     constexpr int kAcc = WM * SPW * 4;                           // sums per lane and accumulator
     // cross-wave partial sums red[wave][value][lane] (one accumulator per
     // round: raw mode adds the base and then the residual sums); FQ: packed
@@ -758,10 +762,13 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     // residual blocks continue the pipeline without a bubble.
     struct Stage {
         uint4 x[WM], b[SPW];
+        uint4 xh[A8 ? WM : 1][2];                        // A8: the e4m3 high plane (32 bytes)
         uint16_t sc[SPW];
         int g;
         bool res;
     };
+    // A8: the low plane follows the M K bytes of the high plane
+    const uint32_t lo_base = A8 ? (uint32_t)M * (uint32_t)K : 0u;
     const int nitems = ng + ne;
     // group of the next residual entry to issue (scalar, loaded one entry ahead)
     int kb_next = (ne > 0) ? (int)res_kb[pb] : 0;
@@ -782,7 +789,15 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         S.res = res;
         if constexpr (!FQ) {
 #pragma unroll
-            for (int i = 0; i < WM; ++i) S.x[i] = bload16(rx, x_offset(g, i) | dead, 0);
+            for (int i = 0; i < WM; ++i) S.x[i] = bload16(rx, (lo_base + x_offset(g, i)) | dead, 0);
+        }
+        if constexpr (A8) {
+#pragma unroll
+            for (int i = 0; i < WM; ++i) {
+                const uint32_t ho = ((uint32_t)g * (uint32_t)M + (uint32_t)(mw + 16 * i + lrow)) * 128u + (uint32_t)lq * 32u;
+                S.xh[i][0] = bload16(rx, ho | dead, 0);
+                S.xh[i][1] = bload16(rx, (ho + 16u) | dead, 0);
+            }
         }
         // resources built from the selected base (a select of scalars, not of
         // two descriptors, which the compiler would turn into branches)
@@ -805,16 +820,23 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     };
     auto compute_item = [&](const Stage& S, auto res_c) {
         constexpr bool RES = decltype(res_c)::value;
-        i32x8 av[WM];
+        i32x8 av[WM], ah[A8 ? WM : 1];
 #pragma unroll
         for (int i = 0; i < WM; ++i) av[i] = unfold_codes(FQ ? x_lds(S.g, i) : S.x[i]);
+        if constexpr (A8) {
+#pragma unroll
+            for (int i = 0; i < WM; ++i)
+                ah[i] = i32x8{(int)S.xh[i][0].x, (int)S.xh[i][0].y, (int)S.xh[i][0].z, (int)S.xh[i][0].w,
+                              (int)S.xh[i][1].x, (int)S.xh[i][1].y, (int)S.xh[i][1].z, (int)S.xh[i][1].w};
+        }
 #pragma unroll
         for (int s = 0; s < SPW; ++s) {
             const i32x8 bv = unfold_codes(S.b[s]);
             const float sc = RAW ? 0.f : half_bits_to_float(S.sc[s]) * kCodeScale;
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
-                const f32x4 t = mfma_codes(av[i], bv, f32x4{0.f, 0.f, 0.f, 0.f});
+                f32x4 t = mfma_codes(av[i], bv, f32x4{0.f, 0.f, 0.f, 0.f});
+                if constexpr (A8) t = mfma_e4m3_codes(ah[i], bv, t);   // + the high plane: exact
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     if constexpr (!RAW) acc[i][s][r] = __builtin_fmaf(sc, t[r], acc[i][s][r]);
@@ -948,21 +970,22 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
 constexpr int kSkinnyMaxM = 32;
 constexpr int kSkinnyAutoM = 32;   // AUTO picks the skinny kernel up to this M
 
-// Strips per decode workgroup: the most that still give every CU a
+// Strips per decode workgroup: two when that still gives every CU a
 // workgroup (a workgroup's adjacent strips share DRAM pages and the block
-// row's CSR entries); two at most for 17 to 32 rows (register and LDS budget).
+// row's CSR entries), else one.  (Four measured no faster than two on the
+// 5120 -> 25600 layer at one token, slightly slower.)
 constexpr int kCUs = 256;
 static int decode_spw(int M, int N) {
     const int S = N / 16;
-    if (M <= 16 && S / 4 >= kCUs) return 4;
+    (void)M;
     if (S / 2 >= kCUs) return 2;
     return 1;
 }
 
-template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ>
+template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false>
 static void launch_stream(const GemmArgs& a, size_t xs_bytes, hipStream_t stream) {
     const int64_t tiles = (int64_t)((a.M + 16 * WM * WGM - 1) / (16 * WM * WGM)) * (a.N / (16 * WN * WGN));
-    hipLaunchKernelGGL((gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ>), dim3((unsigned)tiles),
+    hipLaunchKernelGGL((gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ, A8>), dim3((unsigned)tiles),
                        dim3(64 * kDecodeWaves), xs_bytes, stream, a);
 }
 
@@ -974,9 +997,6 @@ static void launch_decode_spw(const GemmArgs& a, size_t xs_bytes, hipStream_t st
 // xs_bytes: LDS for the quantised rows (fused quantisation), 0 otherwise
 template <int WM, bool RAW, bool FQ>
 static void launch_decode(const GemmArgs& a, int spw, size_t xs_bytes, hipStream_t stream) {
-    if constexpr (WM == 1) {
-        if (spw == 4) return launch_decode_spw<WM, 4, RAW, FQ>(a, xs_bytes, stream);
-    }
     if (spw >= 2) return launch_decode_spw<WM, 2, RAW, FQ>(a, xs_bytes, stream);
     launch_decode_spw<WM, 1, RAW, FQ>(a, xs_bytes, stream);
 }
@@ -1008,9 +1028,10 @@ static bool medium_preferred(int M, int N) {
 // Whole-operand resources take 32-bit offsets (and offsets from 2 GB up serve
 // as "past the end"), so every operand must stay below 2 GB.
 template <bool RAW>
-static mq_status operand_resources(GemmArgs& a) {
+static mq_status operand_resources(GemmArgs& a, bool a8 = false) {
     const uint64_t G = (uint64_t)(a.K / kGroup);
-    const uint64_t sizes[5] = {G * a.M * kGroupBytes, G * a.N * kGroupBytes, (uint64_t)a.nnzb * kTB * kGroupBytes,
+    const uint64_t sizes[5] = {G * a.M * kGroupBytes * (a8 ? 3 : 1), G * a.N * kGroupBytes,
+                               (uint64_t)a.nnzb * kTB * kGroupBytes,
                                G * a.N * 2, (uint64_t)a.nnzb * kTB * 2};
     for (uint64_t b : sizes)
         if (b >= (1ull << 31)) return MQ_ERR_UNSUPPORTED_SHAPE;
@@ -1172,6 +1193,70 @@ extern "C" mq_status mq_fused_gemm_acc_i32(mq_variant variant, int M, int N, int
                nullptr, nullptr, 0, Tb, Tr};
     a.nnzb = nnzb;
     return launch<true>(variant, a, nullptr, 0, stream);
+}
+
+// ---------------------------------------------------------------------------
+// W4A8 (per-token INT8 activations): the streaming kernels for every M --
+// decode tiles up to 32 rows, 64 x 64 tiles (32 x 64 when those are fewer
+// than the CUs) above.
+// ---------------------------------------------------------------------------
+template <bool RAW>
+static mq_status launch_a8(GemmArgs a, hipStream_t stream) {
+    const mq_status rs = operand_resources<RAW>(a, true);
+    if (rs != MQ_OK) return rs;
+    if (a.M <= 16) {
+        const int spw = decode_spw(a.M, a.N);
+        if (spw == 2) launch_stream<1, 2, 1, 1, RAW, false, true>(a, 0, stream);
+        else launch_stream<1, 1, 1, 1, RAW, false, true>(a, 0, stream);
+    } else if (a.M <= 32) {
+        if (decode_spw(a.M, a.N) >= 2) launch_stream<2, 2, 1, 1, RAW, false, true>(a, 0, stream);
+        else launch_stream<2, 1, 1, 1, RAW, false, true>(a, 0, stream);
+    } else {
+        const int64_t t64 = (int64_t)((a.M + 63) / 64) * (a.N / 64);
+        const int64_t t32 = (int64_t)((a.M + 31) / 32) * (a.N / 64);
+        if (t32 > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
+        if (t64 >= kCUs) launch_stream<4, 4, 1, 1, RAW, false, true>(a, 0, stream);
+        else launch_stream<2, 4, 1, 1, RAW, false, true>(a, 0, stream);
+    }
+    return mq_host::launch_status();
+}
+
+extern "C" mq_status mq_fused_gemm_a8(int M, int N, int K,
+                                      const uint8_t* Xq8, const void* s_x,
+                                      const uint8_t* Wq, const void* s_w,
+                                      const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                                      const uint8_t* Rq, const void* s_r,
+                                      void* Y, int ldy, hipStream_t stream) {
+    mq_status st = check_common(M, N, K, Xq8, Wq, res_rowptr, res_kb, nnzb, Rq);
+    if (st != MQ_OK) return st;
+    if (ldy < N || ldy % 8 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
+    if (M == 0) return MQ_OK;
+    if (!s_x || !s_w || !Y || (nnzb > 0 && !s_r)) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::aligned(s_x, 2) || !mq_host::aligned(s_w, 2) || !mq_host::aligned(Y, 2) ||
+        (s_r && !mq_host::aligned(s_r, 2)))
+        return MQ_ERR_MISALIGNED;
+    GemmArgs a{M, N, K, Xq8, static_cast<const uint16_t*>(s_x), Wq, static_cast<const uint16_t*>(s_w),
+               nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq, static_cast<const uint16_t*>(s_r),
+               static_cast<uint16_t*>(Y), ldy, nullptr, nullptr};
+    a.nnzb = nnzb;
+    return launch_a8<false>(a, stream);
+}
+
+extern "C" mq_status mq_fused_gemm_a8_acc_i32(int M, int N, int K,
+                                              const uint8_t* Xq8,
+                                              const uint8_t* Wq,
+                                              const int32_t* res_rowptr, const int32_t* res_kb, int nnzb,
+                                              const uint8_t* Rq,
+                                              int32_t* Tb, int32_t* Tr, hipStream_t stream) {
+    mq_status st = check_common(M, N, K, Xq8, Wq, res_rowptr, res_kb, nnzb, Rq);
+    if (st != MQ_OK) return st;
+    if (M == 0) return MQ_OK;
+    if (!Tb || !Tr) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::aligned(Tb, 4) || !mq_host::aligned(Tr, 4)) return MQ_ERR_MISALIGNED;
+    GemmArgs a{M, N, K, Xq8, nullptr, Wq, nullptr, nnzb > 0 ? res_rowptr : nullptr, res_kb, Rq,
+               nullptr, nullptr, 0, Tb, Tr};
+    a.nnzb = nnzb;
+    return launch_a8<true>(a, stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -27,8 +27,8 @@ __device__ __forceinline__ uint16_t float_to_half_bits(float f) {
 // Scale of a symmetric 4-bit quantiser with row/group maximum `amax`:
 // fp16_rn(fp32(amax) / 7).  The library is built with correctly rounded fp32
 // division (-fhip-fp32-correctly-rounded-divide-sqrt, no fast-math).
-__device__ __forceinline__ uint16_t scale_bits_from_amax(float amax) {
-    return float_to_half_bits(amax / (float)kQmax);
+__device__ __forceinline__ uint16_t scale_bits_from_amax(float amax, int qmax = kQmax) {
+    return float_to_half_bits(amax / (float)qmax);
 }
 
 // |code| of an fp16 x for an fp16 scale s > 0 (the activation quantiser):
@@ -57,15 +57,51 @@ __device__ __forceinline__ float quant_mag(float ax, float s, float inv_s) {
 // is exact (an fma: for q != 0 both terms are multiples of half an ulp of s
 // and |e| is at most about s; for q = 0, e = x); comparing |e| with s/2
 // (exact) moves q to the nearest integer, ties to the even one.
-__device__ __forceinline__ int quant_code(float x, float s, float inv_s) {
+// (The argument does not depend on the size of q: it holds for the INT8
+// activation codes of the W4A8 variant, qmax = 127, as well.)
+__device__ __forceinline__ int quant_code_max(float x, float s, float inv_s, int qmax) {
     float q = rintf(x * inv_s);
     const float e = __builtin_fmaf(-q, s, x);
     const float h = 0.5f * s;
     const float ae = fabsf(e);
     const bool odd = ((int)q & 1) != 0;
     if (ae > h || (ae == h && odd)) q += e > 0.f ? 1.f : -1.f;
-    q = fminf(fmaxf(q, -(float)kQmax), (float)kQmax);
+    q = fminf(fmaxf(q, -(float)qmax), (float)qmax);
     return (int)q;
+}
+__device__ __forceinline__ int quant_code(float x, float s, float inv_s) {
+    return quant_code_max(x, s, inv_s, kQmax);
+}
+
+// --------------------------------------------------- W4A8 activation codes --
+// An INT8 code x in [-127, 127] is stored as x = 8 h + l with h = floor(x / 8)
+// in [-16, 15] and l in [0, 7]: h as an fp8 e4m3 byte (every integer up to 16
+// in magnitude is exact), l as a folded 4-bit code (e2m3 subnormal l / 8).
+// The matrix instruction then sums h (q/8) and (l/8)(q/8) exactly, and the
+// two products chained give the group sum / 64 as for W4A4.
+constexpr int kQmax8 = 127;
+// Byte offset, inside the 128-byte high-plane piece of a row and group, of the
+// 16-code chunk c (codes 16c .. 16c + 15).  A lane of the matrix instruction
+// reads 32 bytes at 32 (l / 16) and, for an fp8 operand, takes them as the
+// codes 16 (l / 16) + 0..15 and 64 + 16 (l / 16) + 0..15 of the group (the
+// pairing with the fp6 operand's codes 32 (l / 16) + 0..31 of the folded
+// layout, measured on the GPU by the raw-sum parity tests).
+__device__ __forceinline__ int hi_chunk_offset(int c) { return 32 * (c & 3) + 16 * (c >> 2); }
+
+// e4m3 byte of an integer h with |h| <= 16 (sign, exponent bias 7, 3 mantissa bits)
+__device__ __forceinline__ uint32_t e4m3_of_int(int h) {
+    const uint32_t a = (uint32_t)(h < 0 ? -h : h);
+    if (a == 0u) return 0u;
+    const int e = 31 - __builtin_clz(a);
+    const uint32_t m = ((a << 3) >> e) & 7u;
+    return (h < 0 ? 0x80u : 0u) | ((uint32_t)(e + 7) << 3) | m;
+}
+// integer value of an e4m3 byte written by e4m3_of_int
+__device__ __forceinline__ int int_of_e4m3(uint32_t b) {
+    if ((b & 0x7Fu) == 0u) return 0;
+    const int e = (int)((b >> 3) & 15u) - 7;
+    const int a = (int)(((8u + (b & 7u)) << e) >> 3);
+    return (b & 0x80u) ? -a : a;
 }
 
 // ---------------------------------------------------------- packed codes --
@@ -119,6 +155,11 @@ __device__ __forceinline__ i32x8 unfold_codes(const uint4 p) {
 // are exact and so is their sum: D = (sum of code products) / 64.
 __device__ __forceinline__ f32x4 mfma_codes(const i32x8 a, const i32x8 b, const f32x4 c) {
     return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 2, 2, 0, 0, 0, 0);
+}
+// the same with A given as 32 e4m3 bytes per lane (eight dwords, k order):
+// D = A (16 x 128, fp8) B^T (fp6 codes) + C
+__device__ __forceinline__ f32x4 mfma_e4m3_codes(const i32x8 a, const i32x8 b, const f32x4 c) {
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 2, 0, 0, 0, 0);
 }
 // removes the 1/64 of the e2m3 encoding (exact)
 constexpr float kCodeScale = 64.0f;

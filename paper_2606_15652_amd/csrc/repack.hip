@@ -77,6 +77,56 @@ __global__ __launch_bounds__(256) void repack_scales_kernel(const uint16_t* __re
     else dst[idx] = src[wscale_index(N, n, g)];
 }
 
+// W4A8 activation codes: library layout (e4m3 high plane, folded low plane,
+// both in group order) <-> canonical int8 rows [rows, ld].  One thread per 16
+// codes; -128 (not a code of the method) is stored as -127 and counted.
+template <bool TO_LIB>
+__global__ __launch_bounds__(256) void repack_act8_kernel(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                                          int rows, int K, int ld, int32_t* __restrict__ n_invalid) {
+    const int cpr = K / 16;
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (int64_t)rows * cpr) return;
+    const int r = (int)(idx / cpr), c = (int)(idx % cpr);
+    const int g = c >> 3, cc = c & 7;
+    const int64_t canon = (int64_t)r * ld + 16 * c;
+    const uint8_t* lib_src = TO_LIB ? nullptr : src;
+    uint8_t* lib_dst = TO_LIB ? dst : nullptr;
+    const int64_t hi_off = ((int64_t)g * rows + r) * 128 + hi_chunk_offset(cc);
+    const int64_t lo_off = (int64_t)rows * K + piece_offset(rows, r, g) + 8 * cc;
+    if constexpr (TO_LIB) {
+        const uint4 v = *reinterpret_cast<const uint4*>(src + canon);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        int l[16], bad = 0;
+        uint32_t hb[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            int q = (int)(int8_t)(uint8_t)(w[e >> 2] >> (8 * (e & 3)));
+            if (q == -128) {
+                q = -kQmax8;
+                ++bad;
+            }
+            const int h = q >> 3;
+            l[e] = q - 8 * h;
+            hb[e >> 2] |= e4m3_of_int(h) << (8 * (e & 3));
+        }
+        *reinterpret_cast<uint4*>(lib_dst + hi_off) = make_uint4(hb[0], hb[1], hb[2], hb[3]);
+        *reinterpret_cast<uint2*>(lib_dst + lo_off) = fold_codes(l);
+        if (bad && n_invalid) atomicAdd(n_invalid, bad);
+    } else {
+        const uint4 hv = *reinterpret_cast<const uint4*>(lib_src + hi_off);
+        const uint2 lv = *reinterpret_cast<const uint2*>(lib_src + lo_off);
+        const uint32_t hw[4] = {hv.x, hv.y, hv.z, hv.w};
+        uint32_t ow[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int h = int_of_e4m3((hw[e >> 2] >> (8 * (e & 3))) & 0xFFu);
+            const int q = 8 * h + chunk_code(lv.x, lv.y, e);
+            ow[e >> 2] |= ((uint32_t)q & 0xFFu) << (8 * (e & 3));
+        }
+        *reinterpret_cast<uint4*>(dst + canon) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+    }
+}
+
 static unsigned blocks_for(int64_t n) { return (unsigned)((n + 255) / 256); }
 
 template <bool TO_LIB, bool GROUPED>
@@ -152,4 +202,30 @@ extern "C" mq_status mq_unpack_act(int M, int K, const uint8_t* Xq, uint8_t* Xq_
     if (!Xq_c || !Xq) return MQ_ERR_INVALID_ARG;
     if (!mq_host::aligned(Xq_c, 8) || !mq_host::aligned(Xq, 16)) return MQ_ERR_MISALIGNED;
     return rows_launch<false, true>(Xq, Xq_c, M, K, ldq, nullptr, stream);
+}
+
+extern "C" mq_status mq_repack_act8(int M, int K, const int8_t* Xc, int ldq, uint8_t* Xq8, int32_t* n_invalid,
+                                    hipStream_t stream) {
+    if (M < 0 || K < 0) return MQ_ERR_INVALID_ARG;
+    if (!k_ok(K) || M > (1 << 24) || ldq < K || ldq % 16 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
+    if (M == 0) return MQ_OK;
+    if (!Xc || !Xq8) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::aligned(Xc, 16) || !mq_host::aligned(Xq8, 16) || (n_invalid && !mq_host::aligned(n_invalid, 4)))
+        return MQ_ERR_MISALIGNED;
+    const int64_t n = (int64_t)M * (K / 16);
+    hipLaunchKernelGGL((repack_act8_kernel<true>), dim3(blocks_for(n)), dim3(256), 0, stream,
+                       reinterpret_cast<const uint8_t*>(Xc), Xq8, M, K, ldq, n_invalid);
+    return mq_host::launch_status();
+}
+
+extern "C" mq_status mq_unpack_act8(int M, int K, const uint8_t* Xq8, int8_t* Xc, int ldq, hipStream_t stream) {
+    if (M < 0 || K < 0) return MQ_ERR_INVALID_ARG;
+    if (!k_ok(K) || M > (1 << 24) || ldq < K || ldq % 16 != 0) return MQ_ERR_UNSUPPORTED_SHAPE;
+    if (M == 0) return MQ_OK;
+    if (!Xc || !Xq8) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::aligned(Xc, 16) || !mq_host::aligned(Xq8, 16)) return MQ_ERR_MISALIGNED;
+    const int64_t n = (int64_t)M * (K / 16);
+    hipLaunchKernelGGL((repack_act8_kernel<false>), dim3(blocks_for(n)), dim3(256), 0, stream, Xq8,
+                       reinterpret_cast<uint8_t*>(Xc), M, K, ldq, nullptr);
+    return mq_host::launch_status();
 }

@@ -167,8 +167,22 @@ def workloads() -> List[Layer]:
     return out
 
 
+def table5_workloads() -> List[Layer]:
+    """Qwen3-8B GEMM operators with concatenated outputs (the shapes of the
+    paper's kernel-fusion latency table, out x in): qkv 6144 x 4096, o
+    4096 x 4096, gate_up 24576 x 4096, down 4096 x 12288; 10 % residual
+    density; prefill M = batch x 2048 tokens (the input length of the paper's
+    serving runs) and decode M = batch, for batch 4, 8, 16, 32."""
+    ms = (4, 8, 16, 32, 4 * 2048, 8 * 2048, 16 * 2048, 32 * 2048)
+    out: List[Layer] = []
+    for i, (k, n, tag) in enumerate(((4096, 6144, "qkv"), (4096, 4096, "o"),
+                                     (4096, 24576, "gate_up"), (12288, 4096, "down"))):
+        out.append(Layer(f"t5_{tag}", k, n, 10, seed_for(6, i), ms))
+    return out
+
+
 def workload(name: str) -> Layer:
-    for w in workloads():
+    for w in workloads() + table5_workloads():
         if w.name == name:
             return w
     raise KeyError(name)

@@ -158,3 +158,19 @@ def test_noalloc_validation(lib):
     assert f(0, 256, 256, A, 256, A, A, A, A, 1, A, A, A, 256, None) == OK        # empty: no scratch used
     assert f(4, 256, 200, A, 256, A, A, A, A, 1, A, A, A, 256, None) == SHAPE     # K not a multiple of 128
     assert f(65536, 256, 8192, A, 8192, A, A, None, None, 0, None, None, A, 256, None) == -6   # beyond scratch
+
+
+def test_a8_validation(lib):
+    assert lib.mq_quantize_act8(A, 0, 128, 128, A, A, None) == OK
+    assert lib.mq_quantize_act8(A, 4, 100, 128, A, A, None) == SHAPE
+    assert lib.mq_quantize_act8(A, 4, 128, 128, A + 8, A, None) == MISALIGNED
+    g = lib.mq_fused_gemm_a8
+    assert g(0, 256, 256, A, A, A, A, A, A, 1, A, A, A, 256, None) == OK
+    assert g(4, 200, 256, A, A, A, A, A, A, 1, A, A, A, 256, None) == SHAPE
+    assert g(4, 256, 256, A, A, A, A, A, A, 1, A, A, A, 252, None) == SHAPE
+    assert g(4, 256, 256, A + 8, A, A, A, A, A, 1, A, A, A, 256, None) == MISALIGNED
+    assert g(4, 256, 256, A, None, A, A, A, A, 1, A, A, A, 256, None) == INVALID
+    r = lib.mq_fused_gemm_a8_acc_i32
+    assert r(4, 256, 256, A, A, A, A, 1, A, None, A, None) == INVALID
+    assert lib.mq_repack_act8(4, 256, A, 250, A, None, None) == SHAPE
+    assert lib.mq_unpack_act8(4, 256, A + 8, A, 256, None) == MISALIGNED

@@ -301,3 +301,31 @@ def test_decode_kernel_every_output(tc, mq, orc, M, N, K, kind):
         Yl = mq.linear(dev(tc, X), pw)
         tc.cuda.synchronize()
         assert maxabsrel(Yl, Y64x) <= TIGHT
+
+
+# ------------------------------------------- concatenated-output operators --
+T5 = [("t5_qkv", 32), ("t5_gate_up", 4), ("t5_down", 8), ("t5_o", 8192), ("t5_qkv", 8192),
+      ("t5_gate_up", 8192), ("t5_down", 8192)]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,M", T5, ids=[f"{n}_M{m}" for n, m in T5])
+def test_table5_operators(tc, mq, orc, name, M):
+    """Qwen3-8B concatenated-output operators at decode and prefill sizes:
+    every output at decode M, whole tiles at prefill M."""
+    layer = synth.workload(name)
+    ref, Xq_ref, sx_ref, Y, Tb, Tr = run_layer(tc, mq, orc, layer, M)
+    if M <= 32:
+        Tb_ref, Tr_ref, Y64 = orc.linear(Xq_ref, sx_ref, ref)
+        assert np.array_equal(host(Tb), Tb_ref) and np.array_equal(host(Tr), Tr_ref)
+        assert maxabsrel(Y, Y64) <= TIGHT
+        return
+    for m0, m1, n0, n1 in tiles_to_check(M, layer.N, ref.rowptr):
+        mm, nn = np.meshgrid(np.arange(m0, m1, dtype=np.int32), np.arange(n0, n1, dtype=np.int32),
+                             indexing="ij")
+        tb_ref, tr_ref, y64 = orc.linear_sampled(Xq_ref, sx_ref, ref, mm.ravel(), nn.ravel())
+        tile = (slice(m0, m1), slice(n0, n1))
+        assert np.array_equal(host(Tb[tile]).ravel(), tb_ref)
+        assert np.array_equal(host(Tr[tile]).ravel(), tr_ref)
+        y = Y[tile].float().cpu().numpy().astype(np.float64).ravel()
+        assert np.abs(y - y64).max() / max(np.abs(y64).max(), 1e-30) <= TIGHT
