@@ -55,6 +55,8 @@ def lib() -> C.CDLL:
             "orc_unpack_codes": (None, [P, i, i, P]),
             "orc_pack_nibbles": (None, [P, i, i, P]),
             "orc_unpack_nibbles": (None, [P, i, i, P]),
+            "orc_pack_act6": (None, [P, i, i, P]),
+            "orc_unpack_act6": (i64, [P, i, i, P]),
             "orc_unpack_code": (i, [P, i]),
             "orc_quantize_act": (None, [P, i, i, i, P, P]),
             "orc_quantize_weight": (None, [P, i, i, P, P, P]),
@@ -226,6 +228,44 @@ def unblock_scales(dev: np.ndarray) -> np.ndarray:
     d = np.ascontiguousarray(dev)
     N, G = d.shape
     return np.ascontiguousarray(d.reshape(G, N).T)
+
+
+# The activation operand layout the library's quantiser writes (3K/4 bytes
+# a row; oracle C, from the field definition): a main plane and a tail plane
+# per 128-code group, holding the unfolded 6-bit fields of each 32-code quarter.
+def pack_act6(codes: np.ndarray) -> np.ndarray:
+    """Activation operand layout [M, 3K/4] of int codes [M, K] in [-7, 7]."""
+    q = np.ascontiguousarray(codes, dtype=np.int8)
+    M, K = q.shape
+    if np.abs(q.astype(np.int16)).max(initial=0) > 7:
+        raise ValueError("codes must lie in [-7, 7]")
+    out = np.empty((M, 3 * K // 4), np.uint8)
+    lib().orc_pack_act6(_p(q), M, K, _p(out))
+    return out
+
+
+def unpack_act6(dev: np.ndarray, K: int):
+    """Codes [M, K] of the activation operand layout, and the number of
+    fields that are not codes (non-zero exponent bits)."""
+    d = np.ascontiguousarray(dev, np.uint8).reshape(-1)
+    M = d.size // (3 * K // 4)
+    out = np.empty((M, K), np.int8)
+    bad = lib().orc_unpack_act6(_p(d), M, K, _p(out))
+    return out, int(bad)
+
+
+def act6_from_packed(packed: np.ndarray, K: int) -> np.ndarray:
+    """Row-major folded packed rows [M, K/2] -> activation operand layout."""
+    return pack_act6(unpack_codes_c(packed, K))
+
+
+def packed_from_act6(dev: np.ndarray, K: int) -> np.ndarray:
+    """Activation operand layout -> row-major folded packed rows [M, K/2]
+    (raises if a field is not a code)."""
+    q, bad = unpack_act6(dev, K)
+    if bad:
+        raise ValueError(f"{bad} fields of the activation operand layout are not codes")
+    return pack_codes(q)
 
 
 # ------------------------------------------------------- quantisation ----

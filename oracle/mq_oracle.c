@@ -237,6 +237,75 @@ void orc_unpack_codes(const uint8_t* packed, int rows, int K, int8_t* out)
 }
 
 /* ------------------------------------------------------------------------ */
+/* Activation operand layout (the form the library's quantiser writes): for  */
+/* row r, 128-code group g and quarter j (codes k = 128 g + 32 j + e,         */
+/* e = 0 .. 31), the 6-bit fields f_e of the packed layout (not folded) form */
+/* the 192-bit word F = sum_e f_e 2^(6e), six little-endian 32-bit words     */
+/* d0 .. d5.  With G = K / 128 groups and M rows:                            */
+/*   d0 .. d3 at byte (g M + r) 64 + 16 j          (main plane), and        */
+/*   d4, d5   at byte G M 64 + ((4 g + j) M + r) 8  (tail plane).            */
+/* 3K/4 bytes per row.  The fields' exponent bits (6e+3, 6e+4) are zero.     */
+/* ------------------------------------------------------------------------ */
+static uint64_t act6_main(int M, int r, int g, int j) { return ((uint64_t)g * M + r) * 64 + 16 * (uint64_t)j; }
+static uint64_t act6_tail(int M, int G, int r, int g, int j)
+{
+    return (uint64_t)G * M * 64 + (((uint64_t)g * 4 + j) * M + r) * 8;
+}
+
+void orc_pack_act6(const int8_t* q, int M, int K, uint8_t* out)
+{
+    int G = K / 128;
+    for (int r = 0; r < M; ++r)
+        for (int g = 0; g < G; ++g)
+            for (int j = 0; j < 4; ++j) {
+                uint32_t d[6] = {0, 0, 0, 0, 0, 0};
+                for (int e = 0; e < 32; ++e) {
+                    int v = q[(int64_t)r * K + 128 * g + 32 * j + e];
+                    uint32_t f = (uint32_t)((v < 0 ? 32 : 0) + (v < 0 ? -v : v));
+                    for (int b = 0; b < 6; ++b)
+                        if (f & (1u << b)) {
+                            int bit = 6 * e + b;
+                            d[bit / 32] |= 1u << (bit % 32);
+                        }
+                }
+                uint8_t* mp = out + act6_main(M, r, g, j);
+                for (int w = 0; w < 4; ++w) wr32(mp + 4 * w, d[w]);
+                uint8_t* tp = out + act6_tail(M, G, r, g, j);
+                wr32(tp, d[4]);
+                wr32(tp + 4, d[5]);
+            }
+}
+
+/* the inverse; returns the number of fields with a non-zero exponent bit
+ * (such a field is not a code) */
+int64_t orc_unpack_act6(const uint8_t* in, int M, int K, int8_t* q)
+{
+    int G = K / 128;
+    int64_t bad = 0;
+    for (int r = 0; r < M; ++r)
+        for (int g = 0; g < G; ++g)
+            for (int j = 0; j < 4; ++j) {
+                uint32_t d[6];
+                const uint8_t* mp = in + act6_main(M, r, g, j);
+                const uint8_t* tp = in + act6_tail(M, G, r, g, j);
+                for (int w = 0; w < 4; ++w) d[w] = rd32(mp + 4 * w);
+                d[4] = rd32(tp);
+                d[5] = rd32(tp + 4);
+                for (int e = 0; e < 32; ++e) {
+                    uint32_t f = 0;
+                    for (int b = 0; b < 6; ++b) {
+                        int bit = 6 * e + b;
+                        if (d[bit / 32] & (1u << (bit % 32))) f |= 1u << b;
+                    }
+                    if (f & 24u) ++bad;
+                    int mag = (int)(f & 7u);
+                    q[(int64_t)r * K + 128 * g + 32 * j + e] = (int8_t)((f & 32u) ? -mag : mag);
+                }
+            }
+    return bad;
+}
+
+/* ------------------------------------------------------------------------ */
 /* Canonical nibble layout (the interchange format of the library's          */
 /* boundary): one 4-bit two's-complement code per nibble, two per byte, the  */
 /* even k in the low nibble, rows of K/2 bytes in k order.  A nibble holds   */

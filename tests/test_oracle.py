@@ -680,6 +680,84 @@ def test_device_order_formula_random(orc):
             assert ds[g * R + n] == s[n, g]
 
 
+def _act_layout_golden():
+    M = K = None
+    cases = []
+    for line in open(os.path.join(GOLDEN, "act_operand_layout.txt")):
+        line = line.split("#", 1)[0].strip()
+        if not line:
+            continue
+        key, val = line.split(":", 1)
+        if key == "M":
+            M = int(val)
+        elif key == "K":
+            K = int(val)
+        else:
+            code, nz = val.split("|")
+            r, k, q = (int(x) for x in code.split())
+            cases.append((r, k, q, {int(a): int(b) for a, b in (t.split(":") for t in nz.split())}))
+    return M, K, cases
+
+
+def test_act_operand_layout_golden(orc):
+    """pack_act6 / unpack_act6 (the activation operand layout every GPU test
+    compares the quantiser's output with) against hand-worked bytes."""
+    M, K, cases = _act_layout_golden()
+    for r, k, q, nz in cases:
+        codes = np.zeros((M, K), np.int8)
+        codes[r, k] = q
+        dev = orc.pack_act6(codes).reshape(-1)
+        assert dev.size == M * K * 3 // 4
+        got = {int(i): int(dev[i]) for i in np.nonzero(dev)[0]}
+        assert got == nz, (r, k, q, got)
+        back, bad = orc.unpack_act6(dev, K)
+        assert bad == 0 and np.array_equal(back, codes)
+
+
+def test_act_operand_layout_matches_unfolded_chunks(orc):
+    """Each quarter's six words are the unfolded words (o0, o1, o2) of the two
+    folded chunks of the same 32 codes in the packed layout (whose decoder the
+    pack-layout pins fix), and every field decodes back to its code."""
+    rng = np.random.default_rng(12)
+    for M, K in ((5, 384), (1, 128), (33, 1024)):
+        codes = rng.integers(-7, 8, (M, K)).astype(np.int8)
+        dev = orc.pack_act6(codes).reshape(-1)
+        packed = orc.pack_codes(codes)
+        za = sum(1 << (6 * e + b) for e in range(16) for b in (3, 4) if (6 * e + b) < 32)
+        zb = sum(1 << (6 * e + b - 32) for e in range(16) for b in (3, 4) if 32 <= (6 * e + b) < 64)
+        G = K // B
+        for _ in range(40):
+            r, g, j = int(rng.integers(M)), int(rng.integers(G)), int(rng.integers(4))
+            mo = (g * M + r) * 64 + 16 * j
+            to = G * M * 64 + ((4 * g + j) * M + r) * 8
+            d = np.concatenate([dev[mo:mo + 16], dev[to:to + 8]]).view("<u4").astype(np.uint64)
+            F = sum(int(d[w]) << (32 * w) for w in range(6))
+            for h in range(2):
+                c = (128 * g + 32 * j + 16 * h) // 16
+                p0, p1 = (int(x) for x in packed[r, 8 * c:8 * c + 8].view("<u4"))
+                o = (p0 & ~za & 0xFFFFFFFF) | ((p1 & ~zb & 0xFFFFFFFF) << 32) | (((p0 & za) | (p1 & zb)) << 64)
+                assert (F >> (96 * h)) & ((1 << 96) - 1) == o, (M, K, r, g, j, h)
+            for e in range(32):
+                f = (F >> (6 * e)) & 63
+                v = -(f & 7) if f & 32 else f & 7
+                assert v == codes[r, 128 * g + 32 * j + e]
+        back, bad = orc.unpack_act6(dev, K)
+        assert bad == 0 and np.array_equal(back, codes)
+        assert np.array_equal(orc.packed_from_act6(dev, K), packed)
+
+
+def test_act_operand_layout_counts_non_codes(orc):
+    """A field with an exponent bit set is not a code: unpack_act6 counts it."""
+    M, K = 2, 128
+    dev = orc.pack_act6(np.zeros((M, K), np.int8)).reshape(-1).copy()
+    dev[0] |= 0x08                      # bit 3 of field 0 (exponent) of row 0
+    dev[M * 64] |= 0x80                # tail plane, row 0, quarter 0: d4 bit 7 = F bit 135 (field 22, bit 3)
+    _, bad = orc.unpack_act6(dev, K)
+    assert bad == 2
+    with pytest.raises(ValueError):
+        orc.packed_from_act6(dev, K)
+
+
 def test_hessian_constant_against_exact_distortion(orc):
     """App. A: the exact output distortion L(S) = (2/N) ||X E_S^T||_F^2 (its own
     constant, computed by a matrix product) equals the diagonal surrogate
