@@ -91,6 +91,10 @@ def parse():
     ap.add_argument("--summarize-counters", nargs="+", metavar=("OUT_MD", "CSV"),
                     help="fold the counter_collection.csv files of --kernel-run passes into a "
                          "markdown table OUT_MD (needs no GPU); SPECS from --kernel-run")
+    ap.add_argument("--selection", action="store_true",
+                    help="residual block selection study (Section 3 Eq. (5), Fig. 2b): output-distortion "
+                         "reduction C(S) of Delta-Hessian, residual-norm, weight-magnitude and random "
+                         "selection (and exact greedy selection on the smallest layer) over block budgets")
     ap.add_argument("--traffic", action="store_true",
                     help="counter run: eager fused GEMM launches at the largest M, then a plain "
                          "256 MiB device copy as the scale reference for FETCH_SIZE / WRITE_SIZE")
@@ -292,6 +296,99 @@ def summarize_counters(args):
     print("\n".join(lines + raw))
 
 
+SELECTION_BUDGETS = (0.01, 0.02, 0.05, 0.10, 0.20, 0.30, 0.50)
+SELECTION_LAYERS = ("c1_1024", "c2_4096", "c4_qo")
+SELECTION_TOKENS = 512
+GREEDY_MAX_BLOCKS = 64
+
+
+def selection(args):
+    """C(S) = (||X R||^2 - ||X (R - M_S . Q(R))||^2) / ||X R||^2 (Section 3,
+    Eq. (5)) on the calibration activations X, for the block sets chosen by:
+    Algorithm 1's Delta-Hessian score, the residual norm ||R_B||_F^2, the
+    largest weight magnitude in the block, a random order and, where the layer
+    has at most GREEDY_MAX_BLOCKS blocks, the exact greedy output-distortion
+    selection (largest marginal gain first).  Scores, base and residual
+    quantisation come from the library's weight preparation (GPU); the
+    distortion sums are fp64 matrix products.  One JSON line per layer."""
+    import numpy as np
+    import torch
+    import paper_2606_15652_amd as mq
+    import synth
+
+    dev = torch.device("cuda:0")
+    names = args.only.split(",") if args.only else SELECTION_LAYERS
+    for name in names:
+        layer = synth.workload(name)
+        N, K = layer.N, layer.K
+        NB, KB = N // 128, K // 128
+        W = torch.from_numpy(layer.weight()).to(dev)
+        X = torch.from_numpy(layer.act(SELECTION_TOKENS)).to(dev)
+        # every block's residual quantised: Q(R) of any selection is a mask of it
+        pw = mq.prepare_weight(W, NB * KB)
+        Wc, swc, Rc = mq.unpack_weights(pw)
+        def codes(nib):
+            lo = (nib & 0xF).to(torch.int16)
+            hi = (nib >> 4).to(torch.int16)
+            q = torch.stack((lo, hi), -1).reshape(*nib.shape[:-1], nib.shape[-1] * 2)
+            return torch.where(q >= 8, q - 16, q).to(torch.float64)
+        s_w = swc.to(torch.float64).repeat_interleave(128, dim=1)
+        Qw = (codes(Wc).to(torch.float32) * s_w.to(torch.float32))      # exact: 3-bit code x fp16 scale
+        R = (W - Qw).to(torch.float64)                                  # fp32 residual, as the library forms it
+        QR = torch.zeros((N, K), dtype=torch.float64, device=dev)
+        rowptr = pw.rowptr.cpu().numpy()
+        kb = pw.kb.cpu().numpy()
+        qr_blocks = codes(Rc) * pw.s_r.to(torch.float64)[:, :, None]
+        for nb in range(NB):
+            for p in range(rowptr[nb], rowptr[nb + 1]):
+                QR[128 * nb:128 * nb + 128, 128 * kb[p]:128 * kb[p] + 128] = qr_blocks[p]
+        Xd = X.to(torch.float64)
+        XR = Xd @ R.T
+        base = float((XR * XR).sum())
+        # the effect of each block on X E^T: X_k (QR_B)^T for block (nb, kb)
+        def dist(mask):
+            E = R - QR * mask.repeat_interleave(128, 0).repeat_interleave(128, 1)
+            XE = Xd @ E.T
+            return float((XE * XE).sum())
+        h = mq.hessian_diag(X)
+        Wq_lib, s_w_lib, _ = mq.quantize_weight(W, with_score=False)
+        scores = {
+            "dhessian": mq.block_scores_dhessian(W, Wq_lib, s_w_lib, h),
+            "resnorm": pw.score,
+            "magnitude": W.abs().reshape(NB, 128, KB, 128).amax(dim=(1, 3)).to(torch.float64),
+            "random": torch.from_numpy(np.random.default_rng(7).permutation(NB * KB).astype(np.float64))
+                      .reshape(NB, KB).to(dev),
+        }
+        orders = {k: torch.argsort(v.reshape(-1), descending=True, stable=True) for k, v in scores.items()}
+        if NB * KB <= GREEDY_MAX_BLOCKS:
+            mask = torch.zeros(NB * KB, dtype=torch.float64, device=dev)
+            order = []
+            for _ in range(NB * KB):
+                best, best_d = None, None
+                for b in range(NB * KB):
+                    if mask[b] > 0:
+                        continue
+                    mask[b] = 1
+                    d = dist(mask.reshape(NB, KB))
+                    mask[b] = 0
+                    if best_d is None or d < best_d:
+                        best, best_d = b, d
+                mask[best] = 1
+                order.append(best)
+            orders["greedy_exact"] = torch.tensor(order, device=dev)
+        rows = {}
+        for crit, order in orders.items():
+            curve = []
+            for rho in SELECTION_BUDGETS:
+                nsel = int(rho * NB * KB + 0.5)
+                mask = torch.zeros(NB * KB, dtype=torch.float64, device=dev)
+                mask[order[:nsel]] = 1
+                curve.append(round(1.0 - dist(mask.reshape(NB, KB)) / base, 4))
+            rows[crit] = curve
+        print(json.dumps({"selection": name, "N": N, "K": K, "blocks": NB * KB, "tokens": SELECTION_TOKENS,
+                          "budgets": list(SELECTION_BUDGETS), "C": rows}), flush=True)
+
+
 def graph_of(torch, fn, calls):
     """Capture `calls` back-to-back invocations of fn in one HIP graph."""
     fn()                                   # warm the libraries outside capture
@@ -370,7 +467,7 @@ def families(args):
             if args.max_m is not None and m > args.max_m:
                 continue
             X = torch.from_numpy(layer.act(m)).to(dev)
-            Xq = torch.empty((m, K // 2), dtype=torch.uint8, device=dev)
+            Xq = torch.empty((m, mq.act_bytes(K)), dtype=torch.uint8, device=dev)
             sx = torch.empty((m,), dtype=torch.float16, device=dev)
             Y = torch.empty((m, N), dtype=torch.float16, device=dev)
             ws = torch.empty(max(1, mq.linear_workspace_bytes(m, N, K)), dtype=torch.uint8, device=dev)
@@ -434,6 +531,9 @@ def main():
     if args.kernel_run:
         kernel_run(args)
         return
+    if args.selection:
+        selection(args)
+        return
 
     import numpy as np
     import torch
@@ -459,7 +559,7 @@ def main():
                                       pw0.kb.clone(), pw0.Rq.clone(), pw0.s_r.clone())
                       for _ in range(ncopy - 1)]
     Xs = {m: torch.from_numpy(layer.act(m)).to(dev) for m in ms}
-    Xqs = {m: torch.empty((m, K // 2), dtype=torch.uint8, device=dev) for m in ms}
+    Xqs = {m: torch.empty((m, mq.act_bytes(K)), dtype=torch.uint8, device=dev) for m in ms}
     sxs = {m: torch.empty((m,), dtype=torch.float16, device=dev) for m in ms}
     Ys = {m: torch.empty((m, N), dtype=torch.float16, device=dev) for m in ms}
     Ws = {m: torch.empty(max(1, mq.linear_workspace_bytes(m, N, K)), dtype=torch.uint8, device=dev) for m in ms}

@@ -21,7 +21,7 @@
  * - fp16 arrays are IEEE binary16 passed as `void*` / `const void*`.
  * - Shapes: K and N are multiples of 128 with 128 <= K <= 2^20 and
  *   128 <= N <= 2^24; 0 <= M <= 2^24 (M == 0 is a no-op).
- * - Packed 4-bit codes (Xq, Wq, Rq): codes q in [-7, 7], 4 bits each, a row
+ * - Packed 4-bit weight codes (Wq, Rq): codes q in [-7, 7], 4 bits each, a row
  *   of K codes taking K/2 bytes as K/16 chunks of 8 bytes; chunk c holds codes
  *   16c .. 16c+15.  Code e of a chunk is the 6-bit sign-magnitude field
  *   f_e = 32 [q < 0] + |q| at bit 6e of a 96-bit word O = (o0, o1, o2) of
@@ -34,14 +34,24 @@
  *   the fp6 (e2m3) matrix instruction of CDNA4 with four bit operations per
  *   chunk; the paper fixes no bit layout (Section 4.2 fuses layout packing
  *   with quantisation).
- * - Group order of packed rows (Xq [M rows], Wq [N rows]): a row's K/2 bytes
- *   are K/128 pieces of 64 bytes (one 128-code group each), stored
- *   group-major: piece (row r, group g) of a matrix of R rows sits at byte
- *   (g R + r) 64.  Every 128-row x 128-code tile is then one contiguous run
- *   of bytes, and the tiles of neighbouring row blocks are neighbours.
+ * - Group order of packed weight rows (Wq [N rows]): a row's K/2 bytes are
+ *   K/128 pieces of 64 bytes (one 128-code group each), stored group-major:
+ *   piece (row n, group g) sits at byte (g N + n) 64.  Every 128-row x
+ *   128-code tile is then one contiguous run of bytes, and the tiles of
+ *   neighbouring row blocks are neighbours.
+ * - Activation codes Xq [M rows] (codes in [-7, 7]) are stored in the
+ *   operand form of the fp6 matrix instruction, so the GEMM reads them with
+ *   no bit work: 3K/4 bytes a row.  For row r, group g (G = K/128 groups)
+ *   and quarter j = 0..3 (codes k = 128 g + 32 j + e, e = 0..31), the fields
+ *   f_e above, unfolded, form the 192-bit word F = sum_e f_e 2^(6e), six
+ *   little-endian 32-bit words d0..d5:
+ *       d0..d3 at byte (g M + r) 64 + 16 j               (main plane),
+ *       d4, d5 at byte G M 64 + ((4 g + j) M + r) 8       (tail plane).
+ *   The bits 6e+3, 6e+4 of every field must be zero (mq_quantize_act and
+ *   mq_repack_act write them so); other patterns give unspecified outputs.
  * - Weight scales s_w are stored [K/128][N]: s_w of (row n, group g) at
  *   element g N + n.
- * - Packed operand pointers (Xq, Wq, Rq) must be 16-byte aligned; fp16
+ * - Code operand pointers (Xq, Wq, Rq) must be 16-byte aligned; fp16
  *   pointers 2-byte aligned; int32 pointers 4-byte aligned; fp32/fp64 arrays
  *   naturally aligned.  Violations return MQ_ERR_MISALIGNED.
  * - Canonical interchange layout (mq_repack_*, mq_unpack_*): one
@@ -53,7 +63,8 @@
  *   layout above.
  * - Inputs must be finite.  Outputs must not alias inputs.
  * - Thread safety: every call may be made concurrently from several host
- *   threads; the library keeps no mutable global state.
+ *   threads.  The only global state is the per-device address of the
+ *   scratch array of mq_linear_noalloc, set once per device under a lock.
  */
 #ifndef MQ_H
 #define MQ_H
@@ -109,7 +120,7 @@ int mq_version(void);
  *     a = max_k |X[m,k]|,  s_x[m] = fp16_rn(fp32(a) / 7),
  *     Xq[m,k] = clamp(round_half_even(X[m,k] / s_x[m]), -7, 7)  (0 if s == 0)
  *   X   : fp16 [M, ldx] row-major, ldx >= K, ldx % 8 == 0, 16-byte aligned.
- *   Xq  : out, uint8 [M, K/2] packed codes in group order (layout above).
+ *   Xq  : out, uint8 [M, 3K/4] codes in the activation operand layout (above).
  *   s_x : out, fp16 [M].
  */
 mq_status mq_quantize_act(const void* X, int M, int K, int ldx,
@@ -125,7 +136,7 @@ size_t mq_fused_gemm_workspace_size(int M, int N, int K);
  *     A_b[m,n,g] = sum_{k in g} Xq[m,k] Wq[n,k]
  *     A_r[m,n,g] = sum_{k in g} Xq[m,k] Rq[p][n%128][k%128]   if (n/128,g) in S
  *     Y[m,n] = fp16( s_x[m] * sum_g ( s_w[n,g] A_b + s_r[p][n%128] A_r ) )
- *   Xq, s_x          : uint8 [M, K/2] group order, fp16 [M] (from mq_quantize_act)
+ *   Xq, s_x          : uint8 [M, 3K/4] operand layout, fp16 [M] (from mq_quantize_act)
  *   Wq, s_w          : uint8 [N, K/2] group order, fp16 [K/128, N]
  *   res_rowptr       : int32 [N/128 + 1], CSR over 128-row block rows;
  *                      res_rowptr[0] == 0, res_rowptr[N/128] == nnzb.
@@ -301,10 +312,10 @@ mq_status mq_unpack_weights(int N, int K, const uint8_t* Wq, const void* s_w, in
                             hipStream_t stream);
 
 /*
- * Canonical int4 activation codes -> library layout (group order), e.g. for
+ * Canonical int4 activation codes -> the library's activation operand layout, e.g. for
  * codes quantised elsewhere; -8 handled as for mq_repack_weights.
  *   Xq_c : uint8 [M, ldq] canonical rows (ldq >= K/2, ldq % 8 == 0), 8-byte aligned.
- *   Xq   : out, uint8 [M, K/2] library layout, 16-byte aligned.
+ *   Xq   : out, uint8 [M, 3K/4] activation operand layout, 16-byte aligned.
  */
 mq_status mq_repack_act(int M, int K, const uint8_t* Xq_c, int ldq, uint8_t* Xq,
                         int32_t* n_invalid, hipStream_t stream);

@@ -146,17 +146,23 @@ def _scratch(nbytes, device, stream, given=None, name="workspace"):
 
 
 # -------------------------------------------------------------- hot path --
+def act_bytes(K: int) -> int:
+    """Bytes per row of INT4 activation codes in the library's operand layout (3K/4)."""
+    return 3 * K // 4
+
+
 def quantize_act(X, out=None, stream=None):
-    """Per-token INT4 quantisation of fp16 X [M, K] -> (Xq uint8 [M, K/2], s_x fp16 [M])."""
+    """Per-token INT4 quantisation of fp16 X [M, K] -> (Xq uint8 [M, 3K/4] in
+    the operand layout, s_x fp16 [M])."""
     torch = _torch()
     _need(X, torch.float16, "X", 2)
     M, K = X.shape
     if out is None:
-        Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=X.device)
+        Xq = torch.empty((M, act_bytes(K)), dtype=torch.uint8, device=X.device)
         s_x = torch.empty((M,), dtype=torch.float16, device=X.device)
     else:
         Xq, s_x = out
-        _need_out(Xq, (M, K // 2), torch.uint8, "out[0] (Xq)")
+        _need_out(Xq, (M, act_bytes(K)), torch.uint8, "out[0] (Xq)")
         _need_out(s_x, (M,), torch.float16, "out[1] (s_x)")
     _check("mq_quantize_act", load().mq_quantize_act(_ptr(X), M, K, X.stride(0), _ptr(Xq),
                                                      _ptr(s_x), _stream(stream)))
@@ -201,7 +207,7 @@ def fused_gemm(Xq, s_x, pw: PackedWeight, out=None, variant: str = "auto", strea
     _need(Xq, torch.uint8, "Xq", 2)
     _need(s_x, torch.float16, "s_x", 1)
     M = Xq.shape[0]
-    if Xq.shape[1] * 2 != pw.K or s_x.shape[0] != M:
+    if Xq.shape[1] != act_bytes(pw.K) or s_x.shape[0] != M:
         raise ValueError("Xq / s_x shapes do not match the weight")
     Y = out if out is not None else torch.empty((M, pw.N), dtype=torch.float16, device=Xq.device)
     if out is not None:
@@ -223,7 +229,7 @@ def unfused_gemm(Xq, s_x, pw: PackedWeight, out=None, stream=None, workspace=Non
     _need(Xq, torch.uint8, "Xq", 2)
     _need(s_x, torch.float16, "s_x", 1)
     M = Xq.shape[0]
-    if Xq.shape[1] * 2 != pw.K or s_x.shape[0] != M:
+    if Xq.shape[1] != act_bytes(pw.K) or s_x.shape[0] != M:
         raise ValueError("Xq / s_x shapes do not match the weight")
     Y = out if out is not None else torch.empty((M, pw.N), dtype=torch.float16, device=Xq.device)
     if out is not None:
@@ -243,6 +249,8 @@ def fused_gemm_acc_i32(Xq, pw: PackedWeight, variant: str = "auto", stream=None)
     torch = _torch()
     _need(Xq, torch.uint8, "Xq", 2)
     M = Xq.shape[0]
+    if Xq.shape[1] != act_bytes(pw.K):
+        raise ValueError("Xq shape does not match the weight")
     Tb = torch.empty((M, pw.N), dtype=torch.int32, device=Xq.device)
     Tr = torch.empty((M, pw.N), dtype=torch.int32, device=Xq.device)
     rp, kb, rq, _ = _res_ptrs(pw)
@@ -387,11 +395,11 @@ def unpack_weights(pw: PackedWeight, stream=None):
 
 
 def repack_act(Xq_c, n_invalid=None, stream=None):
-    """Canonical int4 activation rows uint8 [M, K/2] -> library layout."""
+    """Canonical int4 activation rows uint8 [M, K/2] -> library operand layout [M, 3K/4]."""
     torch = _torch()
     _need(Xq_c, torch.uint8, "Xq_c", 2)
     M, K = Xq_c.shape[0], Xq_c.shape[1] * 2
-    Xq = torch.empty((M, K // 2), dtype=torch.uint8, device=Xq_c.device)
+    Xq = torch.empty((M, act_bytes(K)), dtype=torch.uint8, device=Xq_c.device)
     if n_invalid is not None:
         _need(n_invalid, torch.int32, "n_invalid", 1)
     _check("mq_repack_act", load().mq_repack_act(M, K, _ptr(Xq_c), Xq_c.stride(0), _ptr(Xq),
@@ -400,10 +408,12 @@ def repack_act(Xq_c, n_invalid=None, stream=None):
 
 
 def unpack_act(Xq, stream=None):
-    """Library-layout activation codes uint8 [M, K/2] -> canonical rows."""
+    """Library-layout activation codes uint8 [M, 3K/4] -> canonical rows [M, K/2]."""
     torch = _torch()
     _need(Xq, torch.uint8, "Xq", 2)
-    M, K = Xq.shape[0], Xq.shape[1] * 2
+    M, K = Xq.shape[0], Xq.shape[1] * 4 // 3
+    if Xq.shape[1] != act_bytes(K) or K % 128:
+        raise ValueError("Xq is not in the operand layout of a K divisible by 128")
     Xq_c = torch.empty((M, K // 2), dtype=torch.uint8, device=Xq.device)
     _check("mq_unpack_act", load().mq_unpack_act(M, K, _ptr(Xq), _ptr(Xq_c), K // 2, _stream(stream)))
     return Xq_c

@@ -8,9 +8,10 @@
 // values, packed 16-bit maxima), reduced across the wave with xor-shuffles and
 // across the four waves through LDS.  Codes are then formed from the
 // registers (rows up to CPT * 4096 elements) or by re-reading the row (longer
-// rows), with the division-free exact rounding of quant_mag, and written as
-// one folded 8-byte chunk per 16 codes in the device group order
-// (piece_offset): coalesced 16-byte loads, 8-byte stores.
+// rows), with the division-free exact rounding of quant_mag, and written in
+// the matrix instruction's operand form (act_main_offset / act_tail_offset):
+// the 16 codes of an even chunk are dwords d0 .. d2 of their quarter, those of
+// the odd chunk d3 (main plane) and d4, d5 (tail plane).
 #include "mq_device.h"
 
 namespace mq {
@@ -27,10 +28,19 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
     const int m = blockIdx.x;
     const int t = threadIdx.x;
     const uint16_t* row = X + (int64_t)m * ldx;
-    const int nchunks = K / 16;
-    // chunk c (codes 16c .. 16c+15) is chunk c % 8 of the piece of group c / 8
-    auto out = [&](int c) -> uint2& {
-        return *reinterpret_cast<uint2*>(Xq + piece_offset(M, m, c >> 3) + (c & 7) * 8);
+    const int nchunks = K / 16, G = K / 128;
+    // chunk c (codes 16c .. 16c+15) is half c % 2 of quarter (c / 2) % 4 of group c / 8
+    auto store = [&](int c, const uint4 v0, const uint4 v1, float s, float inv_s) {
+        uint32_t o0, o1, o2;
+        quant_fields(v0, v1, s, inv_s, o0, o1, o2);
+        const int g = c >> 3, j = (c >> 1) & 3;
+        uint8_t* main = Xq + act_main_offset(M, m, g) + 16 * j;
+        if ((c & 1) == 0) {
+            *reinterpret_cast<uint3*>(main) = make_uint3(o0, o1, o2);
+        } else {
+            *reinterpret_cast<uint32_t*>(main + 12) = o0;
+            *reinterpret_cast<uint2*>(Xq + act_tail_offset(M, G, m, g, j)) = make_uint2(o1, o2);
+        }
     };
 
     uint32_t amax = 0;
@@ -69,12 +79,12 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
 #pragma unroll
         for (int i = 0; i < CPT; ++i) {
             const int c = t + i * kActThreads;
-            if (c < nchunks) out(c) = quant_chunk(v[i][0], v[i][1], s, inv_s);
+            if (c < nchunks) store(c, v[i][0], v[i][1], s, inv_s);
         }
     } else {
         for (int c = t; c < nchunks; c += kActThreads)
-            out(c) = quant_chunk(*reinterpret_cast<const uint4*>(row + 16 * c),
-                                 *reinterpret_cast<const uint4*>(row + 16 * c + 8), s, inv_s);
+            store(c, *reinterpret_cast<const uint4*>(row + 16 * c), *reinterpret_cast<const uint4*>(row + 16 * c + 8),
+                  s, inv_s);
     }
 }
 

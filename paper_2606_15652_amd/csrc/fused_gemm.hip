@@ -144,6 +144,7 @@ __device__ __forceinline__ void group_row(const i32x8 a, const i32x8 (&w)[WN], c
 // fp32 partial sums; reduce_splits_kernel adds them in split order
 // (deterministic) and applies s_x.
 constexpr int kTB = 128;
+constexpr uint32_t kPastEnd = 0x80000000u;   // buffer offset past every operand (< 2 GB): reads zero
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
 
@@ -195,6 +196,18 @@ __device__ __forceinline__ i32x4 buf_desc(const void* base, uint32_t bytes) {
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return (uint32_t)(uintptr_t)(lds_ptr_t)p;
 }
+// reads at LDS byte address addr (aligned to the size read)
+__device__ __forceinline__ uint4 lds_read16(uint32_t addr) {
+    const i32x4 v = *(__attribute__((address_space(3))) const i32x4*)(uintptr_t)addr;
+    return make_uint4((uint32_t)v[0], (uint32_t)v[1], (uint32_t)v[2], (uint32_t)v[3]);
+}
+__device__ __forceinline__ uint2 lds_read8(uint32_t addr) {
+    const i32x2 v = *(__attribute__((address_space(3))) const i32x2*)(uintptr_t)addr;
+    return make_uint2((uint32_t)v[0], (uint32_t)v[1]);
+}
+__device__ __forceinline__ uint16_t lds_read2(uint32_t addr) {
+    return *(__attribute__((address_space(3))) const uint16_t*)(uintptr_t)addr;
+}
 // An LDS DMA reads M0; after an SALU write of M0 it needs one wait state
 // (the compiler adds none inside inline assembly, hence the s_nop).  The
 // destination and the resource are wave-uniform; readfirstlane makes that
@@ -203,9 +216,21 @@ __device__ __forceinline__ i32x4 uniform4(const i32x4 d) {
     return i32x4{__builtin_amdgcn_readfirstlane(d[0]), __builtin_amdgcn_readfirstlane(d[1]),
                  __builtin_amdgcn_readfirstlane(d[2]), __builtin_amdgcn_readfirstlane(d[3])};
 }
-__device__ __forceinline__ void dma16(const i32x4 desc, uint32_t dst, uint32_t voff) {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+// Four 1 KB blocks at dst + 1024 k from voff + 1024 k (k = 0 .. 3): the
+// instruction's immediate offset moves both the memory and the LDS address.
+__device__ __forceinline__ void dma16x4(const i32x4 desc, uint32_t dst, uint32_t voff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\t"
+                 "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+                 "buffer_load_dwordx4 %1, %2, 0 offen offset:1024 lds\n\t"
+                 "buffer_load_dwordx4 %1, %2, 0 offen offset:2048 lds\n\t"
+                 "buffer_load_dwordx4 %1, %2, 0 offen offset:3072 lds"
                  :: "s"(__builtin_amdgcn_readfirstlane(dst)), "v"(voff), "s"(uniform4(desc)) : "memory", "m0");
+}
+// one 1 KB block with a scalar offset added to the memory address
+__device__ __forceinline__ void dma16s(const i32x4 desc, uint32_t dst, uint32_t voff, uint32_t soff) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(__builtin_amdgcn_readfirstlane(dst)), "v"(voff), "s"(uniform4(desc)),
+                    "s"(__builtin_amdgcn_readfirstlane(soff)) : "memory", "m0");
 }
 __device__ __forceinline__ void dma4(const i32x4 desc, uint32_t dst, uint32_t voff) {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
@@ -268,17 +293,25 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     using TS = TileShape<WMB, WAVES_N>;
     static_assert(TS::kThreads == 128 * WAVES_N && TS::kPerCU == (WAVES_N == 2 ? 2 : 1), "launch bounds");
     constexpr int WM = WMB, WN = 4;
-    constexpr int kRow = kGroupBytes;                       // 64 packed bytes per row per group
+    constexpr int kRow = kGroupBytes;                       // 64 bytes per row per group (W rows, X main plane)
     constexpr int kTile = kTB * kRow;                       // 8 KB: one 128-row tile
     constexpr int TM = TS::kTM, TN = TS::kTN, NBR = TS::kBlockRows, kWaves = TS::kWaves;
     constexpr int kCPerBR = WN / NBR;                       // a wave's sub-tiles per block row
     constexpr int kStages = 3;
     static_assert((NBR == 1 || NBR == 2) && kWaves == 4 * NBR, "one or two block rows, four waves per block row");
-    struct Slot {
-        uint8_t x[TM * kRow], w[TN * kRow], r[NBR][kTile];
-        uint32_t sw[TN / 2], sr[NBR][kTB / 2];              // fp16 scales, two per dword
+    // X, W and weight scales: three slots, loaded two groups ahead; residual
+    // tiles and their scales: two slots, loaded one group ahead (they are only
+    // read after the dense pass).  Arrays by kind, so that a read of a slot
+    // known at compile time is one lane address plus an immediate offset.
+    struct Ring {
+        uint8_t x[kStages][TM * kRow];                      // activation main plane, 16-byte chunks swizzled
+        uint8_t xt[kStages][4][TM * 8];                     // activation tail plane: [quarter][row]
+        uint8_t w[kStages][TN * kRow];
+        uint32_t sw[kStages][TN / 2];                       // fp16 scales, two per dword
+        uint8_t r[2][NBR][kTile];
+        uint32_t sr[2][NBR][kTB / 2];
     };
-    __shared__ __attribute__((aligned(16))) Slot ring[kStages];
+    __shared__ __attribute__((aligned(16))) Ring L;
 
     const int M = a.M, N = a.N, K = a.K;
     const int G = K / kGroup;
@@ -294,13 +327,16 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     const int gb = SPLIT ? blockIdx.y * groups_per_split : 0;
     const int ge = SPLIT ? min(G, gb + groups_per_split) : G;
 
-    // Operands in device group order: the group-g tile of X rows m0.. is
-    // xrows * 64 contiguous bytes at (g M + m0) 64, that of W rows n0.. TN * 64
-    // bytes at (g N + n0) 64, and R block p is 8 KB.  Every tile load goes
-    // through a resource spanning exactly that tile (offsets in the vector
-    // operand only), so X rows past xrows fail the range check and read zero.
+    // Operands in device group order: the group-g main-plane tile of X rows
+    // m0.. is xrows * 64 contiguous bytes at (g M + m0) 64, that of W rows
+    // n0.. TN * 64 bytes at (g N + n0) 64, and R block p is 8 KB.  These loads
+    // go through a resource spanning exactly that tile (offsets in the vector
+    // operand only), so X rows past xrows fail the range check and read zero;
+    // the tail-plane loads use the whole-operand resource with such rows moved
+    // past its end.
     const uint32_t xrows = (uint32_t)min(TM, M - m0);
     const uint32_t xbytes = xrows * (uint32_t)kRow;
+    const uint32_t tail0 = (uint32_t)G * (uint32_t)M * (uint32_t)kRow;
 
     // CSR walks of the tile's NBR block rows, from the first entry at or after
     // gb.  They read through the constant address space so they stay in scalar
@@ -326,45 +362,62 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     // everything; they are the ones that reach the group's barrier first (the
     // older waves win issue), so the issue cost lands where there is slack.
     // Loader ld fills the 1 KB blocks (16 rows each) 4 ld .. 4 ld + 3 of the X
-    // and W tiles, and of the residual tiles of the block rows flattened
-    // (block 8 br + j is block j of block row br), i.e. blocks
-    // 4 (ld & 1) .. + 3 of block row ld / 2, when that block row has a block
-    // at the group; and its scale share: loaders ld < NBR the weight scales of
-    // block row ld, loaders NBR .. 2 NBR - 1 the residual scales of block row
-    // ld - NBR (256 B each).  Lane l takes row 16 b + l / 4 and physical chunk
-    // l % 4, i.e. logical chunk (l % 4) ^ swz(row) of that row, so each load
-    // instruction reads 1 KB of whole 64-byte rows, contiguous.
+    // main-plane and W tiles, the tail-plane blocks 2 ld and 2 ld + 1 (block b:
+    // quarter b / (TM / 128), rows 128 (b % (TM / 128)) .., two rows a lane),
+    // and of the residual tiles of the block rows flattened (block 8 br + j is
+    // block j of block row br), i.e. blocks 4 (ld & 1) .. + 3 of block row
+    // ld / 2, when that block row has a block at the group; and its scale
+    // share: loaders ld < NBR the weight scales of block row ld, loaders
+    // NBR .. 2 NBR - 1 the residual scales of block row ld - NBR (256 B each).
+    // Lane l takes row 16 b + l / 4 and physical chunk l % 4, i.e. logical
+    // chunk (l % 4) ^ swz(row) of that row, so each load instruction reads
+    // 1 KB of whole 64-byte rows, contiguous.
     static_assert(TM == 64 * WAVES_N && TN == 64 * WAVES_N && 8 * NBR == 4 * WAVES_N,
                   "four X, W and R blocks per loader");
+    static_assert(TM / 32 == 2 * WAVES_N, "two tail-plane blocks per loader");
     const bool loader = wm == 0;
     const int ld = wn, lbr = ld >> 1;
-    uint32_t vt[4], vr[4];
+    // lane offsets of the first of the loader's four blocks (the swizzle of
+    // row 16 b + l / 4 is (l / 8) % 4 for every b, so block k is 1024 k on)
+    const uint32_t vt = (uint32_t)(64 * ld + (lane >> 2)) * kRow + (((lane & 3) ^ ((lane >> 3) & 3)) << 4);
+    const uint32_t vr = (uint32_t)(64 * (ld & 1) + (lane >> 2)) * kRow + (((lane & 3) ^ ((lane >> 3) & 3)) << 4);
+    // tail blocks: quarter tq[k], rows trow[k] + 2 l, 2 l + 1 (lane offsets
+    // past the end for rows from M on)
+    constexpr int kRowBlocks = TM / 128;                    // 128-row blocks of the tail tile per quarter
+    int tq[2], trow[2];
+    uint32_t vtl[2];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int row = 16 * (4 * ld + k) + (lane >> 2);
-        vt[k] = (uint32_t)row * kRow + (((lane & 3) ^ ((row >> 1) & 3)) << 4);
-        const int rrow = 16 * (4 * (ld & 1) + k) + (lane >> 2);
-        vr[k] = (uint32_t)rrow * kRow + (((lane & 3) ^ ((rrow >> 1) & 3)) << 4);
+    for (int k = 0; k < 2; ++k) {
+        const int b = 2 * ld + k;
+        tq[k] = b / kRowBlocks;
+        trow[k] = 128 * (b % kRowBlocks);
+        vtl[k] = (uint32_t)lane * 16u | (m0 + trow[k] + 2 * lane < M ? 0u : kPastEnd);
     }
 
     // Loads of group g into `slot` (issued by the loaders right after the
-    // barrier inside the dense pass of group g - 2; past the last group the X
-    // and W loads read nothing: zero-size resources).  p[b] is block row b's
-    // residual block at g (-1: none).
+    // barrier inside the dense pass of group g - 2; past the last group they
+    // read nothing: zero-size resources, offsets past the end).  p[b] is block
+    // row b's residual block at g (-1: none).
     struct Plan {
-        i32x4 xr, wr, rr, sc;                // resources
-        uint32_t x, w, r, s;                 // LDS destinations
-        bool has_r, has_s;
+        i32x4 xr, wr, sc;                    // resources
+        uint32_t x, w, s, xt[2];             // LDS destinations
+        uint32_t xto[2];                     // tail-plane block offsets (uniform; past the end: read nothing)
+        bool has_s;
     };
     auto plan = [&](int g, int slot, int (&p)[NBR]) -> Plan {
-        Slot& S = ring[slot];
         const bool live = g < ge;
         const int gl = live ? g : 0;
         Plan P;
         P.xr = buf_desc(a.Xq + piece_offset(M, m0, gl), live ? xbytes : 0u);
         P.wr = buf_desc(a.Wq + piece_offset(N, n0, gl), live ? (uint32_t)(TN * kRow) : 0u);
-        P.x = lds_addr(&S.x[(4 * ld) * 1024]);
-        P.w = lds_addr(&S.w[(4 * ld) * 1024]);
+        P.x = lds_addr(&L.x[slot][(4 * ld) * 1024]);
+        P.w = lds_addr(&L.w[slot][(4 * ld) * 1024]);
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+            P.xt[k] = lds_addr(&L.xt[slot][tq[k]][trow[k] * 8]);
+            P.xto[k] = live ? tail0 + (((uint32_t)gl * 4u + (uint32_t)tq[k]) * (uint32_t)M + (uint32_t)(m0 + trow[k])) * 8u
+                            : kPastEnd;
+        }
 #pragma unroll
         for (int b = 0; b < NBR; ++b) {
             p[b] = -1;
@@ -373,10 +426,6 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
                 nk[b] = rp[b] < re[b] ? res_kb[rp[b]] : 0x7fffffff;
             }
         }
-        const int pr = (NBR == 2 && lbr == 1) ? p[NBR - 1] : p[0];
-        P.has_r = pr >= 0;
-        P.rr = buf_desc(a.Rq + (int64_t)(pr >= 0 ? pr : 0) * kTile, (uint32_t)kTile);
-        P.r = lds_addr(&S.r[lbr][(4 * (ld & 1)) * 1024]);
         P.has_s = false;
         P.sc = buf_desc(a.Wq, 0u);
         P.s = 0;
@@ -384,14 +433,34 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
             if (live && ld < NBR) {
                 P.has_s = true;
                 P.sc = buf_desc(a.s_w + wscale_index(N, n0 + kTB * ld, g), kTB * 2);
-                P.s = lds_addr(&S.sw[64 * ld]);
+                P.s = lds_addr(&L.sw[slot][64 * ld]);
             }
+        }
+        return P;
+    };
+    // Residual loads of group g (blocks p) into residual slot rs, issued one
+    // group ahead.
+    struct RPlan {
+        i32x4 rr, sc;
+        uint32_t r, s;
+        bool has_r, has_s;
+    };
+    auto rplan = [&](int rs, const int (&p)[NBR]) -> RPlan {
+        RPlan P;
+        const int pr = (NBR == 2 && lbr == 1) ? p[NBR - 1] : p[0];
+        P.has_r = pr >= 0;
+        P.rr = buf_desc(a.Rq + (int64_t)(pr >= 0 ? pr : 0) * kTile, (uint32_t)kTile);
+        P.r = lds_addr(&L.r[rs][lbr][(4 * (ld & 1)) * 1024]);
+        P.has_s = false;
+        P.sc = buf_desc(a.Wq, 0u);
+        P.s = 0;
+        if constexpr (!RAW) {
             const int sb = ld - NBR;
             const int ps = (NBR == 2 && sb == 1) ? p[NBR - 1] : p[0];
             if (sb >= 0 && sb < NBR && ps >= 0) {
                 P.has_s = true;
                 P.sc = buf_desc(a.s_r + (int64_t)ps * kTB, kTB * 2);
-                P.s = lds_addr(S.sr[sb]);
+                P.s = lds_addr(L.sr[rs][sb]);
             }
         }
         return P;
@@ -399,14 +468,15 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     // the loads of a plan (loaders only; outside any MFMA block)
     auto issue = [&](const Plan& P) {
         if (!loader) return;
+        dma16x4(P.xr, P.x, vt);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) dma16(P.xr, P.x + 1024 * k, vt[k]);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) dma16(P.wr, P.w + 1024 * k, vt[k]);
-        if (P.has_r) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) dma16(P.rr, P.r + 1024 * k, vr[k]);
-        }
+        for (int k = 0; k < 2; ++k) dma16s(a.rx, P.xt[k], vtl[k], P.xto[k]);
+        dma16x4(P.wr, P.w, vt);
+        if (P.has_s) dma4(P.sc, P.s, (uint32_t)lane * 4);
+    };
+    auto issue_r = [&](const RPlan& P) {
+        if (!loader) return;
+        if (P.has_r) dma16x4(P.rr, P.r, vr);
         if (P.has_s) dma4(P.sc, P.s, (uint32_t)lane * 4);
     };
 
@@ -427,36 +497,68 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     // block keeps all the waves busy, not only those of its block row.
     const int wrow = 16 * WM * wm;
 
+    // LDS reads.  Every row and column this lane reads has the same swizzle
+    // (rows wrow + 16 i + lrow, columns 16 (wn + WAVES_N c) + lrow: (row / 2) % 4
+    // is (lrow / 2) % 4), so each read is a lane offset computed once plus a
+    // constant (slot, sub-tile row i, sub-tile column c).
+    // The lane offsets include the start of their array (each kept opaque to
+    // the compiler, so that the constant that remains is below the 64 KB of
+    // an LDS instruction's immediate offset).
+    const uint32_t swz_l = (uint32_t)(lq ^ ((lrow >> 1) & 3)) << 4;
+    auto lane_base = [](const void* array, uint32_t off) {
+        uint32_t v = lds_addr(array) + off;
+        asm volatile("" : "+v"(v));
+        return v;
+    };
+    const uint32_t xo = lane_base(L.x, (uint32_t)(wrow + lrow) * kRow + swz_l);                   // + 1024 i
+    const uint32_t to = lane_base(L.xt, (uint32_t)lq * (TM * 8) + (uint32_t)(wrow + lrow) * 8);   // + 128 i
+    const uint32_t wo = lane_base(L.w, (uint32_t)(16 * wn + lrow) * kRow + swz_l);      // + 1024 WAVES_N c
+    const uint32_t so = lane_base(L.sw, (uint32_t)(16 * wn + lrow) * 2);                // + 32 WAVES_N c
+    const uint32_t ro = lane_base(L.r, (uint32_t)(16 * wn + lrow) * kRow + swz_l);
+    const uint32_t sro = lane_base(L.sr, (uint32_t)(16 * wn + lrow) * 2);
+    // the activation operand of sub-tile row i: main-plane chunk and tail
+    auto a_main = [&](int slot, int i) { return lds_read16(xo + TM * kRow * slot + 1024 * i); };
+    auto a_tail = [&](int slot, int i) { return lds_read8(to + TM * 32 * slot + 128 * i); };
+    // a weight or residual scale as an fp32 register value (kept out of the
+    // fma, whose mixed-precision form measured slower)
+    auto scale_f32 = [](uint16_t bits) {
+        float v = half_bits_to_float(bits);
+        asm volatile("" : "+v"(v));
+        return v;
+    };
+
     // Operands of a group's dense pass that are read ahead, right after the
     // barrier that publishes the group (in the middle of the previous group's
     // dense pass): the wave's four W fragments (folded), their scales and its
     // first A fragment.  The pass then starts without waiting for LDS.
     struct Ahead {
         uint4 w[WN], a0;
-        float s[WN];
+        uint2 a0t;
+        uint16_t s[WN];
     };
-    auto read_ahead = [&](const Slot& S, Ahead& H) {
-        const uint16_t* sw16 = reinterpret_cast<const uint16_t*>(S.sw);
+    auto read_ahead = [&](int slot, Ahead& H) {
 #pragma unroll
         for (int c = 0; c < WN; ++c) {
-            const int col = 16 * (wn + WAVES_N * c) + lrow;
-            H.w[c] = *reinterpret_cast<const uint4*>(&S.w[col * kRow + (swz(col, lq) << 4)]);
-            H.s[c] = RAW ? 0.f : half_bits_to_float(sw16[col]) * kCodeScale;
+            H.w[c] = lds_read16(wo + TN * kRow * slot + 1024 * WAVES_N * c);
+            H.s[c] = RAW ? 0 : lds_read2(so + TN * 2 * slot + 32 * WAVES_N * c);
         }
-        const int row = wrow + lrow;
-        H.a0 = *reinterpret_cast<const uint4*>(&S.x[row * kRow + (swz(row, lq) << 4)]);
+        H.a0 = a_main(slot, 0);
+        H.a0t = a_tail(slot, 0);
     };
 
     // One pass over the staged group S.  The dense pass (RES == 0) multiplies
     // all four sub-tiles with the W fragments (from H) in two halves; between
     // them (a block boundary: the first half's epilogue is complete) it waits
-    // for the next group's loads, meets the other waves (which frees the slot
-    // of the previous group), has the loaders issue the loads of plan P and
-    // reads the next group's operands ahead into H.  A residual pass
+    // for the loads in flight, meets the other waves (which frees the slots of
+    // the previous group), has the loaders issue the loads of plans P and RP
+    // and reads the next group's operands ahead into H.  A residual pass
     // multiplies the sub-tiles in the bit set RES (those of one block row) with
-    // the R fragments of that block row.
+    // the R fragments of that block row from residual slot RS.  The fp32 path
+    // accumulates scale x (group sum / 64); the factor 64 is applied once, in
+    // the final epilogue (exact).
     constexpr int kSync = WM / 2;
-    auto phase = [&](const Slot& S, auto res_c, Ahead& H, const Slot& Snext, const Plan& P) {
+    auto phase = [&](auto slot_c, auto res_c, Ahead& H, int rs, const Plan& P, const RPlan& RP) {
+        constexpr int SL = decltype(slot_c)::value, SNEXT = SL == kStages - 1 ? 0 : SL + 1;
         constexpr int RES = decltype(res_c)::value;
         constexpr bool DENSE = RES == 0;
         constexpr int kBR = DENSE ? 0 : (RES >> kCPerBR ? 1 : 0);   // block row of a residual pass
@@ -468,24 +570,26 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
             if (!has(c)) continue;
             if constexpr (DENSE) {
                 b[c] = unfold_codes(H.w[c]);
-                bs[c] = H.s[c];
+                bs[c] = RAW ? 0.f : scale_f32(H.s[c]);
             } else {
-                const int row = 16 * (wn + WAVES_N * c) + lrow - kTB * kBR;   // row of the R tile
-                b[c] = unfold_codes(*reinterpret_cast<const uint4*>(&S.r[kBR][row * kRow + (swz(row, lq) << 4)]));
-                bs[c] = RAW ? 0.f : half_bits_to_float(reinterpret_cast<const uint16_t*>(S.sr[kBR])[row]) * kCodeScale;
+                // row 16 (wn + WAVES_N c) + lrow - 128 kBR of the block row's R tile
+                const int rc = 1024 * WAVES_N * c - kTile * kBR;
+                b[c] = unfold_codes(lds_read16(ro + (uint32_t)(rs * NBR * kTile) + kBR * kTile + rc));
+                bs[c] = RAW ? 0.f : scale_f32(lds_read2(sro + (uint32_t)(rs * NBR * kTB * 2) + kBR * kTB * 2 + rc / 32));
             }
         }
-        // Software pipeline over the sub-tile rows: the MFMAs of row i are
-        // issued before the epilogue of row i - 1, so each result is read
-        // several MFMAs after it was started (no wait states to fill).
+        // Software pipeline over the sub-tile rows: the activation operand of
+        // row i + 1 is read before the MFMAs of row i are issued, and those
+        // before the epilogue of row i - 1, so each result is read several
+        // MFMAs after it was started (no wait states to fill).
         f32x4 tq[2][WN];
-        auto mfma_row = [&](auto ic) {
+        auto a_row = [&](auto ic) -> i32x8 {
             constexpr int i = decltype(ic)::value;
-            const int row = wrow + 16 * i + lrow;
-            uint4 araw;
-            if constexpr (DENSE && i == 0) araw = H.a0;
-            else araw = *reinterpret_cast<const uint4*>(&S.x[row * kRow + (swz(row, lq) << 4)]);
-            const i32x8 av = unfold_codes(araw);
+            if constexpr (DENSE && i == 0) return act_operand(H.a0, H.a0t);
+            else return act_operand(a_main(SL, i), a_tail(SL, i));
+        };
+        auto mfma_row = [&](auto ic, const i32x8 av) {
+            constexpr int i = decltype(ic)::value;
 #pragma unroll
             for (int c = 0; c < WN; ++c)
                 if (has(c)) tq[i & 1][c] = mfma_codes(av, b[c], f32x4{0.f, 0.f, 0.f, 0.f});
@@ -507,10 +611,14 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         // inside the block (see pin)
         auto rows = [&](auto i0c, auto i1c) {
             constexpr int I0 = decltype(i0c)::value, I1 = decltype(i1c)::value;
+            i32x8 av = a_row(std::integral_constant<int, I0>{});
             static_for<I1 - I0>([&](auto jc) {
                 constexpr int i = I0 + decltype(jc)::value;
-                mfma_row(std::integral_constant<int, i>{});
+                i32x8 an = av;
+                if constexpr (i + 1 < I1) an = a_row(std::integral_constant<int, i + 1>{});
+                mfma_row(std::integral_constant<int, i>{}, av);
                 if constexpr (i > I0) epilogue_row(std::integral_constant<int, i - 1>{});
+                av = an;
             });
             epilogue_row(std::integral_constant<int, I1 - 1>{});
 #pragma unroll
@@ -525,59 +633,69 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         };
         if constexpr (DENSE) {
             rows(std::integral_constant<int, 0>{}, std::integral_constant<int, kSync>{});
-            wait_loads_and_sync();          // the only loads in flight are the next group's
+            wait_loads_and_sync();          // the only loads in flight are those issued one group ago
             issue(P);
-            read_ahead(Snext, H);
+            issue_r(RP);
+            read_ahead(SNEXT, H);
             rows(std::integral_constant<int, kSync>{}, std::integral_constant<int, WM>{});
         } else {
             rows(std::integral_constant<int, 0>{}, std::integral_constant<int, WM>{});
         }
     };
 
-    // residual blocks of the groups one and two ahead (-1: none), per block row
+    // residual blocks of the current group and of the groups one and two
+    // ahead (-1: none), per block row
     int p_cur[NBR], p_next[NBR], p_new[NBR];
     issue(plan(gb, 0, p_cur));
     issue(plan(gb + 1, 1, p_next));
+    issue_r(rplan(gb & 1, p_cur));
     constexpr int kBR0 = (1 << kCPerBR) - 1;                // sub-tiles of block row 0
-    wait_loads_and_sync();                                 // groups gb, gb + 1 landed
+    wait_loads_and_sync();                                 // groups gb, gb + 1 (residual: gb) landed
     Ahead H;
-    read_ahead(ring[0], H);
-    int slot = 0;
-    for (int g = gb; g < ge; ++g) {
-        // Group g's slot holds its operands (published by the barrier inside
-        // the previous dense pass) and H its dense pass's first operands.  The
-        // dense pass issues the loads of group g + 2 into the slot of group
-        // g - 1, which its barrier frees; then a residual pass per block row
-        // with a block at this group: every wave multiplies its kCPerBR
-        // sub-tiles of that block row.  (Passes rather than variants of the
-        // dense code: one code path per group keeps the accumulators in fixed
-        // registers.)
-        const int snext = slot == 2 ? 0 : slot + 1, sfree = snext == 2 ? 0 : snext + 1;
-        const Plan P = plan(g + 2, sfree, p_new);
-        const Slot& S = ring[slot];
-        phase(S, std::integral_constant<int, 0>{}, H, ring[snext], P);
-        if (p_cur[0] >= 0) phase(S, std::integral_constant<int, kBR0>{}, H, S, P);
+    read_ahead(0, H);
+    // Group g (ring slot SL, known at compile time: the loop below is unrolled
+    // three times) holds its operands (published by the barrier inside the
+    // previous dense pass), residual slot g & 1 its residual tiles, and H its
+    // dense pass's first operands.  The dense pass issues the loads of group
+    // g + 2 into the slot of group g - 1 and the residual loads of group g + 1
+    // into the residual slot of group g - 1, both freed by its barrier; then a
+    // residual pass per block row with a block at this group: every wave
+    // multiplies its kCPerBR sub-tiles of that block row.  (Passes rather than
+    // variants of the dense code: one code path per group keeps the
+    // accumulators in fixed registers.)
+    auto step = [&](auto slot_c, int g) {
+        constexpr int SL = decltype(slot_c)::value, SFREE = (SL + 2) % kStages;
+        const Plan P = plan(g + 2, SFREE, p_new);
+        const RPlan RP = rplan((g + 1) & 1, p_next);
+        const int rs = g & 1;
+        phase(slot_c, std::integral_constant<int, 0>{}, H, rs, P, RP);
+        if (p_cur[0] >= 0) phase(slot_c, std::integral_constant<int, kBR0>{}, H, rs, P, RP);
         if constexpr (NBR == 2)
-            if (p_cur[1] >= 0) phase(S, std::integral_constant<int, kBR0 << kCPerBR>{}, H, S, P);
+            if (p_cur[1] >= 0) phase(slot_c, std::integral_constant<int, kBR0 << kCPerBR>{}, H, rs, P, RP);
 #pragma unroll
         for (int b = 0; b < NBR; ++b) {
             p_cur[b] = p_next[b];
             p_next[b] = p_new[b];
         }
-        slot = snext;
+    };
+    for (int g = gb; g < ge; g += kStages) {
+        step(std::integral_constant<int, 0>{}, g);
+        if (g + 1 < ge) step(std::integral_constant<int, 1>{}, g + 1);
+        if (g + 2 < ge) step(std::integral_constant<int, 2>{}, g + 2);
     }
     // the X and W loads issued for the two groups past the end read nothing,
     // but they still write a ring slot: let them finish first
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
-    // epilogue: lane holds rows 4 * (lane / 16) + r of each sub-tile, column lane % 16
+    // epilogue: lane holds rows 4 * (lane / 16) + r of each sub-tile, column
+    // lane % 16; the fp32 sums are scale x (group sum / 64)
 #pragma unroll
     for (int i = 0; i < WM; ++i) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int m = m0 + wrow + 16 * i + 4 * lq + r;
             if (m >= M) continue;
-            const float sx = (RAW || SPLIT) ? 0.f : half_bits_to_float(a.s_x[m]);
+            const float sx = (RAW || SPLIT) ? 0.f : half_bits_to_float(a.s_x[m]) * kCodeScale;
 #pragma unroll
             for (int c = 0; c < WN; ++c) {
                 const int n = n0 + 16 * (wn + WAVES_N * c) + lrow;
@@ -589,7 +707,7 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
                     a.Tb[(int64_t)m * N + n] = iacc[i][c][r];
                     a.Tr[(int64_t)m * N + n] = racc[i][c][r];
                 } else if constexpr (SPLIT) {
-                    part[((int64_t)blockIdx.y * M + m) * N + n] = acc[i][c][r];
+                    part[((int64_t)blockIdx.y * M + m) * N + n] = acc[i][c][r] * kCodeScale;
                 } else {
                     a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(sx * acc[i][c][r]);
                 }
@@ -645,14 +763,13 @@ static int tiled_splits(int M, int N, int K) {
 // into LDS itself (same arithmetic as mq_quantize_act) instead of reading Xq.
 constexpr int kFusedMaxM = 4, kFusedCPT = 4;
 constexpr int kDecodeWaves = 8;
-constexpr uint32_t kPastEnd = 0x80000000u;   // buffer offset past every operand (< 2 GB): reads zero
 
 // Items in flight per wave: stages of WM X fragments, WN B fragments and WN
 // scales filling about 96 registers (measured: a deeper ring of the 64 x 64
 // medium tile, 144 registers, ran slower).
 template <int WM, int WN, bool RAW, bool A8 = false>
 struct StreamDepth {
-    static constexpr int kStageRegs = (A8 ? 12 : 4) * WM + 4 * WN + WN;
+    static constexpr int kStageRegs = (A8 ? 12 : 6) * WM + 4 * WN + WN;
     static constexpr int kBudget = 96;
     static constexpr int GD = kBudget / kStageRegs < 2 ? 2 : kBudget / kStageRegs > 6 ? 6 : kBudget / kStageRegs;
 };
@@ -662,6 +779,8 @@ struct StreamDepth {
 // a (16 WM WGM) x (16 WN WGN) output tile.  Decode: WM <= 2, WN = 1, 2 or 4
 // (all M <= 32 rows, K over eight waves); medium M: WM = 2 or 4, WN = 4 (the
 // whole 32 x 64 or 64 x 64 tile per wave, K over eight waves).
+// The W4A4 activation operand is read in its stored operand form (main-plane
+// chunk and tail), fused quantisation (FQ) unfolds its codes from LDS.
 // A8 (the W4A8 variant): the activation operand is INT8, stored as an e4m3
 // high plane and a folded 4-bit low plane (mq_quantize_act8); each product
 // takes the low-plane MFMA and the fp8 x fp6 MFMA of the high plane chained
@@ -673,6 +792,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     static_assert(!(FQ && RAW), "fused quantisation feeds the fp16 path");
     static_assert(!FQ || (WGM == 1 && WGN == 1), "fused quantisation: one tile of all rows");
     static_assert(!(FQ && A8), "fused quantisation is the W4A4 decode path");
+    constexpr bool A4 = !FQ && !A8;                              // activations in operand form
     constexpr int NW = kDecodeWaves, WG2 = WGM * WGN, KS = NW / WG2;
     static_assert(KS * WG2 == NW, "eight waves");
     constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
@@ -723,8 +843,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     const uint32_t loff = (uint32_t)lrow * kGroupBytes + (uint32_t)lq * 16;   // lane's bytes of a 16-row piece
 
     // X fragment of rows 16 i .. 16 i + 15 at group g: from the quantised rows
-    // in LDS (FQ; rows past M read 0) or from Xq (rows past M read other rows'
-    // bytes or zeros past the end: they only feed output rows never written)
+    // in LDS (FQ; rows past M read 0) or from Xq (rows past M read 0)
     auto x_offset = [&](int g, int i) -> uint32_t {
         return ((uint32_t)g * (uint32_t)M + (uint32_t)mw + 16u * i) * kGroupBytes + loff;
     };
@@ -762,16 +881,24 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     // residual blocks continue the pipeline without a bubble.
     struct Stage {
         uint4 x[WM], b[SPW];
+        uint2 xt[A4 ? WM : 1];                           // A4: the operand's tail dwords
         uint4 xh[A8 ? WM : 1][2];                        // A8: the e4m3 high plane (32 bytes)
         uint16_t sc[SPW];
         int g;
         bool res;
     };
-    // A8: the low plane follows the M K bytes of the high plane
+    // A8: the low plane follows the M K bytes of the high plane; A4: the tail
+    // plane follows the G M 64 bytes of the main plane
     const uint32_t lo_base = A8 ? (uint32_t)M * (uint32_t)K : 0u;
+    const uint32_t tail0 = (uint32_t)G * (uint32_t)M * (uint32_t)kGroupBytes;
     const int nitems = ng + ne;
     // group of the next residual entry to issue (scalar, loaded one entry ahead)
     int kb_next = (ne > 0) ? (int)res_kb[pb] : 0;
+    // activation rows from M on are read as zeros without touching memory
+    // (decode tiles are mostly such rows)
+    uint32_t xdead[WM];
+#pragma unroll
+    for (int i = 0; i < WM; ++i) xdead[i] = mw + 16 * i + lrow < M ? 0u : kPastEnd;
     auto load_item = [&](Stage& S, int j) {
         const bool live = j < nitems;
         // past the last item every offset gets bit 31: past every resource
@@ -789,14 +916,23 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         S.res = res;
         if constexpr (!FQ) {
 #pragma unroll
-            for (int i = 0; i < WM; ++i) S.x[i] = bload16(rx, (lo_base + x_offset(g, i)) | dead, 0);
+            for (int i = 0; i < WM; ++i) S.x[i] = bload16(rx, (lo_base + x_offset(g, i)) | dead | xdead[i], 0);
+        }
+        if constexpr (A4) {
+#pragma unroll
+            for (int i = 0; i < WM; ++i) {
+                const uint32_t to = tail0 + (((uint32_t)g * 4u + (uint32_t)lq) * (uint32_t)M +
+                                             (uint32_t)(mw + 16 * i + lrow)) * 8u;
+                const i32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rx, to | dead | xdead[i], 0, 0);
+                S.xt[i] = make_uint2((uint32_t)v[0], (uint32_t)v[1]);
+            }
         }
         if constexpr (A8) {
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
                 const uint32_t ho = ((uint32_t)g * (uint32_t)M + (uint32_t)(mw + 16 * i + lrow)) * 128u + (uint32_t)lq * 32u;
-                S.xh[i][0] = bload16(rx, ho | dead, 0);
-                S.xh[i][1] = bload16(rx, (ho + 16u) | dead, 0);
+                S.xh[i][0] = bload16(rx, ho | dead | xdead[i], 0);
+                S.xh[i][1] = bload16(rx, (ho + 16u) | dead | xdead[i], 0);
             }
         }
         // resources built from the selected base (a select of scalars, not of
@@ -822,7 +958,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         constexpr bool RES = decltype(res_c)::value;
         i32x8 av[WM], ah[A8 ? WM : 1];
 #pragma unroll
-        for (int i = 0; i < WM; ++i) av[i] = unfold_codes(FQ ? x_lds(S.g, i) : S.x[i]);
+        for (int i = 0; i < WM; ++i) {
+            if constexpr (A4) av[i] = act_operand(S.x[i], S.xt[i]);
+            else av[i] = unfold_codes(FQ ? x_lds(S.g, i) : S.x[i]);
+        }
         if constexpr (A8) {
 #pragma unroll
             for (int i = 0; i < WM; ++i)
@@ -832,7 +971,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
 #pragma unroll
         for (int s = 0; s < SPW; ++s) {
             const i32x8 bv = unfold_codes(S.b[s]);
-            const float sc = RAW ? 0.f : half_bits_to_float(S.sc[s]) * kCodeScale;
+            const float sc = RAW ? 0.f : half_bits_to_float(S.sc[s]);   // x 64: at the end
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
                 f32x4 t = mfma_codes(av[i], bv, f32x4{0.f, 0.f, 0.f, 0.f});
@@ -958,7 +1097,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
                 float sum = 0.f;
                 for (int k = 0; k < KS; ++k) sum += __uint_as_float(red[k * WG2 + wp][v][l]);
                 const uint16_t sxb = FQ ? sx_sh[m] : a.s_x[m];
-                a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * sum);
+                a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * kCodeScale * sum);
             }
         }
     }
@@ -1030,7 +1169,7 @@ static bool medium_preferred(int M, int N) {
 template <bool RAW>
 static mq_status operand_resources(GemmArgs& a, bool a8 = false) {
     const uint64_t G = (uint64_t)(a.K / kGroup);
-    const uint64_t sizes[5] = {G * a.M * kGroupBytes * (a8 ? 3 : 1), G * a.N * kGroupBytes,
+    const uint64_t sizes[5] = {G * a.M * (a8 ? 3 * kGroupBytes : kActGroupBytes), G * a.N * kGroupBytes,
                                (uint64_t)a.nnzb * kTB * kGroupBytes,
                                G * a.N * 2, (uint64_t)a.nnzb * kTB * 2};
     for (uint64_t b : sizes)
@@ -1271,7 +1410,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 extern "C" size_t mq_linear_workspace_size(int M, int N, int K) {
     if (M <= 0 || !mq_host::shape_ok(N, K) || fused_decode_ok(M, K)) return 0;
-    return align256(mq_fused_gemm_workspace_size(M, N, K)) + align256((size_t)M * (K / 2)) +
+    return align256(mq_fused_gemm_workspace_size(M, N, K)) + align256((size_t)M * (K / 4) * 3) +
            align256((size_t)2 * M);
 }
 
@@ -1305,7 +1444,7 @@ static mq_status linear_impl(int M, int N, int K, const void* X, int ldx,
     uint8_t* ws = static_cast<uint8_t*>(workspace);
     const size_t gws = mq_fused_gemm_workspace_size(M, N, K);
     uint8_t* Xq = ws + align256(gws);
-    void* sx = Xq + align256((size_t)M * (K / 2));
+    void* sx = Xq + align256((size_t)M * (K / 4) * 3);
     st = mq_quantize_act(X, M, K, ldx, Xq, sx, stream);
     if (st != MQ_OK) return st;
     return mq_fused_gemm(M, N, K, Xq, sx, Wq, s_w, res_rowptr, res_kb, nnzb, Rq, s_r, Y, ldy,

@@ -13,6 +13,7 @@ constexpr int kGroup = 128;       // weight group length along K == residual blo
 constexpr int kGroupBytes = 64;   // packed bytes of one group of one row
 constexpr int kQmax = 7;
 
+typedef int32_t i32x2 __attribute__((ext_vector_type(2)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -118,9 +119,9 @@ constexpr uint32_t kFoldB = 0x86186186u;   // bits 6e+3, 6e+4 inside word 1
 
 typedef int32_t i32x8 __attribute__((ext_vector_type(8)));
 
-// 16 codes -> one folded chunk (quantisers)
-__device__ __forceinline__ uint2 fold_codes(const int (&q)[16]) {
-    uint32_t o[3] = {0u, 0u, 0u};
+// 16 codes -> the 96-bit word (o0, o1, o2) of their 6-bit fields
+__device__ __forceinline__ void code_fields(const int (&q)[16], uint32_t (&o)[3]) {
+    o[0] = o[1] = o[2] = 0u;
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
         const uint32_t f = (q[e] < 0 ? 32u : 0u) | (uint32_t)(q[e] < 0 ? -q[e] : q[e]);
@@ -128,17 +129,28 @@ __device__ __forceinline__ uint2 fold_codes(const int (&q)[16]) {
         o[w] |= f << off;
         if (off > 26) o[w + 1] |= f >> (32 - off);
     }
+}
+
+// 16 codes -> one folded chunk (quantisers)
+__device__ __forceinline__ uint2 fold_codes(const int (&q)[16]) {
+    uint32_t o[3];
+    code_fields(q, o);
     return make_uint2(o[0] | (o[2] & kFoldA), o[1] | (o[2] & kFoldB));
 }
 
-// code e (0..15) of a folded chunk
-__device__ __forceinline__ int chunk_code(uint32_t p0, uint32_t p1, int e) {
-    const uint32_t o[3] = {p0 & ~kFoldA, p1 & ~kFoldB, (p0 & kFoldA) | (p1 & kFoldB)};
+// code e (0..15) of a 96-bit field word
+__device__ __forceinline__ int field_code(const uint32_t (&o)[3], int e) {
     const int bit = 6 * e, w = bit >> 5, off = bit & 31;
     uint32_t f = o[w] >> off;
     if (off > 26) f |= o[w + 1] << (32 - off);
     const int mag = (int)(f & 7u);
     return (f & 32u) ? -mag : mag;
+}
+
+// code e (0..15) of a folded chunk
+__device__ __forceinline__ int chunk_code(uint32_t p0, uint32_t p1, int e) {
+    const uint32_t o[3] = {p0 & ~kFoldA, p1 & ~kFoldB, (p0 & kFoldA) | (p1 & kFoldB)};
+    return field_code(o, e);
 }
 
 // 16 bytes = two chunks (32 codes) -> the six e2m3 dwords of one MFMA lane
@@ -200,8 +212,13 @@ __device__ __forceinline__ uint32_t code_field(uint32_t h16, float s, float inv_
     const uint32_t m = min((uint32_t)fabsf(q), (uint32_t)kQmax);
     return m | ((__float_as_uint(q) >> 31) << 5);
 }
-__device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, float s, float inv_s) {
-    if (s == 0.0f) return make_uint2(0u, 0u);
+// 16 fp16 -> the 96-bit word (o0, o1, o2) of their 6-bit code fields
+__device__ __forceinline__ void quant_fields(const uint4 v0, const uint4 v1, float s, float inv_s,
+                                             uint32_t& o0, uint32_t& o1, uint32_t& o2) {
+    if (s == 0.0f) {
+        o0 = o1 = o2 = 0u;
+        return;
+    }
     const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
     uint32_t f[16];
 #pragma unroll
@@ -209,9 +226,13 @@ __device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, flo
         f[2 * i] = code_field(w[i] & 0xFFFFu, s, inv_s);
         f[2 * i + 1] = code_field(w[i] >> 16, s, inv_s);
     }
-    const uint32_t o0 = f[0] | (f[1] << 6) | (f[2] << 12) | (f[3] << 18) | (f[4] << 24) | (f[5] << 30);
-    const uint32_t o1 = (f[5] >> 2) | (f[6] << 4) | (f[7] << 10) | (f[8] << 16) | (f[9] << 22) | (f[10] << 28);
-    const uint32_t o2 = (f[10] >> 4) | (f[11] << 2) | (f[12] << 8) | (f[13] << 14) | (f[14] << 20) | (f[15] << 26);
+    o0 = f[0] | (f[1] << 6) | (f[2] << 12) | (f[3] << 18) | (f[4] << 24) | (f[5] << 30);
+    o1 = (f[5] >> 2) | (f[6] << 4) | (f[7] << 10) | (f[8] << 16) | (f[9] << 22) | (f[10] << 28);
+    o2 = (f[10] >> 4) | (f[11] << 2) | (f[12] << 8) | (f[13] << 14) | (f[14] << 20) | (f[15] << 26);
+}
+__device__ __forceinline__ uint2 quant_chunk(const uint4 v0, const uint4 v1, float s, float inv_s) {
+    uint32_t o0, o1, o2;
+    quant_fields(v0, v1, s, inv_s, o0, o1, o2);
     return make_uint2(o0 | (o2 & kFoldA), o1 | (o2 & kFoldB));
 }
 
@@ -226,6 +247,28 @@ __device__ __forceinline__ int64_t piece_offset(int rows, int r, int g) {
 }
 __device__ __forceinline__ int64_t wscale_index(int N, int n, int g) {
     return (int64_t)g * N + n;
+}
+
+// ------------------------------------------------ activation operand order --
+// Activation codes (Xq of mq_quantize_act) are stored in the matrix
+// instruction's operand form, so the GEMMs read them with no bit work: the
+// 32 codes of quarter j (codes 32j .. 32j + 31 of a 128-code group) are one
+// 192-bit word of their 6-bit fields (code e at bit 6e, the fields of the
+// packed layout, not folded), six dwords d0 .. d5.  Main plane: d0 .. d3 of
+// quarter j of (row r, group g) at byte (g M + r) 64 + 16 j; tail plane, from
+// byte G M 64 on: d4, d5 at byte G M 64 + ((4 g + j) M + r) 8.  A 16-row piece
+// of the main plane is 1 KB contiguous, like the packed rows, and the tails
+// of consecutive rows for one quarter are consecutive.
+constexpr int kActGroupBytes = 96;   // bytes of one group of one row (64 main + 32 tail)
+__device__ __forceinline__ int64_t act_main_offset(int M, int r, int g) {
+    return ((int64_t)g * M + r) * 64;
+}
+__device__ __forceinline__ int64_t act_tail_offset(int M, int G, int r, int g, int j) {
+    return (int64_t)G * M * 64 + (((int64_t)g * 4 + j) * M + r) * 8;
+}
+// the operand of quarter j from its main (d0 .. d3) and tail (d4, d5) parts
+__device__ __forceinline__ i32x8 act_operand(const uint4 m, const uint2 t) {
+    return i32x8{(int)m.x, (int)m.y, (int)m.z, (int)m.w, (int)t.x, (int)t.y, 0, 0};
 }
 
 __device__ __forceinline__ uint4 ldg16(const uint8_t* p) {

@@ -3,9 +3,10 @@
 //
 // Canonical: one two's-complement code per nibble, two per byte, the even k
 // in the low nibble, rows of K/2 bytes in k order; weight scales [N][K/128].
-// Library: folded sign-magnitude chunks of 16 codes (the operand form of the
-// fp6 matrix instruction), packed rows (Xq, Wq) in group order, weight scales
-// [K/128][N]; residual blocks keep their [nnzb][128][64] order.
+// Library: weights (Wq, Rq) as folded sign-magnitude chunks of 16 codes,
+// packed rows of Wq in group order, weight scales [K/128][N], residual blocks
+// in their [nnzb][128][64] order; activations (Xq) in the fp6 matrix
+// instruction's operand form (act_main_offset / act_tail_offset).
 //
 // The paper fixes no bit layout (Section 4.2 fuses layout packing with
 // quantisation); these conversions let a caller that holds plain int4 codes
@@ -63,6 +64,53 @@ __global__ __launch_bounds__(256) void repack_rows_kernel(const uint8_t* __restr
         if (bad && n_invalid) atomicAdd(n_invalid, bad);
     } else {
         *reinterpret_cast<uint2*>(dst + canon) = chunk_to_nibbles(*reinterpret_cast<const uint2*>(src + lib));
+    }
+}
+
+// Activation rows: chunk c of row r (canonical bytes 8c of row r, stride ld)
+// <-> half c % 2 of quarter (c / 2) % 4 of group c / 8 in the operand layout
+// (dwords d0 .. d2 of the quarter for an even chunk, d3 and the tail d4, d5
+// for an odd one).
+template <bool TO_LIB>
+__global__ __launch_bounds__(256) void repack_act_kernel(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                                         int rows, int K, int ld, int32_t* __restrict__ n_invalid) {
+    const int cpr = K / 16, G = K / kGroup;
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (int64_t)rows * cpr) return;
+    const int r = (int)(idx / cpr), c = (int)(idx % cpr);
+    const int g = c >> 3, j = (c >> 1) & 3;
+    const int64_t canon = (int64_t)r * ld + 8 * c;
+    const int64_t main = act_main_offset(rows, r, g) + 16 * j;
+    const int64_t tail = act_tail_offset(rows, G, r, g, j);
+    if constexpr (TO_LIB) {
+        int q[16];
+        const int bad = nibbles_to_codes(*reinterpret_cast<const uint2*>(src + canon), q);
+        uint32_t o[3];
+        code_fields(q, o);
+        if ((c & 1) == 0) {
+            *reinterpret_cast<uint3*>(dst + main) = make_uint3(o[0], o[1], o[2]);
+        } else {
+            *reinterpret_cast<uint32_t*>(dst + main + 12) = o[0];
+            *reinterpret_cast<uint2*>(dst + tail) = make_uint2(o[1], o[2]);
+        }
+        if (bad && n_invalid) atomicAdd(n_invalid, bad);
+    } else {
+        uint32_t o[3];
+        if ((c & 1) == 0) {
+            const uint3 v = *reinterpret_cast<const uint3*>(src + main);
+            o[0] = v.x, o[1] = v.y, o[2] = v.z;
+        } else {
+            const uint2 t = *reinterpret_cast<const uint2*>(src + tail);
+            o[0] = *reinterpret_cast<const uint32_t*>(src + main + 12), o[1] = t.x, o[2] = t.y;
+        }
+        uint32_t lo = 0u, hi = 0u;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const uint32_t nib = (uint32_t)field_code(o, e) & 0xFu;
+            if (e < 8) lo |= nib << (4 * e);
+            else hi |= nib << (4 * (e - 8));
+        }
+        *reinterpret_cast<uint2*>(dst + canon) = make_uint2(lo, hi);
     }
 }
 
@@ -139,6 +187,16 @@ static mq_status rows_launch(const uint8_t* src, uint8_t* dst, int rows, int K, 
     return mq_host::launch_status();
 }
 
+template <bool TO_LIB>
+static mq_status act_launch(const uint8_t* src, uint8_t* dst, int rows, int K, int ld, int32_t* n_invalid,
+                            hipStream_t stream) {
+    const int64_t n = (int64_t)rows * (K / 16);
+    if (n == 0) return MQ_OK;
+    hipLaunchKernelGGL((repack_act_kernel<TO_LIB>), dim3(blocks_for(n)), dim3(256), 0, stream, src, dst, rows, K,
+                       ld, n_invalid);
+    return mq_host::launch_status();
+}
+
 static bool k_ok(int K) { return K >= 128 && K % 128 == 0 && K <= (1 << 20); }
 
 template <bool TO_LIB>
@@ -192,7 +250,7 @@ extern "C" mq_status mq_repack_act(int M, int K, const uint8_t* Xq_c, int ldq, u
     if (!Xq_c || !Xq) return MQ_ERR_INVALID_ARG;
     if (!mq_host::aligned(Xq_c, 8) || !mq_host::aligned(Xq, 16) || (n_invalid && !mq_host::aligned(n_invalid, 4)))
         return MQ_ERR_MISALIGNED;
-    return rows_launch<true, true>(Xq_c, Xq, M, K, ldq, n_invalid, stream);
+    return act_launch<true>(Xq_c, Xq, M, K, ldq, n_invalid, stream);
 }
 
 extern "C" mq_status mq_unpack_act(int M, int K, const uint8_t* Xq, uint8_t* Xq_c, int ldq, hipStream_t stream) {
@@ -201,7 +259,7 @@ extern "C" mq_status mq_unpack_act(int M, int K, const uint8_t* Xq, uint8_t* Xq_
     if (M == 0) return MQ_OK;
     if (!Xq_c || !Xq) return MQ_ERR_INVALID_ARG;
     if (!mq_host::aligned(Xq_c, 8) || !mq_host::aligned(Xq, 16)) return MQ_ERR_MISALIGNED;
-    return rows_launch<false, true>(Xq, Xq_c, M, K, ldq, nullptr, stream);
+    return act_launch<false>(Xq, Xq_c, M, K, ldq, nullptr, stream);
 }
 
 extern "C" mq_status mq_repack_act8(int M, int K, const int8_t* Xc, int ldq, uint8_t* Xq8, int32_t* n_invalid,

@@ -20,7 +20,7 @@ namespace mq {
 // memory), scales each block row's sums by s_r, and the splits are added
 // through LDS in split order.  WGMR = 1 for M <= 16, else 4.
 template <int WGMR>
-__global__ __launch_bounds__(512) void gemm_residual_kernel(int M, int N, const uint8_t* __restrict__ Xq,
+__global__ __launch_bounds__(512) void gemm_residual_kernel(int M, int N, int K, const uint8_t* __restrict__ Xq,
                                                             const int32_t* __restrict__ rowptr,
                                                             const int32_t* __restrict__ res_kb,
                                                             const uint8_t* __restrict__ Rq,
@@ -40,16 +40,22 @@ __global__ __launch_bounds__(512) void gemm_residual_kernel(int M, int N, const 
     const int pb = rp + split * per + min(split, extra);
     const int ne = per + (split < extra ? 1 : 0);
 
+    const int G = K / kGroup;
     struct Stage {
         uint4 x, r[8];
+        uint2 xt;
         uint16_t s[8];
     };
     auto load = [&](Stage& S, int e) {
         S.x = make_uint4(0u, 0u, 0u, 0u);
+        S.xt = make_uint2(0u, 0u);
         if (e >= ne) return;
         const int p = pb + e;
         const int g = res_kb[p];
-        if (xr < M) S.x = ldg16(Xq + piece_offset(M, xr, g) + 16 * lq);
+        if (xr < M) {
+            S.x = ldg16(Xq + act_main_offset(M, xr, g) + 16 * lq);
+            S.xt = *reinterpret_cast<const uint2*>(Xq + act_tail_offset(M, G, xr, g, lq));
+        }
         const uint8_t* rt = Rq + (int64_t)p * kGroup * kGroupBytes;
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
@@ -61,7 +67,7 @@ __global__ __launch_bounds__(512) void gemm_residual_kernel(int M, int N, const 
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
     auto compute = [&](const Stage& S) {
-        const i32x8 av = unfold_codes(S.x);
+        const i32x8 av = act_operand(S.x, S.xt);
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
             const f32x4 t = mfma_codes(av, unfold_codes(S.r[c]), f32x4{0.f, 0.f, 0.f, 0.f});
@@ -150,11 +156,11 @@ extern "C" mq_status mq_unfused_gemm(int M, int N, int K, const uint8_t* Xq, con
     // 2. sparse residual GEMM into P
     const int NB = N / kGroup;
     if (M <= 16)
-        hipLaunchKernelGGL((gemm_residual_kernel<1>), dim3(1u, (unsigned)NB), dim3(512), 0, stream, M, N, Xq,
+        hipLaunchKernelGGL((gemm_residual_kernel<1>), dim3(1u, (unsigned)NB), dim3(512), 0, stream, M, N, K, Xq,
                            res_rowptr, res_kb, Rq, static_cast<const uint16_t*>(s_r), P);
     else
         hipLaunchKernelGGL((gemm_residual_kernel<4>), dim3((unsigned)((M + 63) / 64), (unsigned)NB), dim3(512), 0,
-                           stream, M, N, Xq, res_rowptr, res_kb, Rq, static_cast<const uint16_t*>(s_r), P);
+                           stream, M, N, K, Xq, res_rowptr, res_kb, Rq, static_cast<const uint16_t*>(s_r), P);
     st = mq_host::launch_status();
     if (st != MQ_OK) return st;
     // 3. reduce-add

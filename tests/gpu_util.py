@@ -87,8 +87,8 @@ def orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r):
 
 
 def dev_x(tc, Xq):
-    """Row-major packed activations -> the library's group order on the GPU."""
-    return dev(tc, layout.block_rows(Xq, Xq.shape[1] * 2))
+    """Row-major packed activations -> the library's operand layout on the GPU."""
+    return dev(tc, layout.act6_from_packed(Xq, Xq.shape[1] * 2))
 
 
 def gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r):

@@ -50,7 +50,7 @@ def run_layer(tc, mq, orc, layer, M):
     X = layer.act(M)
     Xq, s_x = mq.quantize_act(dev(tc, X))
     Xq_ref, sx_ref = orc.quantize_act(X)
-    assert np.array_equal(orc.unblock_rows(host(Xq), layer.K), Xq_ref)
+    assert np.array_equal(orc.packed_from_act6(host(Xq), layer.K), Xq_ref)
     assert np.array_equal(half_bits(s_x), sx_ref)
     Y = mq.fused_gemm(Xq, s_x, pw)                    # the launch bench.py times (AUTO)
     Tb, Tr = mq.fused_gemm_acc_i32(Xq, pw)            # same kernel family, tiles and splits
@@ -186,7 +186,7 @@ def test_canonical_operands_parity(tc, mq, orc, M, N, K, nnzb):
     assert np.array_equal(orc.unblock_rows(host(pw.Wq), K), ref.Wq)
     assert np.array_equal(orc.unblock_scales(half_bits(pw.s_w)), ref.s_w)
     assert np.array_equal(host(pw.Rq), ref.Rq)
-    assert np.array_equal(orc.unblock_rows(host(Xq), K), Xq_fold)
+    assert np.array_equal(orc.packed_from_act6(host(Xq), K), Xq_fold)
     # inverse conversions
     Wq_c, s_w_c, Rq_c = mq.unpack_weights(pw)
     Xq_c = mq.unpack_act(Xq)

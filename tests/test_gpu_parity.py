@@ -43,7 +43,7 @@ def test_act_quant_parity(tc, mq, orc, M, K):
     Xq, s_x = mq.quantize_act(dev(tc, X))
     Xq_ref, sx_ref = orc.quantize_act(X)
     assert np.array_equal(half_bits(s_x), sx_ref)
-    assert np.array_equal(orc.unblock_rows(host(Xq), K), Xq_ref)
+    assert np.array_equal(orc.packed_from_act6(host(Xq), K), Xq_ref)
 
 
 def test_act_quant_exact_ties(tc, mq, orc):
@@ -70,7 +70,7 @@ def test_act_quant_exact_ties(tc, mq, orc):
     Xq, s_x = mq.quantize_act(dev(tc, X))
     Xq_ref, sx_ref = orc.quantize_act(X)
     assert np.array_equal(half_bits(s_x), sx_ref)
-    assert np.array_equal(orc.unblock_rows(host(Xq), 128), Xq_ref)
+    assert np.array_equal(orc.packed_from_act6(host(Xq), 128), Xq_ref)
 
 
 def test_act_quant_strided(tc, mq, orc):
@@ -78,14 +78,14 @@ def test_act_quant_strided(tc, mq, orc):
     Xbig = np.zeros((9, 1024), np.float16)
     Xbig[:, :640] = X
     Xd = dev(tc, Xbig)[:, :640]
-    Xq = tc.empty((9, 320), dtype=tc.uint8, device="cuda")
+    Xq = tc.empty((9, mq.act_bytes(640)), dtype=tc.uint8, device="cuda")
     s_x = tc.empty((9,), dtype=tc.float16, device="cuda")
     lib = mq.load()
     st = lib.mq_quantize_act(Xd.data_ptr(), 9, 640, 1024, Xq.data_ptr(), s_x.data_ptr(), None)
     tc.cuda.synchronize()
     assert st == 0
     Xq_ref, sx_ref = orc.quantize_act(X)
-    assert np.array_equal(orc.unblock_rows(host(Xq), 640), Xq_ref)
+    assert np.array_equal(orc.packed_from_act6(host(Xq), 640), Xq_ref)
     assert np.array_equal(half_bits(s_x), sx_ref)
 
 
@@ -369,7 +369,7 @@ def test_full_size_sampled(tc, mq, orc, name, M):
     Xd = dev(tc, X)
     Xq, s_x = mq.quantize_act(Xd)
     Xq_ref, sx_ref = orc.quantize_act(X)
-    assert np.array_equal(orc.unblock_rows(host(Xq), layer.K), Xq_ref)
+    assert np.array_equal(orc.packed_from_act6(host(Xq), layer.K), Xq_ref)
     assert np.array_equal(half_bits(s_x), sx_ref)
     rng = np.random.default_rng(M + layer.seed)
     ms, ns = _samples(M, layer.N, ref.rowptr, rng)
@@ -391,13 +391,13 @@ def test_graph_replay_matches_eager(tc, mq, orc):
     L = synth.workload("c1_1024")
     pw = mq.prepare_weight(dev(tc, L.weight()), L.nnzb)
     X = dev(tc, L.act(64))
-    Xq = tc.empty((64, L.K // 2), dtype=tc.uint8, device="cuda")
+    Xq = tc.empty((64, mq.act_bytes(L.K)), dtype=tc.uint8, device="cuda")
     s_x = tc.empty((64,), dtype=tc.float16, device="cuda")
     Y = tc.empty((64, L.N), dtype=tc.float16, device="cuda")
     Y_eager = mq.linear(X, pw).clone()
     Ys = tc.empty((16, L.N), dtype=tc.float16, device="cuda")
     Xs = X[:16].contiguous()
-    Xqs = tc.empty((16, L.K // 2), dtype=tc.uint8, device="cuda")
+    Xqs = tc.empty((16, mq.act_bytes(L.K)), dtype=tc.uint8, device="cuda")
     sxs = tc.empty((16,), dtype=tc.float16, device="cuda")
     Ys_eager = mq.linear(Xs, pw).clone()
 
