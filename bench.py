@@ -116,6 +116,17 @@ def algorithmic(M, N, K, nnzb):
     return ops, byts
 
 
+def cpu_model():
+    """The host CPU's model name (/proc/cpuinfo), or None."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def quant_bytes(M, K):
     return M * K * 2 + M * K / 2 + M * 2
 
@@ -693,7 +704,7 @@ def main():
             nsteps += 1
         cs = (time.perf_counter() - c0) / nsteps
         cpu = {"value": round(eff_ops / cs / 1e12, 6), "unit": "TOPS", "cores": oracle.num_threads(),
-               "kind": "oracle", "seconds_per_step": round(cs, 3), "steps": nsteps,
+               "cpu_model": cpu_model(), "kind": "oracle", "seconds_per_step": round(cs, 3), "steps": nsteps,
                "sample": f"{nsteps} full step(s) of the same workload (M={','.join(map(str, ms))}: "
                          "activation quantisation + int64 GEMM + fp64 epilogue), weight "
                          "preparation excluded"}

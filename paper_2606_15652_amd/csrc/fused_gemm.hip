@@ -58,6 +58,7 @@ struct GemmArgs {
     const uint16_t* X;       // fused-quantisation decode path: fp16 activations
     int ldx;
     int nnzb;
+    int rank_rows;           // tiled kernels: order block rows by residual count (one-round grids)
     // byte sizes of Xq, Wq, Rq, s_w, s_r (each below 2 GB) and buffer
     // resources spanning each whole operand (set by launch())
     uint32_t xq_bytes, wq_bytes, rq_bytes, sw_bytes, sr_bytes;
@@ -144,6 +145,7 @@ __device__ __forceinline__ void group_row(const i32x8 a, const i32x8 (&w)[WN], c
 // fp32 partial sums; reduce_splits_kernel adds them in split order
 // (deterministic) and applies s_x.
 constexpr int kTB = 128;
+constexpr int kRankMaxNB = 512;     // block rows the tiled kernel ranks by residual count
 constexpr uint32_t kPastEnd = 0x80000000u;   // buffer offset past every operand (< 2 GB): reads zero
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
@@ -310,6 +312,8 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         uint32_t sw[kStages][TN / 2];                       // fp16 scales, two per dword
         uint8_t r[2][NBR][kTile];
         uint32_t sr[2][NBR][kTB / 2];
+        int cnt[kRankMaxNB];                                // residual blocks per block row (ranking)
+        int sel[NBR];
     };
     __shared__ __attribute__((aligned(16))) Ring L;
 
@@ -323,13 +327,46 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     const int tiles_m = (M + TM - 1) / TM, tiles_n = N / TN;
     int tm, tn;
     tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * TM, n0 = tn * TN;
+    const int m0 = tm * TM;
     const int gb = SPLIT ? blockIdx.y * groups_per_split : 0;
     const int ge = SPLIT ? min(G, gb + groups_per_split) : G;
 
+    // The tile's block rows br[b] (128 output columns each).  Every tile
+    // takes all K groups, so its time is set by its residual blocks: tile
+    // column tn takes the block rows of rank tn (and, with two block rows, of
+    // rank NB - 1 - tn) in the order of decreasing residual-block count (ties:
+    // lower index first), which pairs the heaviest block row with the
+    // lightest, and gives the lowest tile columns -- the first workgroups
+    // dispatched -- the heaviest work.  Each workgroup ranks the block rows
+    // itself (NB <= kRankMaxNB), when the host asks for it: in grids that run
+    // in one round, where nothing else balances the tiles (in longer grids a
+    // workgroup that finishes early takes the next tile, and the ranking's
+    // cost would be paid by every workgroup).
+    const int NB = N / kTB;
+    int br[NBR];
+#pragma unroll
+    for (int b = 0; b < NBR; ++b) br[b] = tn * NBR + b;
+    if (a.rank_rows && a.rowptr && NB <= kRankMaxNB) {
+        for (int u = t; u < NB; u += TS::kThreads) L.cnt[u] = a.rowptr[u + 1] - a.rowptr[u];
+        __syncthreads();
+        for (int u = t; u < NB; u += TS::kThreads) {
+            const int c = L.cnt[u];
+            int rank = 0;
+            for (int v = 0; v < NB; ++v) {
+                const int cv = L.cnt[v];
+                rank += (cv > c) | ((cv == c) & (v < u));
+            }
+            if (rank == tn) L.sel[0] = u;
+            if (NBR == 2 && rank == NB - 1 - tn) L.sel[NBR - 1] = u;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int b = 0; b < NBR; ++b) br[b] = __builtin_amdgcn_readfirstlane(L.sel[b]);
+    }
+
     // Operands in device group order: the group-g main-plane tile of X rows
-    // m0.. is xrows * 64 contiguous bytes at (g M + m0) 64, that of W rows
-    // n0.. TN * 64 bytes at (g N + n0) 64, and R block p is 8 KB.  These loads
+    // m0.. is xrows * 64 contiguous bytes at (g M + m0) 64, that of block row
+    // br 8 KB at (g N + 128 br) 64, and R block p is 8 KB.  These loads
     // go through a resource spanning exactly that tile (offsets in the vector
     // operand only), so X rows past xrows fail the range check and read zero;
     // the tail-plane loads use the whole-operand resource with such rows moved
@@ -351,8 +388,8 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         nk[b] = 0x7fffffff;
         if (a.rowptr) {
             const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
-            rp[b] = rowptr[tn * NBR + b];
-            re[b] = rowptr[tn * NBR + b + 1];
+            rp[b] = rowptr[br[b]];
+            re[b] = rowptr[br[b] + 1];
             while (rp[b] < re[b] && res_kb[rp[b]] < gb) ++rp[b];
             if (rp[b] < re[b]) nk[b] = res_kb[rp[b]];
         }
@@ -409,7 +446,7 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         const int gl = live ? g : 0;
         Plan P;
         P.xr = buf_desc(a.Xq + piece_offset(M, m0, gl), live ? xbytes : 0u);
-        P.wr = buf_desc(a.Wq + piece_offset(N, n0, gl), live ? (uint32_t)(TN * kRow) : 0u);
+        P.wr = buf_desc(a.Wq + piece_offset(N, kTB * br[lbr], gl), live ? (uint32_t)kTile : 0u);
         P.x = lds_addr(&L.x[slot][(4 * ld) * 1024]);
         P.w = lds_addr(&L.w[slot][(4 * ld) * 1024]);
 #pragma unroll
@@ -432,7 +469,7 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         if constexpr (!RAW) {
             if (live && ld < NBR) {
                 P.has_s = true;
-                P.sc = buf_desc(a.s_w + wscale_index(N, n0 + kTB * ld, g), kTB * 2);
+                P.sc = buf_desc(a.s_w + wscale_index(N, kTB * br[ld], g), kTB * 2);
                 P.s = lds_addr(&L.sw[slot][64 * ld]);
             }
         }
@@ -471,7 +508,7 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         dma16x4(P.xr, P.x, vt);
 #pragma unroll
         for (int k = 0; k < 2; ++k) dma16s(a.rx, P.xt[k], vtl[k], P.xto[k]);
-        dma16x4(P.wr, P.w, vt);
+        dma16x4(P.wr, P.w, vr);                            // rows of block row lbr
         if (P.has_s) dma4(P.sc, P.s, (uint32_t)lane * 4);
     };
     auto issue_r = [&](const RPlan& P) {
@@ -647,10 +684,14 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     // ahead (-1: none), per block row
     int p_cur[NBR], p_next[NBR], p_new[NBR];
     issue(plan(gb, 0, p_cur));
-    issue(plan(gb + 1, 1, p_next));
     issue_r(rplan(gb & 1, p_cur));
+    const Plan P1 = plan(gb + 1, 1, p_next);
+    issue(P1);
     constexpr int kBR0 = (1 << kCPerBR) - 1;                // sub-tiles of block row 0
-    wait_loads_and_sync();                                 // groups gb, gb + 1 (residual: gb) landed
+    // group gb (and its residual tiles) have landed once no more than the
+    // loads of group gb + 1 (ten, plus its weight scales) are in flight; the
+    // barrier inside gb's dense pass waits for the rest
+    wait_vm_and_sync(loader ? 10 + (P1.has_s ? 1 : 0) : 0);
     Ahead H;
     read_ahead(0, H);
     // Group g (ring slot SL, known at compile time: the loop below is unrolled
@@ -698,7 +739,7 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
             const float sx = (RAW || SPLIT) ? 0.f : half_bits_to_float(a.s_x[m]) * kCodeScale;
 #pragma unroll
             for (int c = 0; c < WN; ++c) {
-                const int n = n0 + 16 * (wn + WAVES_N * c) + lrow;
+                const int n = kTB * br[c / kCPerBR] + ((16 * (wn + WAVES_N * c) + lrow) & (kTB - 1));
                 if constexpr (RAW && SPLIT) {
                     // integer sums of a group range: added in any order, exact
                     atomicAdd(&a.Tb[(int64_t)m * N + n], iacc[i][c][r]);
@@ -1215,6 +1256,7 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
         using TS = TileShape<8, 4>;
         const int64_t tiles = (int64_t)((a.M + TS::kTM - 1) / TS::kTM) * (a.N / TS::kTN);
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
+        a.rank_rows = tiles <= (int64_t)kCUs * TS::kPerCU;
         hipLaunchKernelGGL((gemm_tiled_kernel<8, 4, RAW, false>), dim3((unsigned)tiles), dim3(TS::kThreads), 0,
                            stream, a, 0, (float*)nullptr);
     } else if (variant == MQ_VARIANT_SKINNY) {
@@ -1224,6 +1266,7 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
         const int64_t tiles = (int64_t)((a.M + kTB - 1) / kTB) * (a.N / kTB);
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
         const int splits = tiled_splits(a.M, a.N, a.K);
+        a.rank_rows = tiles * splits <= (int64_t)kCUs * TileShape<4, 2>::kPerCU;
         if (splits == 1) {
             hipLaunchKernelGGL((gemm_tiled_kernel<4, 2, RAW, false>), dim3((unsigned)tiles),
                                dim3(TileShape<4, 2>::kThreads), 0, stream, a, 0, (float*)nullptr);
