@@ -826,7 +826,7 @@ struct StreamDepth {
 // high plane and a folded 4-bit low plane (mq_quantize_act8); each product
 // takes the low-plane MFMA and the fp8 x fp6 MFMA of the high plane chained
 // on its result (both exact), the rest is unchanged.
-template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false>
+template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false, bool XS = false>
 __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs a) {
     static_assert(WN * WGN == 1 || WN * WGN == 2 || WN * WGN == 4 || WN * WGN == 8,
                   "tile columns inside one block row");
@@ -834,6 +834,8 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     static_assert(!FQ || (WGM == 1 && WGN == 1), "fused quantisation: one tile of all rows");
     static_assert(!(FQ && A8), "fused quantisation is the W4A4 decode path");
     constexpr bool A4 = !FQ && !A8;                              // activations in operand form
+    static_assert(!XS || (A4 && WGM == 1 && WGN == 1), "staged activations: the W4A4 decode tile");
+    constexpr bool A4G = A4 && !XS;                              // ... read from memory per item
     constexpr int NW = kDecodeWaves, WG2 = WGM * WGN, KS = NW / WG2;
     static_assert(KS * WG2 == NW, "eight waves");
     constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
@@ -888,6 +890,20 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     auto x_offset = [&](int g, int i) -> uint32_t {
         return ((uint32_t)g * (uint32_t)M + (uint32_t)mw + 16u * i) * kGroupBytes + loff;
     };
+    // XS: the rows' operand bytes copied into LDS at the start, in the
+    // layout of Xq except that the 16-byte chunk q of a main-plane row r sits
+    // at chunk q ^ ((r / 4) % 4) (the 16 rows of a read then hit distinct
+    // banks); rows from M on read row M - 1 (their outputs are not written)
+    auto xs_main = [&](int g, int r, int q) -> uint32_t {
+        return ((uint32_t)g * (uint32_t)M + (uint32_t)r) * 64u + ((uint32_t)(q ^ ((r >> 2) & 3)) << 4);
+    };
+    auto x_staged = [&](int g, int i) -> i32x8 {
+        const int r = min(mw + 16 * i + lrow, M - 1);
+        const uint4 mv = *reinterpret_cast<const uint4*>(&xs[xs_main(g, r, lq)]);
+        const uint2 tv = *reinterpret_cast<const uint2*>(
+            &xs[(uint32_t)G * (uint32_t)M * 64u + (((uint32_t)g * 4u + (uint32_t)lq) * (uint32_t)M + (uint32_t)r) * 8u]);
+        return act_operand(mv, tv);
+    };
     auto x_lds = [&](int g, int i) -> uint4 {
         const int row = mw + 16 * i + lrow;
         uint4 v = make_uint4(0u, 0u, 0u, 0u);
@@ -922,7 +938,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     // residual blocks continue the pipeline without a bubble.
     struct Stage {
         uint4 x[WM], b[SPW];
-        uint2 xt[A4 ? WM : 1];                           // A4: the operand's tail dwords
+        uint2 xt[A4G ? WM : 1];                          // A4 from memory: the operand's tail dwords
         uint4 xh[A8 ? WM : 1][2];                        // A8: the e4m3 high plane (32 bytes)
         uint16_t sc[SPW];
         int g;
@@ -955,11 +971,11 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         }
         S.g = g;
         S.res = res;
-        if constexpr (!FQ) {
+        if constexpr (!FQ && !XS) {
 #pragma unroll
             for (int i = 0; i < WM; ++i) S.x[i] = bload16(rx, (lo_base + x_offset(g, i)) | dead | xdead[i], 0);
         }
-        if constexpr (A4) {
+        if constexpr (A4G) {
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
                 const uint32_t to = tail0 + (((uint32_t)g * 4u + (uint32_t)lq) * (uint32_t)M +
@@ -1000,7 +1016,8 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         i32x8 av[WM], ah[A8 ? WM : 1];
 #pragma unroll
         for (int i = 0; i < WM; ++i) {
-            if constexpr (A4) av[i] = act_operand(S.x[i], S.xt[i]);
+            if constexpr (XS) av[i] = x_staged(S.g, i);
+            else if constexpr (A4) av[i] = act_operand(S.x[i], S.xt[i]);
             else av[i] = unfold_codes(FQ ? x_lds(S.g, i) : S.x[i]);
         }
         if constexpr (A8) {
@@ -1048,6 +1065,19 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         }
     }
 
+    // XS, part 1: this thread's 16-byte chunks of Xq (up to kStageCPT),
+    // loaded ahead of the ring
+    constexpr int kStageCPT = 8;
+    const int nxs = (int)(a.xq_bytes / 16u);
+    uint4 xsv[XS ? kStageCPT : 1];
+    if constexpr (XS) {
+#pragma unroll
+        for (int k = 0; k < kStageCPT; ++k) {
+            const int idx = (int)threadIdx.x + k * 64 * NW;
+            xsv[k] = bload16(rx, idx < nxs ? (uint32_t)idx * 16u : kPastEnd, 0);
+        }
+    }
+
     // (the scheduling barriers keep each stage's loads together and the
     // stages in ring order, so the wait for a stage counts exactly the
     // stages issued after it)
@@ -1057,6 +1087,24 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         load_item(St[d], d);
         __builtin_amdgcn_sched_barrier(0);
     });
+
+    if constexpr (XS) {
+        // XS, part 2: the chunks into LDS (main-plane chunks swizzled)
+        const int nmain = G * M * 4;                       // main-plane chunks
+#pragma unroll
+        for (int k = 0; k < kStageCPT; ++k) {
+            const int idx = (int)threadIdx.x + k * 64 * NW;
+            if (idx < nxs) {
+                uint32_t dst = (uint32_t)idx * 16u;
+                if (idx < nmain) {
+                    const int q = idx & 3, gr = idx >> 2, g = gr / M, r = gr - g * M;
+                    dst = xs_main(g, r, q);
+                }
+                *reinterpret_cast<uint4*>(&xs[dst]) = xsv[k];
+            }
+        }
+        __syncthreads();
+    }
 
     if constexpr (FQ) {
         // FQ, part 2: row maxima across the workgroup (LDS atomic max on the
@@ -1162,15 +1210,29 @@ static int decode_spw(int M, int N) {
     return 1;
 }
 
-template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false>
+template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false, bool XS = false>
 static void launch_stream(const GemmArgs& a, size_t xs_bytes, hipStream_t stream) {
     const int64_t tiles = (int64_t)((a.M + 16 * WM * WGM - 1) / (16 * WM * WGM)) * (a.N / (16 * WN * WGN));
-    hipLaunchKernelGGL((gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ, A8>), dim3((unsigned)tiles),
+    hipLaunchKernelGGL((gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ, A8, XS>), dim3((unsigned)tiles),
                        dim3(64 * kDecodeWaves), xs_bytes, stream, a);
+}
+
+// Decode: the activation rows are copied into LDS once per workgroup when
+// they fit beside the partial-sum exchange (two workgroups a CU: 80 KB each;
+// at most 8 chunks of 16 bytes a thread), so the items load only weights.
+constexpr size_t kDecodeLdsBytes = 80 * 1024, kStageMaxBytes = 64 * 1024;
+static size_t staged_act_bytes(const GemmArgs& a, int wm, int spw) {
+    const size_t xb = (size_t)a.xq_bytes;
+    const size_t red = (size_t)kDecodeWaves * wm * spw * 4 * 64 * 4;
+    return (xb <= kStageMaxBytes && xb + red <= kDecodeLdsBytes) ? xb : 0;
 }
 
 template <int WM, int SPW, bool RAW, bool FQ>
 static void launch_decode_spw(const GemmArgs& a, size_t xs_bytes, hipStream_t stream) {
+    if constexpr (!FQ) {
+        const size_t xb = staged_act_bytes(a, WM, SPW);
+        if (xb > 0) return launch_stream<WM, SPW, 1, 1, RAW, false, false, true>(a, xb, stream);
+    }
     launch_stream<WM, SPW, 1, 1, RAW, FQ>(a, xs_bytes, stream);
 }
 
