@@ -46,7 +46,7 @@
  *   f_e above, unfolded, form the 192-bit word F = sum_e f_e 2^(6e), six
  *   little-endian 32-bit words d0..d5:
  *       d0..d3 at byte (g M + r) 64 + 16 j               (main plane),
- *       d4, d5 at byte G M 64 + ((4 g + j) M + r) 8       (tail plane).
+ *       d4, d5 at byte G M 64 + (g M + r) 32 + 8 j       (tail plane).
  *   The bits 6e+3, 6e+4 of every field must be zero (mq_quantize_act and
  *   mq_repack_act write them so); other patterns give unspecified outputs.
  * - Weight scales s_w are stored [K/128][N]: s_w of (row n, group g) at

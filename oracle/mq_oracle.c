@@ -243,13 +243,13 @@ void orc_unpack_codes(const uint8_t* packed, int rows, int K, int8_t* out)
 /* the 192-bit word F = sum_e f_e 2^(6e), six little-endian 32-bit words     */
 /* d0 .. d5.  With G = K / 128 groups and M rows:                            */
 /*   d0 .. d3 at byte (g M + r) 64 + 16 j          (main plane), and        */
-/*   d4, d5   at byte G M 64 + ((4 g + j) M + r) 8  (tail plane).            */
+/*   d4, d5   at byte G M 64 + (g M + r) 32 + 8 j   (tail plane).            */
 /* 3K/4 bytes per row.  The fields' exponent bits (6e+3, 6e+4) are zero.     */
 /* ------------------------------------------------------------------------ */
 static uint64_t act6_main(int M, int r, int g, int j) { return ((uint64_t)g * M + r) * 64 + 16 * (uint64_t)j; }
 static uint64_t act6_tail(int M, int G, int r, int g, int j)
 {
-    return (uint64_t)G * M * 64 + (((uint64_t)g * 4 + j) * M + r) * 8;
+    return (uint64_t)G * M * 64 + ((uint64_t)g * M + r) * 32 + 8 * (uint64_t)j;
 }
 
 void orc_pack_act6(const int8_t* q, int M, int K, uint8_t* out)

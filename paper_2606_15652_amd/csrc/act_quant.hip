@@ -11,7 +11,10 @@
 // rows), with the division-free exact rounding of quant_mag, and written in
 // the matrix instruction's operand form (act_main_offset / act_tail_offset):
 // the 16 codes of an even chunk are dwords d0 .. d2 of their quarter, those of
-// the odd chunk d3 (main plane) and d4, d5 (tail plane).
+// the odd chunk d3 .. d5.  The pair of threads of a quarter exchange d3, so
+// that the even thread writes the quarter's 16 main-plane bytes and the odd
+// one its 8 tail bytes (the quarters of a group are then 64 and 32 contiguous
+// bytes).
 #include "mq_device.h"
 
 namespace mq {
@@ -30,17 +33,16 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
     const uint16_t* row = X + (int64_t)m * ldx;
     const int nchunks = K / 16, G = K / 128;
     // chunk c (codes 16c .. 16c+15) is half c % 2 of quarter (c / 2) % 4 of group c / 8
+    // (both threads of a pair are active or neither: K / 16 is even)
     auto store = [&](int c, const uint4 v0, const uint4 v1, float s, float inv_s) {
         uint32_t o0, o1, o2;
         quant_fields(v0, v1, s, inv_s, o0, o1, o2);
+        const uint32_t d3 = __shfl_down(o0, 1, 64);          // the odd neighbour's o0
         const int g = c >> 3, j = (c >> 1) & 3;
-        uint8_t* main = Xq + act_main_offset(M, m, g) + 16 * j;
-        if ((c & 1) == 0) {
-            *reinterpret_cast<uint3*>(main) = make_uint3(o0, o1, o2);
-        } else {
-            *reinterpret_cast<uint32_t*>(main + 12) = o0;
+        if ((c & 1) == 0)
+            *reinterpret_cast<uint4*>(Xq + act_main_offset(M, m, g) + 16 * j) = make_uint4(o0, o1, o2, d3);
+        else
             *reinterpret_cast<uint2*>(Xq + act_tail_offset(M, G, m, g, j)) = make_uint2(o1, o2);
-        }
     };
 
     uint32_t amax = 0;

@@ -307,7 +307,7 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     // known at compile time is one lane address plus an immediate offset.
     struct Ring {
         uint8_t x[kStages][TM * kRow];                      // activation main plane, 16-byte chunks swizzled
-        uint8_t xt[kStages][4][TM * 8];                     // activation tail plane: [quarter][row]
+        uint8_t xt[kStages][2][TM * 16];                    // activation tail plane: [quarter pair][row]
         uint8_t w[kStages][TN * kRow];
         uint32_t sw[kStages][TN / 2];                       // fp16 scales, two per dword
         uint8_t r[2][NBR][kTile];
@@ -400,7 +400,8 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     // older waves win issue), so the issue cost lands where there is slack.
     // Loader ld fills the 1 KB blocks (16 rows each) 4 ld .. 4 ld + 3 of the X
     // main-plane and W tiles, the tail-plane blocks 2 ld and 2 ld + 1 (block b:
-    // quarter b / (TM / 128), rows 128 (b % (TM / 128)) .., two rows a lane),
+    // the 16 bytes of quarters 2 jp, 2 jp + 1 of rows 64 kb + l, jp = b / (TM / 64),
+    // kb = b % (TM / 64); in LDS the tail tile is [quarter pair][row]),
     // and of the residual tiles of the block rows flattened (block 8 br + j is
     // block j of block row br), i.e. blocks 4 (ld & 1) .. + 3 of block row
     // ld / 2, when that block row has a block at the group; and its scale
@@ -418,17 +419,17 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     // row 16 b + l / 4 is (l / 8) % 4 for every b, so block k is 1024 k on)
     const uint32_t vt = (uint32_t)(64 * ld + (lane >> 2)) * kRow + (((lane & 3) ^ ((lane >> 3) & 3)) << 4);
     const uint32_t vr = (uint32_t)(64 * (ld & 1) + (lane >> 2)) * kRow + (((lane & 3) ^ ((lane >> 3) & 3)) << 4);
-    // tail blocks: quarter tq[k], rows trow[k] + 2 l, 2 l + 1 (lane offsets
-    // past the end for rows from M on)
-    constexpr int kRowBlocks = TM / 128;                    // 128-row blocks of the tail tile per quarter
+    // tail blocks: quarter pair tq[k], rows trow[k] + l (lane offsets past the
+    // end for rows from M on)
+    constexpr int kRowBlocks = TM / 64;                     // 64-row blocks of the tail tile per quarter pair
     int tq[2], trow[2];
     uint32_t vtl[2];
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
         const int b = 2 * ld + k;
         tq[k] = b / kRowBlocks;
-        trow[k] = 128 * (b % kRowBlocks);
-        vtl[k] = (uint32_t)lane * 16u | (m0 + trow[k] + 2 * lane < M ? 0u : kPastEnd);
+        trow[k] = 64 * (b % kRowBlocks);
+        vtl[k] = ((uint32_t)(trow[k] + lane) * 32u + 16u * (uint32_t)tq[k]) | (m0 + trow[k] + lane < M ? 0u : kPastEnd);
     }
 
     // Loads of group g into `slot` (issued by the loaders right after the
@@ -451,9 +452,8 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         P.w = lds_addr(&L.w[slot][(4 * ld) * 1024]);
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
-            P.xt[k] = lds_addr(&L.xt[slot][tq[k]][trow[k] * 8]);
-            P.xto[k] = live ? tail0 + (((uint32_t)gl * 4u + (uint32_t)tq[k]) * (uint32_t)M + (uint32_t)(m0 + trow[k])) * 8u
-                            : kPastEnd;
+            P.xt[k] = lds_addr(&L.xt[slot][tq[k]][trow[k] * 16]);
+            P.xto[k] = live ? tail0 + ((uint32_t)gl * (uint32_t)M + (uint32_t)m0) * 32u : kPastEnd;
         }
 #pragma unroll
         for (int b = 0; b < NBR; ++b) {
@@ -548,14 +548,15 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
         return v;
     };
     const uint32_t xo = lane_base(L.x, (uint32_t)(wrow + lrow) * kRow + swz_l);                   // + 1024 i
-    const uint32_t to = lane_base(L.xt, (uint32_t)lq * (TM * 8) + (uint32_t)(wrow + lrow) * 8);   // + 128 i
+    const uint32_t to = lane_base(L.xt, (uint32_t)(lq >> 1) * (TM * 16) + (uint32_t)(wrow + lrow) * 16 +
+                                            (uint32_t)(lq & 1) * 8);                           // + 256 i
     const uint32_t wo = lane_base(L.w, (uint32_t)(16 * wn + lrow) * kRow + swz_l);      // + 1024 WAVES_N c
     const uint32_t so = lane_base(L.sw, (uint32_t)(16 * wn + lrow) * 2);                // + 32 WAVES_N c
     const uint32_t ro = lane_base(L.r, (uint32_t)(16 * wn + lrow) * kRow + swz_l);
     const uint32_t sro = lane_base(L.sr, (uint32_t)(16 * wn + lrow) * 2);
     // the activation operand of sub-tile row i: main-plane chunk and tail
     auto a_main = [&](int slot, int i) { return lds_read16(xo + TM * kRow * slot + 1024 * i); };
-    auto a_tail = [&](int slot, int i) { return lds_read8(to + TM * 32 * slot + 128 * i); };
+    auto a_tail = [&](int slot, int i) { return lds_read8(to + TM * 32 * slot + 256 * i); };
     // a weight or residual scale as an fp32 register value (kept out of the
     // fma, whose mixed-precision form measured slower)
     auto scale_f32 = [](uint16_t bits) {
@@ -901,7 +902,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         const int r = min(mw + 16 * i + lrow, M - 1);
         const uint4 mv = *reinterpret_cast<const uint4*>(&xs[xs_main(g, r, lq)]);
         const uint2 tv = *reinterpret_cast<const uint2*>(
-            &xs[(uint32_t)G * (uint32_t)M * 64u + (((uint32_t)g * 4u + (uint32_t)lq) * (uint32_t)M + (uint32_t)r) * 8u]);
+            &xs[(uint32_t)G * (uint32_t)M * 64u + ((uint32_t)g * (uint32_t)M + (uint32_t)r) * 32u + (uint32_t)lq * 8u]);
         return act_operand(mv, tv);
     };
     auto x_lds = [&](int g, int i) -> uint4 {
@@ -978,8 +979,8 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         if constexpr (A4G) {
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
-                const uint32_t to = tail0 + (((uint32_t)g * 4u + (uint32_t)lq) * (uint32_t)M +
-                                             (uint32_t)(mw + 16 * i + lrow)) * 8u;
+                const uint32_t to = tail0 + ((uint32_t)g * (uint32_t)M + (uint32_t)(mw + 16 * i + lrow)) * 32u +
+                                    (uint32_t)lq * 8u;
                 const i32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rx, to | dead | xdead[i], 0, 0);
                 S.xt[i] = make_uint2((uint32_t)v[0], (uint32_t)v[1]);
             }

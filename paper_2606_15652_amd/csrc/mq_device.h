@@ -256,15 +256,15 @@ __device__ __forceinline__ int64_t wscale_index(int N, int n, int g) {
 // 192-bit word of their 6-bit fields (code e at bit 6e, the fields of the
 // packed layout, not folded), six dwords d0 .. d5.  Main plane: d0 .. d3 of
 // quarter j of (row r, group g) at byte (g M + r) 64 + 16 j; tail plane, from
-// byte G M 64 on: d4, d5 at byte G M 64 + ((4 g + j) M + r) 8.  A 16-row piece
-// of the main plane is 1 KB contiguous, like the packed rows, and the tails
-// of consecutive rows for one quarter are consecutive.
+// byte G M 64 on: d4, d5 at byte G M 64 + (g M + r) 32 + 8 j.  A 16-row piece
+// of the main plane is 1 KB contiguous, like the packed rows, and so are the
+// tails of 32 rows.
 constexpr int kActGroupBytes = 96;   // bytes of one group of one row (64 main + 32 tail)
 __device__ __forceinline__ int64_t act_main_offset(int M, int r, int g) {
     return ((int64_t)g * M + r) * 64;
 }
 __device__ __forceinline__ int64_t act_tail_offset(int M, int G, int r, int g, int j) {
-    return (int64_t)G * M * 64 + (((int64_t)g * 4 + j) * M + r) * 8;
+    return (int64_t)G * M * 64 + ((int64_t)g * M + r) * 32 + 8 * j;
 }
 // the operand of quarter j from its main (d0 .. d3) and tail (d4, d5) parts
 __device__ __forceinline__ i32x8 act_operand(const uint4 m, const uint2 t) {

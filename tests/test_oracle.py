@@ -729,7 +729,7 @@ def test_act_operand_layout_matches_unfolded_chunks(orc):
         for _ in range(40):
             r, g, j = int(rng.integers(M)), int(rng.integers(G)), int(rng.integers(4))
             mo = (g * M + r) * 64 + 16 * j
-            to = G * M * 64 + ((4 * g + j) * M + r) * 8
+            to = G * M * 64 + (g * M + r) * 32 + 8 * j
             d = np.concatenate([dev[mo:mo + 16], dev[to:to + 8]]).view("<u4").astype(np.uint64)
             F = sum(int(d[w]) << (32 * w) for w in range(6))
             for h in range(2):
@@ -751,7 +751,7 @@ def test_act_operand_layout_counts_non_codes(orc):
     M, K = 2, 128
     dev = orc.pack_act6(np.zeros((M, K), np.int8)).reshape(-1).copy()
     dev[0] |= 0x08                      # bit 3 of field 0 (exponent) of row 0
-    dev[M * 64] |= 0x80                # tail plane, row 0, quarter 0: d4 bit 7 = F bit 135 (field 22, bit 3)
+    dev[M * 64] |= 0x80                # tail plane, row 0, group 0, quarter 0: d4 bit 7 = F bit 135 (field 22, bit 3)
     _, bad = orc.unpack_act6(dev, K)
     assert bad == 2
     with pytest.raises(ValueError):
