@@ -95,6 +95,9 @@ def parse():
                     help="residual block selection study (Section 3 Eq. (5), Fig. 2b): output-distortion "
                          "reduction C(S) of Delta-Hessian, residual-norm, weight-magnitude and random "
                          "selection (and exact greedy selection on the smallest layer) over block budgets")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("OUT_MD", "KERNEL_TRACE_CSV"),
+                    help="fold the kernel_trace.csv of a rocprofv3 --kernel-trace run of --kernel-run into "
+                         "per-spec launch durations (markdown, appended to OUT_MD; needs no GPU)")
     ap.add_argument("--traffic", action="store_true",
                     help="counter run: eager fused GEMM launches at the largest M, then a plain "
                          "256 MiB device copy as the scale reference for FETCH_SIZE / WRITE_SIZE")
@@ -224,6 +227,46 @@ def kernel_run(args):
                       "calls": TRAFFIC_CALLS}), flush=True)
 
 
+def summarize_trace(args):
+    """Per spec of a --kernel-run: the kernel, grid and average / min / max
+    duration of its GEMM launches (dispatches of gemm_* / reduce_* kernels in
+    dispatch order, args.calls per spec) from a rocprofv3 kernel trace."""
+    import csv
+    import statistics
+
+    out_md, path = args.summarize_trace
+    specs = parse_specs(args.kernel_run)
+    rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+    gemm = [r for r in rows if "gemm_" in r["Kernel_Name"] or "reduce_splits" in r["Kernel_Name"]]
+    runs, last = [], None
+    for r in gemm:
+        d = int(r["Dispatch_Id"])
+        if runs and last is not None and d == last + 1:
+            runs[-1].append(r)
+        else:
+            runs.append([r])
+        last = d
+    runs = [r for r in runs if len(r) >= args.calls]
+    if len(runs) != len(specs):
+        raise SystemExit(f"{path}: {len(runs)} GEMM dispatch runs for {len(specs)} specs")
+    lines = ["| spec | kernel | grid | launches | average µs | min µs | max µs | algorithmic ops / average |",
+             "|---|---|---|---|---|---|---|---|"]
+    for (name, m, variant), run in zip(specs, runs):
+        import synth
+        layer = synth.workload(name)
+        ops, _ = algorithmic(m, layer.N, layer.K, layer.nnzb)
+        per_launch = len(run) // args.calls
+        durs = [sum(int(x["End_Timestamp"]) - int(x["Start_Timestamp"]) for x in run[j:j + per_launch]) / 1e3
+                for j in range(0, per_launch * args.calls, per_launch)]
+        avg = statistics.mean(durs)
+        kname = run[0]["Kernel_Name"].split("(")[0].replace("void ", "")
+        lines.append(f"| {name} M={m} ({variant}) | `{kname}` | {run[0].get('Grid_Size_X', run[0].get('Grid_Size', ''))} | {len(durs)} | "
+                     f"{avg:.2f} | {min(durs):.2f} | {max(durs):.2f} | {ops / avg / 1e6:.0f} TOP/s |")
+    with open(out_md, "a") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def summarize_counters(args):
     """Per spec of a --kernel-run: the median per dispatch of every counter
     over its GEMM launches (dispatches of kernels named gemm_* / reduce_*,
@@ -269,8 +312,8 @@ def summarize_counters(args):
         for cname in disp[refd[0]]["c"]:
             ref[cname] = statistics.median(disp[d]["c"][cname] for d in refd)
     lines = ["| spec | kernel | matrix ops / launch (counter) | algorithmic ops | MFMA busy | "
-             "VALU per MFMA | LDS bank-conflict cycles / LDS instr | FETCH bytes | WRITE bytes | "
-             "DRAM read bytes | algorithmic bytes |", "|" + "---|" * 11]
+             "VALU beside MFMA | VALU per MFMA | wave cycles waiting | LDS bank-conflict cycles / LDS instr | "
+             "FETCH bytes | WRITE bytes | DRAM read bytes | algorithmic bytes |", "|" + "---|" * 13]
     for (name, m, variant), c in zip(specs, per):
         import synth
         layer = synth.workload(name)
@@ -284,6 +327,10 @@ def summarize_counters(args):
         if c.get("SQ_INSTS_MFMA"):
             vpm = (c.get("SQ_INSTS_VALU", 0.0) - c["SQ_INSTS_MFMA"]) / c["SQ_INSTS_MFMA"]
         lds = c["SQ_LDS_BANK_CONFLICT"] / c["SQ_INSTS_LDS"] if c.get("SQ_INSTS_LDS") else None
+        coexec = (c["SQ_VALU_MFMA_COEXEC_CYCLES"] / c["SQ_VALU_MFMA_BUSY_CYCLES"]
+                  if c.get("SQ_VALU_MFMA_BUSY_CYCLES") and "SQ_VALU_MFMA_COEXEC_CYCLES" in c else None)
+        wait = c["SQ_WAIT_ANY"] / c["SQ_WAVE_CYCLES"] if c.get("SQ_WAVE_CYCLES") and "SQ_WAIT_ANY" in c else None
+        pct = lambda x: "-" if x is None else f"{100 * x:.1f} %"
 
         def scaled(cn, ref_bytes):
             if cn in c and ref.get(cn):
@@ -294,7 +341,7 @@ def summarize_counters(args):
         dram = scaled("TCC_EA0_RDREQ_DRAM_sum", COPY_BYTES) or scaled("TCC_EA0_RDREQ_DRAM", COPY_BYTES)
         lines.append(f"| {name} M={m} ({variant}) | `{c['kernel']}` grid {c['grid']} | "
                      f"{f(None if mops is None else mops * 512)} | {f(ops)} | "
-                     f"{'-' if busy is None else f'{100 * busy:.1f} %'} | {f(vpm)} | {f(lds)} | "
+                     f"{pct(busy)} | {pct(coexec)} | {f(vpm)} | {pct(wait)} | {f(lds)} | "
                      f"{f(fetch)} | {f(write)} | {f(dram)} | {f(byts)} |")
     raw = ["", "Raw medians per launch (counter: value; reference kernel in the last column):", "",
            "| counter | " + " | ".join(f"{n} M={m}" for n, m, _ in specs) + " | reference |",
@@ -526,6 +573,9 @@ def main():
     args = parse()
     if args.summarize_counters:
         summarize_counters(args)
+        return
+    if args.summarize_trace:
+        summarize_trace(args)
         return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, m=max(int(x) for x in args.ms.split(",")))
