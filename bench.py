@@ -98,6 +98,9 @@ def parse():
     ap.add_argument("--summarize-trace", nargs=2, metavar=("OUT_MD", "KERNEL_TRACE_CSV"),
                     help="fold the kernel_trace.csv of a rocprofv3 --kernel-trace run of --kernel-run into "
                          "per-spec launch durations (markdown, appended to OUT_MD; needs no GPU)")
+    ap.add_argument("--summarize-families", nargs="+", metavar=("OUT_MD", "JSONL"),
+                    help="format the JSON lines of --families runs as a markdown table (appended to OUT_MD; "
+                         "needs no GPU)")
     ap.add_argument("--traffic", action="store_true",
                     help="counter run: eager fused GEMM launches at the largest M, then a plain "
                          "256 MiB device copy as the scale reference for FETCH_SIZE / WRITE_SIZE")
@@ -262,6 +265,30 @@ def summarize_trace(args):
         kname = run[0]["Kernel_Name"].split("(")[0].replace("void ", "")
         lines.append(f"| {name} M={m} ({variant}) | `{kname}` | {run[0].get('Grid_Size_X', run[0].get('Grid_Size', ''))} | {len(durs)} | "
                      f"{avg:.2f} | {min(durs):.2f} | {max(durs):.2f} | {ops / avg / 1e6:.0f} TOP/s |")
+    with open(out_md, "a") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def summarize_families(args):
+    """Markdown table of --families JSON lines (one row per layer and M)."""
+    out_md, paths = args.summarize_families[0], args.summarize_families[1:]
+    lines = ["| layer | K → N | M | ρ | nnzb | GEMM µs | layer call µs | eff. TOPS | int8 peak | HBM | "
+             "unfused µs | fused speed-up | W16A16 µs | call speed-up |", "|" + "---|" * 14]
+    for path in paths:
+        for line in open(path):
+            if not line.startswith("{"):
+                continue
+            d = json.loads(line)
+            rho = f"{d['density_pct']} %" + (" (skewed)" if d.get("skewed") else "")
+            unf = d.get("us_unfused")
+            fsu = "-" if unf is None else f"{unf / d['us_gemm']:.2f}×"
+            lines.append(
+                f"| {d['layer']} | {d['K']} → {d['N']} | {d['M']} | {rho} | {d['nnzb']} | {d['us_gemm']:.1f} | "
+                f"{d['us_call']:.1f} | {d['eff_tops']:.0f} | {100 * d['int8_peak_frac']:.1f} % | "
+                f"{100 * d['hbm_frac']:.1f} % | {'-' if unf is None else f'{unf:.1f}'} | "
+                f"{fsu} | {d['us_w16a16']:.1f} | "
+                f"{d['speedup_vs_w16a16']:.2f}× |")
     with open(out_md, "a") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -576,6 +603,9 @@ def main():
         return
     if args.summarize_trace:
         summarize_trace(args)
+        return
+    if args.summarize_families:
+        summarize_families(args)
         return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, m=max(int(x) for x in args.ms.split(",")))
