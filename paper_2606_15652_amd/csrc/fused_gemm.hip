@@ -585,8 +585,9 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     };
 
     // One pass over the staged group S.  The dense pass (RES == 0) multiplies
-    // all four sub-tiles with the W fragments (from H) in two halves; between
-    // them (a block boundary: the first half's epilogue is complete) it waits
+    // all four sub-tiles with the W fragments (from H); in the middle of it
+    // (MFMAs of the first half still running: the compiler places the wait
+    // states of their results across the blocks of the load issue) it waits
     // for the loads in flight, meets the other waves (which frees the slots of
     // the previous group), has the loaders issue the loads of plans P and RP
     // and reads the next group's operands ahead into H.  A residual pass
@@ -645,40 +646,48 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
                 }
             }
         };
-        // rows I0 .. I1 - 1, software-pipelined; their epilogue completes
-        // inside the block (see pin)
-        auto rows = [&](auto i0c, auto i1c) {
-            constexpr int I0 = decltype(i0c)::value, I1 = decltype(i1c)::value;
-            i32x8 av = a_row(std::integral_constant<int, I0>{});
-            static_for<I1 - I0>([&](auto jc) {
-                constexpr int i = I0 + decltype(jc)::value;
-                i32x8 an = av;
-                if constexpr (i + 1 < I1) an = a_row(std::integral_constant<int, i + 1>{});
-                mfma_row(std::integral_constant<int, i>{}, av);
-                if constexpr (i > I0) epilogue_row(std::integral_constant<int, i - 1>{});
-                av = an;
-            });
-            epilogue_row(std::integral_constant<int, I1 - 1>{});
+        // Rows 0 .. WM - 1, software-pipelined.  The dense pass meets the
+        // other waves after issuing the MFMAs of row kSync - 1 (its operand
+        // for row kSync already read: the current slot is not touched by the
+        // barrier), so those MFMAs run across the barrier, the loads and the
+        // reads ahead, and row kSync's MFMAs can issue right after them.
+        // Each row's sums are pinned right after its epilogue, which keeps
+        // that epilogue in place (the compiler would otherwise sink it past
+        // the barrier and the load issue).
+        auto pin_row = [&](int i) {
 #pragma unroll
-            for (int i = I0; i < I1; ++i)
-#pragma unroll
-                for (int c = 0; c < WN; ++c) {
-                    if (!has(c)) continue;
-                    if constexpr (!RAW) pin(acc[i][c]);
-                    else if constexpr (DENSE) pin(iacc[i][c]);
-                    else pin(racc[i][c]);
-                }
+            for (int c = 0; c < WN; ++c) {
+                if (!has(c)) continue;
+                if constexpr (!RAW) pin(acc[i][c]);
+                else if constexpr (DENSE) pin(iacc[i][c]);
+                else pin(racc[i][c]);
+            }
         };
-        if constexpr (DENSE) {
-            rows(std::integral_constant<int, 0>{}, std::integral_constant<int, kSync>{});
-            wait_loads_and_sync();          // the only loads in flight are those issued one group ago
-            issue(P);
-            issue_r(RP);
-            read_ahead(SNEXT, H);
-            rows(std::integral_constant<int, kSync>{}, std::integral_constant<int, WM>{});
-        } else {
-            rows(std::integral_constant<int, 0>{}, std::integral_constant<int, WM>{});
-        }
+        // The activation operand is read two rows ahead (one row of MFMAs
+        // and epilogue does not cover the LDS latency).
+        i32x8 av = a_row(std::integral_constant<int, 0>{});
+        i32x8 an = av;
+        if constexpr (WM > 1) an = a_row(std::integral_constant<int, 1>{});
+        static_for<WM>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            i32x8 ann = an;
+            if constexpr (i + 2 < WM) ann = a_row(std::integral_constant<int, i + 2>{});
+            mfma_row(std::integral_constant<int, i>{}, av);
+            if constexpr (i > 0) {
+                epilogue_row(std::integral_constant<int, i - 1>{});
+                pin_row(i - 1);
+            }
+            if constexpr (DENSE && i == kSync - 1) {
+                wait_loads_and_sync();      // the only loads in flight are those issued one group ago
+                issue(P);
+                issue_r(RP);
+                read_ahead(SNEXT, H);
+            }
+            av = an;
+            an = ann;
+        });
+        epilogue_row(std::integral_constant<int, WM - 1>{});
+        pin_row(WM - 1);
     };
 
     // residual blocks of the current group and of the groups one and two
