@@ -1,11 +1,14 @@
 """Code generation checks on the gfx950 assembly of libmq (no GPU needed).
 
-MFMA results must only be read inside the basic block of the MFMA that wrote
-them: the compiler places the wait states a VALU read of an MFMA result needs
-reliably within a block, but a read in a successor block right after a
-branch has been observed to miss them (stale accumulator values).  The kernels
-are written so that every group's MFMA results are converted in the block
-that produced them; this test keeps it that way.
+A VALU read (or overwrite) of an MFMA result needs wait states after the MFMA:
+8 for the fp6 x fp6 f8f6f4 MFMA, 12 when an operand is fp8 (the counts the
+compiler itself inserts before such a read in the MFMA's own block).  A read in
+a successor block right after a branch has been observed to miss them once
+(stale accumulator values), so this test checks every read of an MFMA result
+that is reached across a block boundary (a label or a branch): on every path
+of the control-flow graph it must come at least that many wait states after
+the MFMA (each instruction is one wait state, s_nop n is n + 1).  Reads inside
+the MFMA's own block are left to the compiler.
 """
 import os
 import re
@@ -62,35 +65,114 @@ def kernels_asm():
     return out
 
 
-def mfma_escapes(lines):
-    """(line index, registers) of MFMA results not consumed in their block."""
-    bad = []
+def required_wait_states(ops):
+    """Wait states before a VALU touches the result of this f8f6f4 MFMA."""
+    mods = " ".join(ops)
+    cbsz = re.search(r"cbsz:(\d)", mods)
+    blgp = re.search(r"blgp:(\d)", mods)
+    fp6_or_fp4 = lambda m: m is not None and int(m.group(1)) >= 2
+    return 8 if fp6_or_fp4(cbsz) and fp6_or_fp4(blgp) else 12
+
+
+def _parse(lines):
+    """Instructions as (op, operands); labels as ("LABEL", name)."""
     insts = []
     for ln in lines:
         s = ln.strip()
-        if not s or s.startswith(";") or s.startswith("."):
-            if re.match(r"^\.LBB\S*:", s):
-                insts.append(("LABEL", []))
+        if not s or s.startswith(";"):
+            continue
+        m = re.match(r"^(\.LBB\S*):", s)
+        if m:
+            insts.append(("LABEL", m.group(1)))
+            continue
+        if s.startswith("."):
             continue
         insts.append(split_operands(s))
+    return insts
+
+
+def _successors(insts):
+    where = {ops: i for i, (op, ops) in enumerate(insts) if op == "LABEL"}
+    succ = []
+    for i, (op, ops) in enumerate(insts):
+        if op == "s_branch":
+            succ.append([where[ops[0]]])
+        elif op.startswith("s_cbranch"):
+            succ.append([i + 1, where[ops[0]]])
+        elif op.startswith(("s_endpgm", "s_setpc", "s_trap")):
+            succ.append([])
+        else:
+            succ.append([i + 1] if i + 1 < len(insts) else [])
+    return succ
+
+
+def _touches(op, ops, pending):
+    """Registers of `pending` that the instruction reads or writes."""
+    if op == "LABEL" or not ops:
+        return set()
+    if op.startswith(_ALL_READ):
+        return pending & regs(",".join(ops))
+    return pending & (regs(",".join(ops[1:])) | regs(ops[0]))
+
+
+def _cost(op, ops):
+    if op == "LABEL":
+        return 0
+    if op == "s_nop":
+        return int(ops[0], 0) + 1
+    return 1
+
+
+def mfma_escapes(lines):
+    """(instruction index, registers, wait states) of MFMA results first
+    touched across a block boundary fewer than the required wait states after
+    the MFMA, on some path."""
+    import heapq
+    insts = _parse(lines)
+    succ = _successors(insts)
+    bad = []
     for i, (op, ops) in enumerate(insts):
         if not op.startswith("v_mfma"):
             continue
         pending = regs(ops[0])
-        for op2, ops2 in insts[i + 1:]:
-            if op2 == "LABEL" or op2.startswith(_BRANCH):
+        need = required_wait_states(ops)
+        # straight-line part of the block: the compiler's wait states hold
+        j = i + 1
+        crossed_at = None
+        while j < len(insts):
+            op2, ops2 = insts[j]
+            if op2 == "LABEL":
+                crossed_at = j
                 break
-            if op2.startswith(_ALL_READ):
-                pending -= regs(",".join(ops2))
-                continue
-            srcs = regs(",".join(ops2[1:])) if ops2 else set()
-            dst = regs(ops2[0]) if ops2 else set()
-            pending -= srcs
-            pending -= dst
+            pending -= _touches(op2, ops2, pending)
             if not pending:
                 break
-        if pending:
-            bad.append((i, sorted(pending)))
+            if op2.startswith(_BRANCH):
+                crossed_at = j
+                break
+            j += 1
+        if not pending or crossed_at is None:
+            continue
+        # every path from the block boundary on: shortest distance to the
+        # first instruction touching a pending register
+        dist0 = sum(_cost(*insts[k]) for k in range(i + 1, crossed_at + 1))
+        starts = [crossed_at] if insts[crossed_at][0] == "LABEL" else succ[crossed_at]
+        best = {}
+        heap = [(dist0 + (0 if insts[crossed_at][0] == "LABEL" else 0), k) for k in starts]
+        heapq.heapify(heap)
+        while heap:
+            d, k = heapq.heappop(heap)
+            if k in best and best[k] <= d:
+                continue
+            best[k] = d
+            op2, ops2 = insts[k]
+            hit = _touches(op2, ops2, pending)
+            if hit:
+                if d < need:
+                    bad.append((i, sorted(hit), d))
+                continue
+            for n in succ[k]:
+                heapq.heappush(heap, (d + _cost(op2, ops2), n))
     return bad
 
 
@@ -106,10 +188,22 @@ def test_gemm_kernels_have_mfma(asm):
         assert any("v_mfma_f32_16x16x128_f8f6f4" in l for l in asm[k]), k
 
 
-def test_mfma_results_consumed_in_block(asm):
+def test_mfma_results_read_across_blocks_are_far(asm):
     problems = {k: mfma_escapes(v) for k, v in asm.items() if "gemm" in k}
     problems = {k: v for k, v in problems.items() if v}
-    assert not problems, f"MFMA results read outside their block: {problems}"
+    assert not problems, f"MFMA results read across a block boundary too soon: {problems}"
+
+
+def test_escape_check_sees_a_near_read():
+    # a read right after a branch join, one wait state after the MFMA on the taken path
+    lines = ["v_mfma_f32_16x16x128_f8f6f4 v[0:3], v[4:9], v[10:15], 0 cbsz:2 blgp:2",
+             "s_cbranch_scc1 .LBB0_1", "v_mov_b32 v20, 1", ".LBB0_1:",
+             "v_add_f32 v21, v0, v1", "s_endpgm"]
+    assert [b[1] for b in mfma_escapes(lines)] == [["v0", "v1"]]
+    far = lines[:1] + ["s_nop 6"] + lines[1:]     # 8 on the taken path
+    assert mfma_escapes(far) == []
+    fp8 = [lines[0].replace(" cbsz:2 blgp:2", "")] + far[1:]
+    assert [b[1] for b in mfma_escapes(fp8)] == [["v0", "v1"]]
 
 
 def test_no_packed_fp32_instructions(asm):
