@@ -815,12 +815,12 @@ static int tiled_splits(int M, int N, int K) {
 constexpr int kFusedMaxM = 4, kFusedCPT = 4;
 constexpr int kDecodeWaves = 8;
 
-// Items in flight per wave: stages of WM X fragments, WN B fragments and WN
-// scales filling about 96 registers (measured: a deeper ring of the 64 x 64
+// Items in flight per wave: stages of WM X fragments, WN B fragments and
+// their scales filling about 96 registers (measured: a deeper ring of the 64 x 64
 // medium tile, 144 registers, ran slower).
 template <int WM, int WN, bool RAW, bool A8 = false>
 struct StreamDepth {
-    static constexpr int kStageRegs = (A8 ? 12 : 6) * WM + 4 * WN + WN;
+    static constexpr int kStageRegs = (A8 ? 12 : 6) * WM + 4 * WN + (WN == 4 ? 1 : WN);
     static constexpr int kBudget = 96;
     static constexpr int GD = kBudget / kStageRegs < 2 ? 2 : kBudget / kStageRegs > 6 ? 6 : kBudget / kStageRegs;
 };
@@ -851,6 +851,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
     constexpr int SPW = WN;
     constexpr int GD = StreamDepth<WM, WN, RAW, A8>::GD;
+    constexpr bool kScaleShfl = SPW == 4;
     constexpr int kAcc = WM * SPW * 4;                           // sums per lane and accumulator
     // cross-wave partial sums red[wave][value][lane] (one accumulator per
     // round: raw mode adds the base and then the residual sums); FQ: packed
@@ -950,7 +951,9 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         uint4 x[WM], b[SPW];
         uint2 xt[A4G ? WM : 1];                          // A4 from memory: the operand's tail dwords
         uint4 xh[A8 ? WM : 1][2];                        // A8: the e4m3 high plane (32 bytes)
-        uint16_t sc[SPW];
+        // scales: four strips, one load (lane l: column row0 + l, handed out by
+        // shuffles); fewer, one load per strip (column row0 + 16 s + lrow)
+        uint16_t sc[kScaleShfl ? 1 : SPW];
         int g;
         bool res;
     };
@@ -1016,9 +1019,14 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
             const bool use_sr = res && a.s_r != nullptr;
             const __amdgpu_buffer_rsrc_t rs =
                 make_rsrc(use_sr ? (const void*)a.s_r : (const void*)a.s_w, use_sr ? a.sr_bytes : a.sw_bytes);
+            if constexpr (kScaleShfl) {
+                S.sc[0] = __builtin_amdgcn_raw_buffer_load_b16(rs, ((row0 + (uint32_t)lane) * 2u) | dead, 0, 0);
+            } else {
 #pragma unroll
-            for (int s = 0; s < SPW; ++s)
-                S.sc[s] = __builtin_amdgcn_raw_buffer_load_b16(rs, ((row0 + 16u * s + (uint32_t)lrow) * 2u) | dead, 0, 0);
+                for (int s = 0; s < SPW; ++s)
+                    S.sc[s] = __builtin_amdgcn_raw_buffer_load_b16(rs, ((row0 + 16u * s + (uint32_t)lrow) * 2u) | dead,
+                                                                   0, 0);
+            }
         }
     };
     auto compute_item = [&](const Stage& S, auto res_c) {
@@ -1039,7 +1047,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
 #pragma unroll
         for (int s = 0; s < SPW; ++s) {
             const i32x8 bv = unfold_codes(S.b[s]);
-            const float sc = RAW ? 0.f : half_bits_to_float(S.sc[s]);   // x 64: at the end
+            // column 16 s + lrow's scale (x 64: at the end)
+            uint16_t sb = 0;
+            if constexpr (!RAW) sb = kScaleShfl ? (uint16_t)__shfl((int)S.sc[0], 16 * s + lrow, 64) : S.sc[s];
+            const float sc = RAW ? 0.f : half_bits_to_float(sb);
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
                 f32x4 t = mfma_codes(av[i], bv, f32x4{0.f, 0.f, 0.f, 0.f});
