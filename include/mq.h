@@ -96,8 +96,9 @@ typedef enum mq_variant {
     MQ_VARIANT_SKINNY = 1,   /* decode: split-K over the waves of a workgroup  */
     MQ_VARIANT_TILED = 2,    /* prefill: 128 x 128 output tiles, K-loop of groups */
     MQ_VARIANT_TILED_LARGE = 3, /* prefill: 256 x 256 output tiles (N % 256 == 0,
-                                   else as TILED); AUTO takes it when every CU
-                                   gets at least one tile                    */
+                                   else as TILED); AUTO takes it when
+                                   128 x 128 tiles would need more than one
+                                   round of two per CU                       */
     MQ_VARIANT_MEDIUM = 4       /* 32 or 64 x 64 output tiles; AUTO takes it
                                    when 128 x 128 tiles would be too few to
                                    fill the chip                             */

@@ -1264,11 +1264,22 @@ static void launch_decode(const GemmArgs& a, int spw, size_t xs_bytes, hipStream
     launch_decode_spw<WM, 1, RAW, FQ>(a, xs_bytes, stream);
 }
 
-// The 256 x 256 tile is used when every CU gets at least one tile; smaller
-// problems keep the 128 x 128 tile (and split-K when even those are few).
-constexpr int kLargeTileMinTiles = 256;
+// 256 x 256 or 128 x 128 tiles, by the estimated number of rounds: the large
+// tile runs one workgroup per CU, the 128 x 128 tile two, and a round of the
+// latter measured about 0.66 of a round of the former (for a quarter of the
+// work: 4096 -> 14336, 14336 -> 4096 and 4096 -> 24576 at M = 4096 / 8192).
+// So the large tile wins whenever the small tiles would need more than one
+// round (even when the large ones leave CUs idle: 5120 -> 5120 and
+// 25600 -> 5120 at M = 2048, 160 tiles, were 9 and 11 % faster than 640 small
+// tiles), and the small tile (with split-K when they are few) takes grids
+// that fit in one round.
+constexpr int kLargeRoundPct = 100, kSmallRoundPct = 66;
 static bool large_tiles_fit(int M, int N) {
-    return N % 256 == 0 && (int64_t)((M + 255) / 256) * (N / 256) >= kLargeTileMinTiles;
+    if (N % 256 != 0) return false;
+    const int64_t tl = (int64_t)((M + 255) / 256) * (N / 256);
+    const int64_t ts = (int64_t)((M + 127) / 128) * (N / 128);
+    const int64_t rl = (tl + kCUs - 1) / kCUs, rs = (ts + 2 * kCUs - 1) / (2 * kCUs);
+    return kLargeRoundPct * rl < kSmallRoundPct * rs;
 }
 
 // Buffer resource words (as buf_desc), built on the host.
