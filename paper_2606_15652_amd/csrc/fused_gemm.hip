@@ -942,11 +942,11 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
             }
     };
 
-    // One stream of items per wave: its dense groups (item j < ng: group
-    // gb + j, B = the strips' W pieces, scales s_w), then its residual entries
-    // (item ng + e: block p = pb + e at group res_kb[p], B = the strips' R
-    // pieces, scales s_r), through one ring of GD register stages, so the
-    // residual blocks continue the pipeline without a bubble.
+    // One stream of items per wave: its dense groups (group gb + j, B = the
+    // strips' W pieces, scales s_w), then its residual entries (block p at
+    // group res_kb[p], B = the strips' R pieces, scales s_r), through one ring
+    // of GD register stages, so the residual blocks continue the pipeline
+    // without a bubble (64 x 64 tiles: the first entry has a stage of its own).
     struct Stage {
         uint4 x[WM], b[SPW];
         uint2 xt[A4G ? WM : 1];                          // A4 from memory: the operand's tail dwords
@@ -961,27 +961,29 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     // plane follows the G M 64 bytes of the main plane
     const uint32_t lo_base = A8 ? (uint32_t)M * (uint32_t)K : 0u;
     const uint32_t tail0 = (uint32_t)G * (uint32_t)M * (uint32_t)kGroupBytes;
-    const int nitems = ng + ne;
-    // group of the next residual entry to issue (scalar, loaded one entry ahead)
-    int kb_next = (ne > 0) ? (int)res_kb[pb] : 0;
+    // 64 x 64 tiles (four dense groups a wave at K = 4096, a two-stage ring):
+    // the split's first residual entry goes through a stage of its own (Sr),
+    // loaded in the prologue right after the ring's stages and multiplied
+    // before the ring loop, so that a wave with one residual block beside its
+    // dense groups needs no third round of the ring (K = N = 4096, M = 256:
+    // 13.5 -> 13.0 us; decode and 32 x 64 tiles, whose rings already hold a
+    // fifth item, measured slower with it).  The ring takes the dense groups
+    // and the other entries: ring item j is group gb + j (j < ng) or entry
+    // j - ng + R0.
+    constexpr int R0 = (WM == 4 && WN == 4 && !A8) ? 1 : 0;
+    const int nitems = ng + (ne > R0 ? ne - R0 : 0);
+    // groups of the first entry and of the ring's next entry (scalar; the
+    // latter loaded one entry ahead)
+    const int kb_first = (R0 && ne > 0) ? (int)res_kb[pb] : 0;
+    int kb_next = (ne > R0) ? (int)res_kb[pb + R0] : 0;
     // activation rows from M on are read as zeros without touching memory
     // (decode tiles are mostly such rows)
     uint32_t xdead[WM];
 #pragma unroll
     for (int i = 0; i < WM; ++i) xdead[i] = mw + 16 * i + lrow < M ? 0u : kPastEnd;
-    auto load_item = [&](Stage& S, int j) {
-        const bool live = j < nitems;
-        // past the last item every offset gets bit 31: past every resource
-        // (arithmetic rather than a select, which the compiler turns into
-        // branches that reorder the ring's loads)
-        const uint32_t dead = (uint32_t)(nitems - 1 - j) & kPastEnd;
-        const bool res = j >= ng;                        // uniform
-        const int p = pb + (j - ng);
-        int g = gb + j;
-        if (res && live) {
-            g = kb_next;
-            if (j + 1 - ng < ne) kb_next = (int)res_kb[p + 1];
-        }
+    // the loads of an item: group g, residual block p (res), offsets with bit
+    // 31 set (dead: past every resource, so zeros without a memory access)
+    auto issue_item = [&](Stage& S, int g, uint32_t dead, bool res, int p) {
         S.g = g;
         S.res = res;
         if constexpr (!FQ && !XS) {
@@ -1028,6 +1030,24 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
                                                                    0, 0);
             }
         }
+    };
+    auto load_item = [&](Stage& S, int j) {
+        const bool live = j < nitems;
+        // past the last item every offset gets bit 31 (arithmetic rather than
+        // a select, which the compiler turns into branches that reorder the
+        // ring's loads)
+        const uint32_t dead = (uint32_t)(nitems - 1 - j) & kPastEnd;
+        const bool res = j >= ng;                        // uniform
+        const int p = pb + (j - ng) + R0;
+        int g = gb + j;
+        if (res && live) {
+            g = kb_next;
+            if (j - ng + R0 + 1 < ne) kb_next = (int)res_kb[p + 1];
+        }
+        issue_item(S, g, dead, res, p);
+    };
+    auto load_first_res = [&](Stage& S) {
+        issue_item(S, kb_first, (uint32_t)(ne - 1) & kPastEnd, true, pb);
     };
     auto compute_item = [&](const Stage& S, auto res_c) {
         constexpr bool RES = decltype(res_c)::value;
@@ -1102,12 +1122,16 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     // (the scheduling barriers keep each stage's loads together and the
     // stages in ring order, so the wait for a stage counts exactly the
     // stages issued after it)
-    Stage St[GD];
+    Stage St[GD], Sr;                                   // Sr: used when R0 > 0
     static_for<GD>([&](auto dc) {
         constexpr int d = decltype(dc)::value;
         load_item(St[d], d);
         __builtin_amdgcn_sched_barrier(0);
     });
+    if constexpr (R0 > 0) {
+        load_first_res(Sr);
+        __builtin_amdgcn_sched_barrier(0);
+    }
 
     if constexpr (XS) {
         // XS, part 2: the chunks into LDS (main-plane chunks swizzled)
@@ -1160,6 +1184,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         __syncthreads();
     }
 
+    if (R0 > 0 && ne > 0) {
+        if (RAW) compute_item(Sr, std::true_type{});
+        else compute_item(Sr, std::false_type{});
+    }
     for (int j0 = 0; j0 < nitems; j0 += GD) {
         static_for<GD>([&](auto dc) {
             constexpr int d = decltype(dc)::value;
