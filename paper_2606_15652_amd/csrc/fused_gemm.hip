@@ -59,6 +59,7 @@ struct GemmArgs {
     int ldx;
     int nnzb;
     int rank_rows;           // tiled kernels: order block rows by residual count (one-round grids)
+    int y16;                 // Y 16-byte aligned: the tiled kernels store Y in 16-byte row pieces
     // byte sizes of Xq, Wq, Rq, s_w, s_r (each below 2 GB) and buffer
     // resources spanning each whole operand (set by launch())
     uint32_t xq_bytes, wq_bytes, rq_bytes, sw_bytes, sr_bytes;
@@ -740,6 +741,46 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
 
     // epilogue: lane holds rows 4 * (lane / 16) + r of each sub-tile, column
     // lane % 16; the fp32 sums are scale x (group sum / 64)
+    if constexpr (!RAW && !SPLIT) {
+        if (a.y16) {
+            // fp16 Y through the ring's LDS: the tile, row-major (row r, local
+            // column lc = 16 (wn + WAVES_N c) + lrow, i.e. block row br[lc / 128]),
+            // its 16-byte chunks (8 columns) swizzled by chunk ^ 2 ((r / 4) % 4) so
+            // the four row quarters a write covers hit distinct banks; then each
+            // thread stores whole 16-byte row pieces (eight times fewer store
+            // instructions than one fp16 value a lane, each covering whole lines)
+            static_assert(sizeof(Ring) >= (size_t)TM * TN * 2, "the output tile fits the ring");
+            uint8_t* ys = reinterpret_cast<uint8_t*>(&L);
+            auto ys_off = [](int r, int lc) {
+                return (uint32_t)r * (uint32_t)(TN * 2) + (uint32_t)((((lc >> 3) ^ (((r >> 2) & 3) << 1)) << 4) +
+                                                                     ((lc & 7) << 1));
+            };
+            __syncthreads();                              // every wave is done with the ring
+#pragma unroll
+            for (int i = 0; i < WM; ++i) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int rl = wrow + 16 * i + 4 * lq + r;
+                    const int m = m0 + rl;
+                    const float sx = m < M ? half_bits_to_float(a.s_x[m]) * kCodeScale : 0.f;
+#pragma unroll
+                    for (int c = 0; c < WN; ++c)
+                        *reinterpret_cast<uint16_t*>(ys + ys_off(rl, 16 * (wn + WAVES_N * c) + lrow)) =
+                            float_to_half_bits(sx * acc[i][c][r]);
+                }
+            }
+            __syncthreads();
+            constexpr int kPiecesPerRow = TN / 8;
+            const int rows = min(TM, M - m0);
+            for (int q = t; q < rows * kPiecesPerRow; q += TS::kThreads) {
+                const int rl = q / kPiecesPerRow, lc = 8 * (q % kPiecesPerRow);
+                const int n = kTB * br[lc / kTB] + (lc & (kTB - 1));
+                *reinterpret_cast<uint4*>(a.Y + (int64_t)(m0 + rl) * a.ldy + n) =
+                    *reinterpret_cast<const uint4*>(ys + ys_off(rl, lc));
+            }
+            return;
+        }
+    }
 #pragma unroll
     for (int i = 0; i < WM; ++i) {
 #pragma unroll
@@ -1360,6 +1401,7 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
     GemmArgs a = args;
     const mq_status rs = operand_resources<RAW>(a);
     if (rs != MQ_OK) return rs;
+    a.y16 = (!RAW && a.Y && mq_host::aligned(a.Y, 16)) ? 1 : 0;
     if (variant == MQ_VARIANT_AUTO)
         variant = a.M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY
                   : large_tiles_fit(a.M, a.N) ? MQ_VARIANT_TILED_LARGE

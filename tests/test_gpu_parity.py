@@ -284,6 +284,36 @@ def test_gemm_guard_bands_and_empty(tc, mq, orc):
     assert st == 0 and np.all(host(Y) == 7)
 
 
+def test_gemm_y_not_16_byte_aligned(tc, mq, orc):
+    """Y two bytes past a 16-byte boundary (the tiled kernels then store one
+    value a lane instead of staging 16-byte row pieces): the same values, and
+    nothing written outside Y[:M, :N]."""
+    M, N, K, nnzb = 37, 512, 512, 4
+    Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=6)
+    Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    Xq_d, sx_d = dev_x(tc, Xq), dev(tc, s_x)
+    lib = mq.load()
+    ldy, canary = N + 8, 12345
+    for v in (2, 3, 4):
+        flat = tc.full(((M + 4) * ldy + 8,), canary, dtype=tc.int16, device="cuda")
+        base = 2 * ldy + 1                                # elements: 2 bytes past alignment
+        assert (flat.data_ptr() + 2 * base) % 16 == 2
+        st = lib.mq_fused_gemm_variant(v, M, N, K, Xq_d.data_ptr(), sx_d.data_ptr(), pw.Wq.data_ptr(),
+                                       pw.s_w.data_ptr(), pw.rowptr.data_ptr(), pw.kb.data_ptr(), nnzb,
+                                       pw.Rq.data_ptr(), pw.s_r.data_ptr(), flat.data_ptr() + 2 * base,
+                                       ldy, None, 0, None)
+        tc.cuda.synchronize()
+        assert st == 0, v
+        h = host(flat)
+        idx = base + np.arange(M)[:, None] * ldy + np.arange(N)[None, :]
+        y = h[idx].view(np.float16).astype(np.float64)
+        assert np.abs(y - Y64).max() / np.abs(Y64).max() <= TIGHT, v
+        mask = np.ones(h.shape, bool)
+        mask[idx.ravel()] = False
+        assert np.all(h[mask] == canary), v
+
+
 def test_gemm_no_residual_null_pointers(tc, mq, orc):
     M, N, K = 40, 256, 384
     Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, 0, seed=9)
