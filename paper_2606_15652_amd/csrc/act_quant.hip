@@ -21,6 +21,16 @@ namespace mq {
 
 constexpr int kActThreads = 256;
 
+// Row of workgroup b.  Workgroups go to the eight XCDs in turn (b % 8), and
+// neighbouring rows share the 128-byte lines of the operand planes (a row
+// writes 64 and 32 bytes of each group's main and tail pieces), so each XCD
+// takes a contiguous range of rows: the lines are then written whole from one
+// L2.  A bijection on [0, M): XCD x holds rows x per + min(x, rem) on.
+__device__ __forceinline__ int xcd_row(int b, int M) {
+    const int x = b % 8, k = b / 8, per = M / 8, rem = M % 8;
+    return x * per + min(x, rem) + k;
+}
+
 // CPT > 0: the row stays in registers (CPT chunks per thread); CPT == 0: the
 // row is read twice.
 template <int CPT>
@@ -28,7 +38,7 @@ __global__ __launch_bounds__(kActThreads) void act_quant_kernel(
     const uint16_t* __restrict__ X, int M, int K, int ldx,
     uint8_t* __restrict__ Xq, uint16_t* __restrict__ s_x) {
     __shared__ uint32_t red[kActThreads / 64];
-    const int m = blockIdx.x;
+    const int m = xcd_row(blockIdx.x, M);
     const int t = threadIdx.x;
     const uint16_t* row = X + (int64_t)m * ldx;
     const int nchunks = K / 16, G = K / 128;
@@ -121,7 +131,7 @@ __global__ __launch_bounds__(kActThreads) void act_quant8_kernel(
     const uint16_t* __restrict__ X, int M, int K, int ldx,
     uint8_t* __restrict__ Xq8, uint16_t* __restrict__ s_x) {
     __shared__ uint32_t red[kActThreads / 64];
-    const int m = blockIdx.x;
+    const int m = xcd_row(blockIdx.x, M);
     const int t = threadIdx.x;
     const uint16_t* row = X + (int64_t)m * ldx;
     const int nchunks = K / 16;
