@@ -1,7 +1,8 @@
 """Build libmq.so (gfx950) in-tree with hipcc.
 
 Every HIP source under csrc/ is compiled for gfx950 only, with correctly
-rounded fp32 division and packed-fp32 instruction selection disabled, and
+rounded fp32 division and packed-fp32 instruction selection disabled, into an
+object of its own (sources may add flags: SOURCE_FLAGS), and the objects are
 linked into ``paper_2606_15652_amd/libmq.so``.
 """
 from __future__ import annotations
@@ -10,6 +11,7 @@ import glob
 import os
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
@@ -17,7 +19,7 @@ LIB = os.path.join(HERE, "libmq.so")
 ARCH = "gfx950"
 
 FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-fhip-fp32-correctly-rounded-divide-sqrt", "-fno-fast-math",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-mllvm", "-amdgpu-mfma-vgpr-form",   # MFMA results in VGPRs: no AGPR read-backs
@@ -25,26 +27,59 @@ FLAGS = [
     f"-I{os.path.join(ROOT, 'include')}", f"-I{os.path.join(HERE, 'csrc')}",
 ]
 
+# Per-source additions: the medium-M streaming tiles schedule for maximum ILP
+# (measured 5 % faster there, slower on the other kernels).
+SOURCE_FLAGS = {
+    "medium_gemm.hip": ["-mllvm", "-amdgpu-sched-strategy=max-ilp"],
+}
+
+# the host pass warns that it does not know the packed-fp32 feature
+_NOISE = ("'-packed-fp32-ops' is not a recognized feature for this target", "ignoring feature")
+
 
 def sources():
     return sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
-    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB + ".tmp"
-    cmd = [hipcc, *FLAGS, *sources(), "-o", tmp]
+def compile_flags(src: str):
+    """Compiler flags of one source (the common ones plus its own)."""
+    return [*FLAGS, *SOURCE_FLAGS.get(os.path.basename(src), [])]
+
+
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
-    proc = subprocess.run(cmd, capture_output=True, text=True)
-    # the host pass warns that it does not know the packed-fp32 feature
-    noise = "'-packed-fp32-ops' is not a recognized feature for this target"
-    err = "\n".join(l for l in proc.stderr.splitlines() if noise not in l and "ignoring feature" not in l)
-    if proc.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({proc.returncode}):\n{proc.stderr}")
-    if verbose and err.strip():
-        print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
+    return subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+
+
+def build(verbose: bool = False, jobs: int = 8) -> str:
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    with tempfile.TemporaryDirectory(prefix="mq_build_") as tmpdir:
+        objs, pending = [], []
+        for src in sources():
+            obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
+            objs.append(obj)
+            pending.append((src, [hipcc, *compile_flags(src), "-c", src, "-o", obj]))
+        running = []
+        while pending or running:
+            while pending and len(running) < jobs:
+                src, cmd = pending.pop(0)
+                running.append((src, _run(cmd, verbose)))
+            src, proc = running.pop(0)
+            _, err = proc.communicate()
+            if proc.returncode != 0:
+                for _, p in running:
+                    p.wait()
+                raise RuntimeError(f"hipcc failed on {os.path.basename(src)} ({proc.returncode}):\n{err}")
+            err = "\n".join(l for l in err.splitlines() if not any(n in l for n in _NOISE))
+            if verbose and err.strip():
+                print(err, file=sys.stderr)
+        tmp = LIB + ".tmp"
+        link = subprocess.run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp],
+                              capture_output=True, text=True)
+        if link.returncode != 0:
+            raise RuntimeError(f"link failed ({link.returncode}):\n{link.stderr}")
+        os.replace(tmp, LIB)
     return LIB
 
 

@@ -808,6 +808,7 @@ void gemm_tiled_kernel(GemmArgs a, int groups_per_split, float* __restrict__ par
     }
 }
 
+#ifndef MQ_MEDIUM_TU
 // Y[m, n] = fp16(s_x[m] * sum_{s < splits} part[s, m, n]), summed in split order.
 __global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, int splits,
                                                             int M, int N, const uint16_t* __restrict__ s_x,
@@ -826,6 +827,7 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(int32_t* __restrict__ p,
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) p[i] = 0;
 }
+#endif
 
 // Split-K factor for the tiled kernel: enough workgroups to give every CU two,
 // with at least 8 groups per split.
@@ -1307,6 +1309,25 @@ static void launch_stream(const GemmArgs& a, size_t xs_bytes, hipStream_t stream
                        dim3(64 * kDecodeWaves), xs_bytes, stream, a);
 }
 
+// The W4A4 medium tiles (64 x 64 when they give every CU one, else 32 x 64)
+// are compiled in a translation unit of their own (medium_gemm.hip, which
+// includes this file with MQ_MEDIUM_TU defined and nothing else of the
+// library), built with the compiler's maximum-ILP scheduling strategy: the
+// default one measured 5 % slower there (K = N = 4096, M = 256: 13.2 against
+// 12.5 us), and that strategy measured slower on the tiled and decode kernels.
+template <bool RAW>
+void launch_medium_tiles(const GemmArgs& a, bool tile64, hipStream_t stream);
+#ifdef MQ_MEDIUM_TU
+template <bool RAW>
+void launch_medium_tiles(const GemmArgs& a, bool tile64, hipStream_t stream) {
+    if (tile64) launch_stream<4, 4, 1, 1, RAW, false>(a, 0, stream);
+    else launch_stream<2, 4, 1, 1, RAW, false>(a, 0, stream);
+}
+template void launch_medium_tiles<false>(const GemmArgs&, bool, hipStream_t);
+template void launch_medium_tiles<true>(const GemmArgs&, bool, hipStream_t);
+}  // namespace mq
+#else
+
 // Decode: the activation rows are copied into LDS once per workgroup when
 // they fit beside the partial-sum exchange (two workgroups a CU: 80 KB each;
 // at most 8 chunks of 16 bytes a thread), so the items load only weights.
@@ -1414,8 +1435,7 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
         const int64_t t64 = (int64_t)((a.M + 63) / 64) * (a.N / 64);
         const int64_t t32 = (int64_t)((a.M + 31) / 32) * (a.N / 64);
         if (t32 > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
-        if (t64 >= kCUs) launch_stream<4, 4, 1, 1, RAW, false>(a, 0, stream);
-        else launch_stream<2, 4, 1, 1, RAW, false>(a, 0, stream);
+        launch_medium_tiles<RAW>(a, t64 >= kCUs, stream);
     } else if (variant == MQ_VARIANT_TILED_LARGE) {
         using TS = TileShape<8, 4>;
         const int64_t tiles = (int64_t)((a.M + TS::kTM - 1) / TS::kTM) * (a.N / TS::kTN);
@@ -1712,3 +1732,4 @@ extern "C" mq_status mq_linear_noalloc(int M, int N, int K, const void* X, int l
     }
     return linear_impl(M, N, K, X, ldx, Wq, s_w, res_rowptr, res_kb, nnzb, Rq, s_r, Y, ldy, ws, need, stream);
 }
+#endif  // MQ_MEDIUM_TU

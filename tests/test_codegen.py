@@ -47,7 +47,7 @@ def kernels_asm():
     from paper_2606_15652_amd import build
     out = {}
     for src in build.sources():
-        cmd = [os.environ.get("HIPCC", "/opt/rocm/bin/hipcc"), *[f for f in build.FLAGS if f not in ("-shared", "-fPIC")],
+        cmd = [os.environ.get("HIPCC", "/opt/rocm/bin/hipcc"), *[f for f in build.compile_flags(src) if f != "-fPIC"],
                "--cuda-device-only", "-S", src, "-o", "-"]
         asm = subprocess.run(cmd, capture_output=True, text=True, check=True).stdout
         cur = None
