@@ -1025,21 +1025,20 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     uint32_t xdead[WM];
 #pragma unroll
     for (int i = 0; i < WM; ++i) xdead[i] = mw + 16 * i + lrow < M ? 0u : kPastEnd;
-    // the loads of an item: group g, residual block p (res), offsets with bit
-    // 31 set (dead: past every resource, so zeros without a memory access)
-    auto issue_item = [&](Stage& S, int g, uint32_t dead, bool res, int p) {
+    // the loads of an item: group g, residual block p (res)
+    auto issue_item = [&](Stage& S, int g, bool res, int p) {
         S.g = g;
         S.res = res;
         if constexpr (!FQ && !XS) {
 #pragma unroll
-            for (int i = 0; i < WM; ++i) S.x[i] = bload16(rx, (lo_base + x_offset(g, i)) | dead | xdead[i], 0);
+            for (int i = 0; i < WM; ++i) S.x[i] = bload16(rx, (lo_base + x_offset(g, i)) | xdead[i], 0);
         }
         if constexpr (A4G) {
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
                 const uint32_t to = tail0 + ((uint32_t)g * (uint32_t)M + (uint32_t)(mw + 16 * i + lrow)) * 32u +
                                     (uint32_t)lq * 8u;
-                const i32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rx, to | dead | xdead[i], 0, 0);
+                const i32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rx, to | xdead[i], 0, 0);
                 S.xt[i] = make_uint2((uint32_t)v[0], (uint32_t)v[1]);
             }
         }
@@ -1047,8 +1046,8 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
 #pragma unroll
             for (int i = 0; i < WM; ++i) {
                 const uint32_t ho = ((uint32_t)g * (uint32_t)M + (uint32_t)(mw + 16 * i + lrow)) * 128u + (uint32_t)lq * 32u;
-                S.xh[i][0] = bload16(rx, ho | dead | xdead[i], 0);
-                S.xh[i][1] = bload16(rx, (ho + 16u) | dead | xdead[i], 0);
+                S.xh[i][0] = bload16(rx, ho | xdead[i], 0);
+                S.xh[i][1] = bload16(rx, (ho + 16u) | xdead[i], 0);
             }
         }
         // resources built from the selected base (a select of scalars, not of
@@ -1060,38 +1059,31 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
                               (uint32_t)nw;
 #pragma unroll
         for (int s = 0; s < SPW; ++s)
-            S.b[s] = bload16(rb, ((row0 + 16u * s) * kGroupBytes + loff) | dead, 0);
+            S.b[s] = bload16(rb, (row0 + 16u * s) * kGroupBytes + loff, 0);
         if constexpr (!RAW) {
             const bool use_sr = res && a.s_r != nullptr;
             const __amdgpu_buffer_rsrc_t rs =
                 make_rsrc(use_sr ? (const void*)a.s_r : (const void*)a.s_w, use_sr ? a.sr_bytes : a.sw_bytes);
             if constexpr (kScaleShfl) {
-                S.sc[0] = __builtin_amdgcn_raw_buffer_load_b16(rs, ((row0 + (uint32_t)lane) * 2u) | dead, 0, 0);
+                S.sc[0] = __builtin_amdgcn_raw_buffer_load_b16(rs, (row0 + (uint32_t)lane) * 2u, 0, 0);
             } else {
 #pragma unroll
                 for (int s = 0; s < SPW; ++s)
-                    S.sc[s] = __builtin_amdgcn_raw_buffer_load_b16(rs, ((row0 + 16u * s + (uint32_t)lrow) * 2u) | dead,
+                    S.sc[s] = __builtin_amdgcn_raw_buffer_load_b16(rs, (row0 + 16u * s + (uint32_t)lrow) * 2u,
                                                                    0, 0);
             }
         }
     };
+    // (item j < nitems; no loads are issued past the last item)
     auto load_item = [&](Stage& S, int j) {
-        const bool live = j < nitems;
-        // past the last item every offset gets bit 31 (arithmetic rather than
-        // a select, which the compiler turns into branches that reorder the
-        // ring's loads)
-        const uint32_t dead = (uint32_t)(nitems - 1 - j) & kPastEnd;
         const bool res = j >= ng;                        // uniform
         const int p = pb + (j - ng) + R0;
         int g = gb + j;
-        if (res && live) {
+        if (res) {
             g = kb_next;
             if (j - ng + R0 + 1 < ne) kb_next = (int)res_kb[p + 1];
         }
-        issue_item(S, g, dead, res, p);
-    };
-    auto load_first_res = [&](Stage& S) {
-        issue_item(S, kb_first, (uint32_t)(ne - 1) & kPastEnd, true, pb);
+        issue_item(S, g, res, p);
     };
     auto compute_item = [&](const Stage& S, auto res_c) {
         constexpr bool RES = decltype(res_c)::value;
@@ -1173,7 +1165,7 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         __builtin_amdgcn_sched_barrier(0);
     });
     if constexpr (R0 > 0) {
-        load_first_res(Sr);
+        if (ne > 0) issue_item(Sr, kb_first, true, pb);
         __builtin_amdgcn_sched_barrier(0);
     }
 
