@@ -880,7 +880,7 @@ struct StreamDepth {
 // high plane and a folded 4-bit low plane (mq_quantize_act8); each product
 // takes the low-plane MFMA and the fp8 x fp6 MFMA of the high plane chained
 // on its result (both exact), the rest is unchanged.
-template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false, bool XS = false>
+template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false, bool XS = false, bool PT = false>
 __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs a) {
     static_assert(WN * WGN == 1 || WN * WGN == 2 || WN * WGN == 4 || WN * WGN == 8,
                   "tile columns inside one block row");
@@ -894,6 +894,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     static_assert(KS * WG2 == NW, "eight waves");
     constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
     constexpr int SPW = WN;
+    // PT (fused-quantisation decode): the workgroup takes the tiles
+    // blockIdx.x + k gridDim.x in turn (all in tile row 0), quantising the
+    // rows once for all of them
+    static_assert(!PT || FQ, "several tiles a workgroup: the fused-quantisation decode tile");
     constexpr int GD = StreamDepth<WM, WN, RAW, A8>::GD;
     constexpr bool kScaleShfl = SPW == 4;
     constexpr int kAcc = WM * SPW * 4;                           // sums per lane and accumulator
@@ -912,8 +916,9 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int lrow = lane & 15, lq = lane >> 4;
     const int split = wave / WG2, wpos = wave % WG2, wm = wpos / WGN, wn = wpos % WGN;
+    const int tiles_m = (M + TM - 1) / TM, tiles_n = N / TN;
     int tm, tn;
-    tile_coords(blockIdx.x, (M + TM - 1) / TM, N / TN, tm, tn);
+    tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * TM, n0 = tn * TN;
     const int nb = n0 / kGroup, roff = n0 % kGroup;
     const int mw = m0 + 16 * WM * wm;                            // the wave's first row
@@ -928,7 +933,32 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     // the constant address space: off the vector-memory counter)
     const cint32_t* res_kb = (const cint32_t*)(a.res_kb);
     int pb = 0, ne = 0;
-    if (a.rowptr) {
+    // PT: the workgroup's ntw tiles (at most 64; every wave has at least one
+    // group in each), lane k holding tile k's first column (vn0) and this
+    // split's run of its block row's entries (vpb, vne); the wave's items
+    // over all its tiles: nall
+    int ntw = 1, vn0 = n0, vpb = 0, vne = 0, nall = 0;
+    if constexpr (PT) {
+        ntw = (tiles_n - (int)blockIdx.x + (int)gridDim.x - 1) / (int)gridDim.x;
+        if (lane < ntw) {
+            int tml, tnl;
+            tile_coords((int)blockIdx.x + lane * (int)gridDim.x, tiles_m, tiles_n, tml, tnl);
+            vn0 = tnl * TN;
+            if (a.rowptr) {
+                const int nbl = vn0 / kGroup;
+                const int rp = a.rowptr[nbl], cnt = a.rowptr[nbl + 1] - rp;
+                const int eper = cnt / KS, eextra = cnt % KS;
+                vpb = rp + split * eper + min(split, eextra);
+                vne = eper + (split < eextra ? 1 : 0);
+            }
+        }
+        int sum = vne;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+        nall = __builtin_amdgcn_readfirstlane(sum) + ntw * ng;
+        pb = __builtin_amdgcn_readlane(vpb, 0);
+        ne = __builtin_amdgcn_readlane(vne, 0);
+    } else if (a.rowptr) {
         const cint32_t* rowptr = (const cint32_t*)(a.rowptr);
         const int rp = rowptr[nb], cnt = rowptr[nb + 1] - rp;
         const int eper = cnt / KS, eextra = cnt % KS;
@@ -1015,7 +1045,8 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     // and the other entries: ring item j is group gb + j (j < ng) or entry
     // j - ng + R0.
     constexpr int R0 = (WM == 4 && WN == 4 && !A8) ? 1 : 0;
-    const int nitems = ng + (ne > R0 ? ne - R0 : 0);
+    static_assert(!(PT && R0), "decode tiles have no first-residual stage");
+    const int nitems = PT ? nall : ng + (ne > R0 ? ne - R0 : 0);
     // groups of the first entry and of the ring's next entry (scalar; the
     // latter loaded one entry ahead)
     const int kb_first = (R0 && ne > 0) ? (int)res_kb[pb] : 0;
@@ -1025,8 +1056,9 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     uint32_t xdead[WM];
 #pragma unroll
     for (int i = 0; i < WM; ++i) xdead[i] = mw + 16 * i + lrow < M ? 0u : kPastEnd;
-    // the loads of an item: group g, residual block p (res)
-    auto issue_item = [&](Stage& S, int g, bool res, int p) {
+    // the loads of an item: group g, residual block p (res), of the tile at
+    // columns n0 or (PT) tn[0]
+    auto issue_item = [&](Stage& S, int g, bool res, int p, auto... tn) {
         S.g = g;
         S.res = res;
         if constexpr (!FQ && !XS) {
@@ -1055,8 +1087,15 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         const bool use_r = res && a.Rq != nullptr;
         const __amdgpu_buffer_rsrc_t rb =
             make_rsrc(use_r ? (const void*)a.Rq : (const void*)a.Wq, use_r ? a.rq_bytes : a.wq_bytes);
-        const uint32_t row0 = (res ? (uint32_t)p * kGroup + (uint32_t)roff : (uint32_t)g * (uint32_t)N + (uint32_t)n0) +
-                              (uint32_t)nw;
+        uint32_t row0;
+        if constexpr (sizeof...(tn) > 0) {
+            const int t0 = (tn, ...);
+            row0 = (res ? (uint32_t)p * kGroup + (uint32_t)(t0 % kGroup) : (uint32_t)g * (uint32_t)N + (uint32_t)t0) +
+                   (uint32_t)nw;
+        } else {
+            row0 = (res ? (uint32_t)p * kGroup + (uint32_t)roff : (uint32_t)g * (uint32_t)N + (uint32_t)n0) +
+                   (uint32_t)nw;
+        }
 #pragma unroll
         for (int s = 0; s < SPW; ++s)
             S.b[s] = bload16(rb, (row0 + 16u * s) * kGroupBytes + loff, 0);
@@ -1084,6 +1123,28 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
             if (j - ng + R0 + 1 < ne) kb_next = (int)res_kb[p + 1];
         }
         issue_item(S, g, res, p);
+    };
+    // PT: items are loaded in order, tile after tile; the cursor: tile lk
+    // (columns ln0, entries lpb .. lpb + lne - 1), item lj of it
+    int lk = 0, lj = 0, ln0 = n0, lpb = pb, lne = ne;
+    auto load_next = [&](Stage& S) {
+        if (lj == ng + lne) {
+            ++lk;
+            lj = 0;
+            ln0 = __builtin_amdgcn_readlane(vn0, lk);
+            lpb = __builtin_amdgcn_readlane(vpb, lk);
+            lne = __builtin_amdgcn_readlane(vne, lk);
+            kb_next = lne > 0 ? (int)res_kb[lpb] : 0;
+        }
+        const bool res = lj >= ng;                       // uniform
+        const int p = lpb + (lj - ng);
+        int g = gb + lj;
+        if (res) {
+            g = kb_next;
+            if (lj - ng + 1 < lne) kb_next = (int)res_kb[p + 1];
+        }
+        issue_item(S, g, res, p, ln0);
+        ++lj;
     };
     auto compute_item = [&](const Stage& S, auto res_c) {
         constexpr bool RES = decltype(res_c)::value;
@@ -1161,7 +1222,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     Stage St[GD], Sr;                                   // Sr: used when R0 > 0
     static_for<GD>([&](auto dc) {
         constexpr int d = decltype(dc)::value;
-        if (d < nitems) load_item(St[d], d);
+        if (d < nitems) {
+            if constexpr (PT) load_next(St[d]);
+            else load_item(St[d], d);
+        }
         __builtin_amdgcn_sched_barrier(0);
     });
     if constexpr (R0 > 0) {
@@ -1224,57 +1288,90 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
         if (RAW) compute_item(Sr, std::true_type{});
         else compute_item(Sr, std::false_type{});
     }
+    // cross-wave reduction of the tile at columns tn0, splits added in split
+    // order (deterministic), and its outputs
+    constexpr int kRounds = RAW ? 2 : 1;
+    auto reduce_store = [&](int tn0) {
+#pragma unroll
+        for (int round = 0; round < kRounds; ++round) {
+            if (round > 0) __syncthreads();                     // the previous round is read
+#pragma unroll
+            for (int i = 0; i < WM; ++i)
+#pragma unroll
+                for (int s = 0; s < SPW; ++s)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int v = (i * SPW + s) * 4 + r;
+                        uint32_t x;
+                        if constexpr (RAW) x = (uint32_t)(round == 0 ? iacc[i][s][r] : racc[i][s][r]);
+                        else x = __float_as_uint(acc[i][s][r]);
+                        red[wave][v][lane] = x;
+                    }
+            __syncthreads();
+            for (int e = threadIdx.x; e < WG2 * kAcc * 64; e += 64 * NW) {
+                const int wp = e / (kAcc * 64), v = (e / 64) % kAcc, l = e % 64;
+                const int is = v / 4, r = v % 4;
+                const int i = is / SPW, s = is % SPW;
+                const int m = m0 + 16 * (WM * (wp / WGN) + i) + 4 * (l >> 4) + r;
+                const int n = tn0 + 16 * (WN * (wp % WGN) + s) + (l & 15);
+                if (m >= M) continue;
+                if constexpr (RAW) {
+                    int32_t t = 0;
+                    for (int k = 0; k < KS; ++k) t += (int32_t)red[k * WG2 + wp][v][l];
+                    (round == 0 ? a.Tb : a.Tr)[(int64_t)m * N + n] = t;
+                } else {
+                    float sum = 0.f;
+                    for (int k = 0; k < KS; ++k) sum += __uint_as_float(red[k * WG2 + wp][v][l]);
+                    const uint16_t sxb = FQ ? sx_sh[m] : a.s_x[m];
+                    a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * kCodeScale * sum);
+                }
+            }
+        }
+    };
+    auto zero_acc = [&]() {
+#pragma unroll
+        for (int i = 0; i < WM; ++i)
+#pragma unroll
+            for (int s = 0; s < SPW; ++s) {
+                acc[i][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+                iacc[i][s] = i32x4{0, 0, 0, 0};
+                racc[i][s] = i32x4{0, 0, 0, 0};
+            }
+    };
+
+    // PT: the tile being multiplied (ordinal ck, columns cn0) and its items
+    // still to come (every wave has at least one item in each tile, so a tile
+    // is complete when the next tile's first item comes up, and every wave
+    // meets the same barriers)
+    int ck = 0, cn0 = n0, cleft = ng + ne;
     for (int j0 = 0; j0 < nitems; j0 += GD) {
         static_for<GD>([&](auto dc) {
             constexpr int d = decltype(dc)::value;
             const int j = j0 + d;
             if (j < nitems) {
+                if constexpr (PT) {
+                    if (cleft == 0) {
+                        reduce_store(cn0);
+                        __syncthreads();                    // its partial sums are read
+                        zero_acc();
+                        ++ck;
+                        cn0 = __builtin_amdgcn_readlane(vn0, ck);
+                        cleft = ng + __builtin_amdgcn_readlane(vne, ck);
+                    }
+                    --cleft;
+                }
                 if (RAW && St[d].res) compute_item(St[d], std::true_type{});
                 else compute_item(St[d], std::false_type{});
             }
             __builtin_amdgcn_sched_barrier(0);
-            if (j + GD < nitems) load_item(St[d], j + GD);
+            if (j + GD < nitems) {
+                if constexpr (PT) load_next(St[d]);
+                else load_item(St[d], j + GD);
+            }
             __builtin_amdgcn_sched_barrier(0);
         });
     }
-
-    // cross-wave reduction, splits added in split order (deterministic)
-    constexpr int kRounds = RAW ? 2 : 1;
-#pragma unroll
-    for (int round = 0; round < kRounds; ++round) {
-        if (round > 0) __syncthreads();                     // the previous round is read
-#pragma unroll
-        for (int i = 0; i < WM; ++i)
-#pragma unroll
-            for (int s = 0; s < SPW; ++s)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int v = (i * SPW + s) * 4 + r;
-                    uint32_t x;
-                    if constexpr (RAW) x = (uint32_t)(round == 0 ? iacc[i][s][r] : racc[i][s][r]);
-                    else x = __float_as_uint(acc[i][s][r]);
-                    red[wave][v][lane] = x;
-                }
-        __syncthreads();
-        for (int e = threadIdx.x; e < WG2 * kAcc * 64; e += 64 * NW) {
-            const int wp = e / (kAcc * 64), v = (e / 64) % kAcc, l = e % 64;
-            const int is = v / 4, r = v % 4;
-            const int i = is / SPW, s = is % SPW;
-            const int m = m0 + 16 * (WM * (wp / WGN) + i) + 4 * (l >> 4) + r;
-            const int n = n0 + 16 * (WN * (wp % WGN) + s) + (l & 15);
-            if (m >= M) continue;
-            if constexpr (RAW) {
-                int32_t t = 0;
-                for (int k = 0; k < KS; ++k) t += (int32_t)red[k * WG2 + wp][v][l];
-                (round == 0 ? a.Tb : a.Tr)[(int64_t)m * N + n] = t;
-            } else {
-                float sum = 0.f;
-                for (int k = 0; k < KS; ++k) sum += __uint_as_float(red[k * WG2 + wp][v][l]);
-                const uint16_t sxb = FQ ? sx_sh[m] : a.s_x[m];
-                a.Y[(int64_t)m * a.ldy + n] = float_to_half_bits(half_bits_to_float(sxb) * kCodeScale * sum);
-            }
-        }
-    }
+    reduce_store(cn0);
 }
 
 // --------------------------------------------------------------------------
@@ -1295,9 +1392,38 @@ static int decode_spw(int M, int N) {
     return 1;
 }
 
+// Fused-quantisation decode grids: one workgroup per tile while the tiles fit
+// in one round of resident workgroups, else a round's worth (a multiple of
+// eight, so a workgroup's tiles stay on its XCD) of PT workgroups, each
+// quantising the rows once and taking its tiles in turn with the next tile's
+// loads in flight while it finishes the current one (four rows, 8192 ->
+// 28672: 38.7 -> 30.6 us, 5120 -> 25600: 26.3 -> 21.7 us; the staged-
+// activation decode, which has no quantisation to share, measured no faster
+// this way).  Every wave needs a group of each tile (K >= 8 x 128) and a workgroup
+// at most 64 tiles (one a lane); 0: one workgroup per tile.
+static unsigned decode_grid(const void* kernel, size_t lds_bytes, int K, int64_t tiles) {
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, 64 * kDecodeWaves, lds_bytes) != hipSuccess ||
+        occ < 1)
+        occ = 1;
+    const int64_t slots = (int64_t)occ * kCUs;
+    if (tiles <= slots || K / kGroup < kDecodeWaves) return 0;
+    const int64_t per = (tiles + slots - 1) / slots;
+    if (per > 64) return (unsigned)(((tiles + 63) / 64 + 7) / 8 * 8);
+    return (unsigned)slots;
+}
+
 template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false, bool XS = false>
 static void launch_stream(const GemmArgs& a, size_t xs_bytes, hipStream_t stream) {
     const int64_t tiles = (int64_t)((a.M + 16 * WM * WGM - 1) / (16 * WM * WGM)) * (a.N / (16 * WN * WGN));
+    if constexpr (FQ) {
+        const auto pt = gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ, A8, XS, true>;
+        const unsigned grid = decode_grid(reinterpret_cast<const void*>(pt), xs_bytes, a.K, tiles);
+        if (grid > 0) {
+            hipLaunchKernelGGL(pt, dim3(grid), dim3(64 * kDecodeWaves), xs_bytes, stream, a);
+            return;
+        }
+    }
     hipLaunchKernelGGL((gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ, A8, XS>), dim3((unsigned)tiles),
                        dim3(64 * kDecodeWaves), xs_bytes, stream, a);
 }

@@ -179,6 +179,47 @@ def test_gemm_parity_random_codes(tc, mq, orc, M, N, K, nnzb):
         assert err <= TIGHT, f"{v}: max-abs-rel {err:.3e}"
 
 
+# (M, N, K, nnzb): more decode tiles than the workgroups resident at once, so
+# each workgroup takes several tiles in turn (the tile count is no multiple of
+# the grid); K = 1024 gives every wave one group of a tile, K = 1152 ragged runs
+MANY_TILE_CASES = [(1, 65920, 1024, 300), (16, 65920, 1152, 600), (32, 49408, 1024, 250)]
+
+
+@pytest.mark.parametrize("M,N,K,nnzb", MANY_TILE_CASES, ids=[f"M{c[0]}_N{c[1]}_K{c[2]}" for c in MANY_TILE_CASES])
+def test_decode_several_tiles_per_workgroup(tc, mq, orc, M, N, K, nnzb):
+    ops = random_operands(M, N, K, nnzb, seed=M * 31 + N + K)
+    Xq, s_x, Wq, s_w, rowptr, kb, sel, Rq, s_r = ops
+    Tb_ref, Tr_ref, Y64 = orc.linear(Xq, s_x, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    Xq_d, sx_d = dev_x(tc, Xq), dev(tc, s_x).view(tc.float16)
+    for v in ("skinny", "auto"):
+        Tb, Tr = mq.fused_gemm_acc_i32(Xq_d, pw, variant=v)
+        Y = mq.fused_gemm(Xq_d, sx_d, pw, variant=v)
+        tc.cuda.synchronize()
+        assert np.array_equal(host(Tb), Tb_ref), f"{v}: Tb differs"
+        assert np.array_equal(host(Tr), Tr_ref), f"{v}: Tr differs"
+        err = maxabsrel(Y, Y64)
+        assert err <= TIGHT, f"{v}: max-abs-rel {err:.3e}"
+
+
+def test_linear_decode_several_tiles_per_workgroup(tc, mq, orc):
+    """The one-kernel decode path (quantisation fused) with several tiles per
+    workgroup: the rows are quantised once and serve every tile."""
+    M, N, K, nnzb = 3, 65920, 1024, 300
+    _, _, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=4242)
+    X = synth.gen_act(M, K, 4243)
+    Xq_r, sx_r = orc.quantize_act(X)
+    _, _, Y64 = orc.linear(Xq_r, sx_r, orc_pw(orc, N, K, Wq, s_w, rowptr, kb, sel, Rq, s_r))
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    Xd = dev(tc, X)
+    Y = mq.linear(Xd, pw)
+    Xq, s_x = mq.quantize_act(Xd)
+    Y2 = mq.fused_gemm(Xq, s_x, pw)
+    tc.cuda.synchronize()
+    assert maxabsrel(Y, Y64) <= TIGHT
+    assert np.array_equal(host(Y.view(tc.int16)), host(Y2.view(tc.int16)))
+
+
 # ------------------------------------------- whole layer from fp16 X ------
 # (M, N, K, nnzb): M <= 4 with M * K <= 32768 take the one-kernel decode path
 # (activation quantisation fused into the GEMM), the others quantise first.
