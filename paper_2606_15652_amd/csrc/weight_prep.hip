@@ -64,7 +64,7 @@ __global__ __launch_bounds__(128) void score_frob_kernel(
     const uint8_t* __restrict__ Wq, const uint16_t* __restrict__ s_w,
     double* __restrict__ score) {
     __shared__ double rows[kGroup];
-    const int KB = K / kGroup, G = KB;
+    const int KB = K / kGroup;
     const int nb = blockIdx.x / KB, kb = blockIdx.x % KB;
     const int r = threadIdx.x;
     const int n = nb * kGroup + r;
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(128) void score_dhessian_kernel(
     const uint8_t* __restrict__ Wq, const uint16_t* __restrict__ s_w,
     const double* __restrict__ h, double* __restrict__ score) {
     __shared__ double before_s[kGroup], after_s[kGroup];
-    const int KB = K / kGroup, G = KB;
+    const int KB = K / kGroup;
     const int nb = blockIdx.x / KB, kb = blockIdx.x % KB;
     const int r = threadIdx.x;
     const int n = nb * kGroup + r;
@@ -231,7 +231,6 @@ __global__ __launch_bounds__(128) void quant_residual_kernel(
         if (rowptr[mid] <= p) lo = mid; else hi = mid - 1;
     }
     const int nb = lo, kb = res_kb[p];
-    const int G = K / kGroup;
     const int r = threadIdx.x;
     const int n = nb * kGroup + r;
     const float* w = W + (int64_t)n * ldw + (int64_t)kb * kGroup;
