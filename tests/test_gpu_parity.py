@@ -456,6 +456,30 @@ def test_full_size_sampled(tc, mq, orc, name, M):
     assert np.abs(y - y64).max() / den <= TIGHT
 
 
+def test_graph_replay_several_tiles_per_workgroup(tc, mq, orc):
+    """The fused-quantisation decode whose workgroups take several tiles each
+    (grid sized on the host from the kernel's occupancy) captured in a HIP
+    graph: every replay equals the eager result bit for bit."""
+    M, N, K, nnzb = 2, 65920, 1024, 200
+    _, _, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=515)
+    pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
+    X = dev(tc, synth.gen_act(M, K, 516))
+    Y = tc.empty((M, N), dtype=tc.float16, device="cuda")
+    Y_eager = mq.linear(X, pw).clone()
+    mq.linear(X, pw, out=Y)
+    tc.cuda.synchronize()
+    g = tc.cuda.CUDAGraph()
+    with tc.cuda.graph(g):
+        mq.linear(X, pw, out=Y)
+    for rep in range(3):
+        Y.zero_()
+        mq.linear(X[:1].contiguous(), pw)            # unrelated eager work in between
+        tc.cuda.synchronize()
+        g.replay()
+        tc.cuda.synchronize()
+        assert tc.equal(Y.view(tc.int16), Y_eager.view(tc.int16)), rep
+
+
 def test_graph_replay_matches_eager(tc, mq, orc):
     """The hot path captured in a HIP graph: every replay (with eager work and
     synchronisation in between) equals the eager result bit for bit."""
