@@ -894,10 +894,10 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
     static_assert(KS * WG2 == NW, "eight waves");
     constexpr int TM = 16 * WM * WGM, TN = 16 * WN * WGN;
     constexpr int SPW = WN;
-    // PT (fused-quantisation decode): the workgroup takes the tiles
-    // blockIdx.x + k gridDim.x in turn (all in tile row 0), quantising the
-    // rows once for all of them
-    static_assert(!PT || FQ, "several tiles a workgroup: the fused-quantisation decode tile");
+    // PT (decode with fused quantisation or staged activations): the
+    // workgroup takes the tiles blockIdx.x + k gridDim.x in turn (all in tile
+    // row 0), quantising or staging the rows once for all of them
+    static_assert(!PT || FQ || XS, "several tiles a workgroup: the decode tiles");
     constexpr int GD = StreamDepth<WM, WN, RAW, A8>::GD;
     constexpr bool kScaleShfl = SPW == 4;
     constexpr int kAcc = WM * SPW * 4;                           // sums per lane and accumulator
@@ -1392,15 +1392,16 @@ static int decode_spw(int M, int N) {
     return 1;
 }
 
-// Fused-quantisation decode grids: one workgroup per tile while the tiles fit
-// in one round of resident workgroups, else a round's worth (a multiple of
-// eight, so a workgroup's tiles stay on its XCD) of PT workgroups, each
-// quantising the rows once and taking its tiles in turn with the next tile's
-// loads in flight while it finishes the current one (four rows, 8192 ->
-// 28672: 38.7 -> 30.6 us, 5120 -> 25600: 26.3 -> 21.7 us; the staged-
-// activation decode, which has no quantisation to share, measured no faster
-// this way).  Every wave needs a group of each tile (K >= 8 x 128) and a workgroup
-// at most 64 tiles (one a lane); 0: one workgroup per tile.
+// Decode grids (fused quantisation or staged activations): one workgroup per
+// tile while the tiles fit in one round of resident workgroups, else a
+// round's worth (a multiple of eight, so a workgroup's tiles stay on its XCD)
+// of PT workgroups, each quantising or staging the rows once and taking its
+// tiles in turn with the next tile's loads in flight while it finishes the
+// current one (fused quantisation, four rows, 8192 -> 28672: 38.7 -> 30.6 us,
+// 5120 -> 25600: 26.3 -> 21.7 us; staged activations, 5120 -> 25600 at one
+// and 16 rows: 18.55 -> 18.25 and 20.2 -> 19.6 us).  Every wave needs a group
+// of each tile (K >= 8 x 128) and a workgroup at most 64 tiles (one a lane);
+// 0: one workgroup per tile.
 static unsigned decode_grid(const void* kernel, size_t lds_bytes, int K, int64_t tiles) {
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, 64 * kDecodeWaves, lds_bytes) != hipSuccess ||
@@ -1416,7 +1417,7 @@ static unsigned decode_grid(const void* kernel, size_t lds_bytes, int K, int64_t
 template <int WM, int WN, int WGM, int WGN, bool RAW, bool FQ, bool A8 = false, bool XS = false>
 static void launch_stream(const GemmArgs& a, size_t xs_bytes, hipStream_t stream) {
     const int64_t tiles = (int64_t)((a.M + 16 * WM * WGM - 1) / (16 * WM * WGM)) * (a.N / (16 * WN * WGN));
-    if constexpr (FQ) {
+    if constexpr (FQ || XS) {
         const auto pt = gemm_stream_kernel<WM, WN, WGM, WGN, RAW, FQ, A8, XS, true>;
         const unsigned grid = decode_grid(reinterpret_cast<const void*>(pt), xs_bytes, a.K, tiles);
         if (grid > 0) {
@@ -1563,7 +1564,8 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
         hipLaunchKernelGGL((gemm_tiled_kernel<8, 4, RAW, false>), dim3((unsigned)tiles), dim3(TS::kThreads), 0,
                            stream, a, 0, (float*)nullptr);
     } else if (variant == MQ_VARIANT_SKINNY) {
-        if (a.M <= 16) launch_decode<1, RAW, false>(a, decode_spw(a.M, a.N), 0, stream);
+        // (one strip a tile at one row, as for fused quantisation)
+        if (a.M <= 16) launch_decode<1, RAW, false>(a, a.M == 1 ? 1 : decode_spw(a.M, a.N), 0, stream);
         else launch_decode<2, RAW, false>(a, decode_spw(a.M, a.N), 0, stream);
     } else {
         const int64_t tiles = (int64_t)((a.M + kTB - 1) / kTB) * (a.N / kTB);

@@ -457,27 +457,39 @@ def test_full_size_sampled(tc, mq, orc, name, M):
 
 
 def test_graph_replay_several_tiles_per_workgroup(tc, mq, orc):
-    """The fused-quantisation decode whose workgroups take several tiles each
-    (grid sized on the host from the kernel's occupancy) captured in a HIP
-    graph: every replay equals the eager result bit for bit."""
-    M, N, K, nnzb = 2, 65920, 1024, 200
-    _, _, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(M, N, K, nnzb, seed=515)
+    """The decode kernels whose workgroups take several tiles each (grid sized
+    on the host from the kernel's occupancy; fused quantisation at 2 rows,
+    staged activations at 16) captured in a HIP graph: every replay equals
+    the eager result bit for bit."""
+    N, K, nnzb = 65920, 1024, 200
+    _, _, Wq, s_w, rowptr, kb, sel, Rq, s_r = random_operands(2, N, K, nnzb, seed=515)
     pw = gpu_pw(tc, mq, N, K, Wq, s_w, rowptr, kb, Rq, s_r)
-    X = dev(tc, synth.gen_act(M, K, 516))
-    Y = tc.empty((M, N), dtype=tc.float16, device="cuda")
+    X = dev(tc, synth.gen_act(2, K, 516))
+    X16 = dev(tc, synth.gen_act(16, K, 517))
+    Xq16, sx16 = mq.quantize_act(X16)
+    Y = tc.empty((2, N), dtype=tc.float16, device="cuda")
+    Y16 = tc.empty((16, N), dtype=tc.float16, device="cuda")
     Y_eager = mq.linear(X, pw).clone()
-    mq.linear(X, pw, out=Y)
+    Y16_eager = mq.fused_gemm(Xq16, sx16, pw).clone()
+
+    def body():
+        mq.linear(X, pw, out=Y)
+        mq.fused_gemm(Xq16, sx16, pw, out=Y16)
+
+    body()
     tc.cuda.synchronize()
     g = tc.cuda.CUDAGraph()
     with tc.cuda.graph(g):
-        mq.linear(X, pw, out=Y)
+        body()
     for rep in range(3):
         Y.zero_()
+        Y16.zero_()
         mq.linear(X[:1].contiguous(), pw)            # unrelated eager work in between
         tc.cuda.synchronize()
         g.replay()
         tc.cuda.synchronize()
         assert tc.equal(Y.view(tc.int16), Y_eager.view(tc.int16)), rep
+        assert tc.equal(Y16.view(tc.int16), Y16_eager.view(tc.int16)), rep
 
 
 def test_graph_replay_matches_eager(tc, mq, orc):
