@@ -58,8 +58,9 @@ def run_layer(tc, mq, orc, layer, M):
     return ref, Xq_ref, sx_ref, Y, Tb, Tr
 
 
+# (the 25600-wide layer at M = 1 and 16: decode workgroups that take several tiles each)
 FULL_EXHAUSTIVE = [("c2_4096", 1), ("c2_4096", 16), ("c2_4096", 256), ("c2_4096", 4096),
-                   ("c3_up_d10", 4096), ("c4_qo", 32), ("c4_kv", 32)]
+                   ("c3_up_d10", 4096), ("c4_qo", 32), ("c4_kv", 32), ("c4_up", 1), ("c4_up", 16)]
 
 
 @pytest.mark.slow
@@ -124,12 +125,16 @@ def test_split_k_raw_sums(tc, mq, orc):
             assert maxabsrel(Y, Y64) <= TIGHT
 
 
-@pytest.mark.parametrize("M", [1, 2, 4])
-def test_linear_decode_benched_shape(tc, mq, orc, M):
-    """mq_linear at the benched decode shape (K = N = 4096, the c2 layer's real
-    weights): one kernel quantises and multiplies; every output against the
+LINEAR_DECODE = [("c2_4096", 1), ("c2_4096", 2), ("c2_4096", 4), ("c4_up", 1), ("c4_up", 4)]
+
+
+@pytest.mark.parametrize("name,M", LINEAR_DECODE, ids=[f"{n}_M{m}" for n, m in LINEAR_DECODE])
+def test_linear_decode_benched_shape(tc, mq, orc, name, M):
+    """mq_linear at decode shapes with the layers' own weights (K = N = 4096,
+    the benched layer; 5120 -> 25600, where each workgroup takes several
+    tiles): one kernel quantises and multiplies; every output against the
     oracle, bit-identical to quantise-then-GEMM."""
-    layer = synth.workload("c2_4096")
+    layer = synth.workload(name)
     ref, pw = prepared(tc, mq, orc, layer)
     X = layer.act(M)
     Xq_ref, sx_ref = orc.quantize_act(X)
