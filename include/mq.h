@@ -101,7 +101,8 @@ typedef enum mq_variant {
                                    round of two per CU                       */
     MQ_VARIANT_MEDIUM = 4       /* 32 or 64 x 64 output tiles; AUTO takes it
                                    when 128 x 128 tiles would be too few to
-                                   fill the chip                             */
+                                   fill the chip and the 64 x 64 tiles fit in
+                                   one round (or in five, up to K = 8192)    */
 } mq_variant;
 
 /* Static string naming a status code.  Never NULL. */

@@ -1499,13 +1499,19 @@ static i32x4 host_buf_desc(const void* base, uint32_t bytes) {
 }
 
 // AUTO takes the medium (streaming) kernel where the 128 x 128 tiles would
-// need split-K to give every CU two workgroups, as long as its 64 x 64 tiles
+// be too few to give every CU two workgroups (the tiled kernel would split K
+// and add the partial sums in a second launch), as long as its 64 x 64 tiles
 // fit on the CUs in one round (one workgroup per CU: its partial-sum exchange
-// takes most of the LDS).
-constexpr int kMediumTargetWGs = 512;
-static bool medium_preferred(int M, int N) {
-    return (int64_t)((M + kTB - 1) / kTB) * (N / kTB) < kMediumTargetWGs &&
-           (int64_t)((M + 63) / 64) * (N / 64) <= kCUs;
+// takes most of the LDS), or, up to K = 8192, in five rounds: there the split
+// and its reduction cost more than the extra rounds (K = N = 4096: M = 512
+// 27.4 -> 20.4 us, M = 768 37.5 -> 29.3 us; 5120 -> 1024 at M = 2048 28.3 ->
+// 22.7 us), while deeper K amortises them (14336 -> 4096 at M = 1024: 78 us
+// split against 96 us medium; 4096 -> 14336 at M = 512, seven rounds, 66.6
+// against 68.3 us).
+constexpr int kMediumTargetWGs = 512, kMediumMaxK = 8192, kMediumMaxRounds = 5;
+static bool medium_preferred(int M, int N, int K) {
+    const int64_t t128 = (int64_t)((M + kTB - 1) / kTB) * (N / kTB), t64 = (int64_t)((M + 63) / 64) * (N / 64);
+    return t128 < kMediumTargetWGs && (t64 <= kCUs || (K <= kMediumMaxK && t64 <= kMediumMaxRounds * kCUs));
 }
 
 // Byte sizes of the operands and buffer resources spanning each of them.
@@ -1546,7 +1552,7 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
     if (variant == MQ_VARIANT_AUTO)
         variant = a.M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY
                   : large_tiles_fit(a.M, a.N) ? MQ_VARIANT_TILED_LARGE
-                  : medium_preferred(a.M, a.N) ? MQ_VARIANT_MEDIUM : MQ_VARIANT_TILED;
+                  : medium_preferred(a.M, a.N, a.K) ? MQ_VARIANT_MEDIUM : MQ_VARIANT_TILED;
     if (variant == MQ_VARIANT_SKINNY && a.M > kSkinnyMaxM) variant = MQ_VARIANT_TILED;
     if (variant == MQ_VARIANT_TILED_LARGE && a.N % 256 != 0) variant = MQ_VARIANT_TILED;
     if (variant == MQ_VARIANT_MEDIUM) {
