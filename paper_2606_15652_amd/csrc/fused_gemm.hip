@@ -829,13 +829,18 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(int32_t* __restrict__ p,
 }
 #endif
 
-// Split-K factor for the tiled kernel: enough workgroups to give every CU two,
-// with at least 8 groups per split.
+// Split-K factor for the tiled kernel: doubled while the split grid still
+// fits in one round of two workgroups per CU (at least 8 groups per split).
+// Past one round only when the splits stay long (32 groups or more), where
+// more, shorter workgroups pay for the partial round: 25600 -> 5120 at M = 512
+// (160 tiles) 124 us with two splits, 108 with four; at shorter K the extra
+// half round costs more (K = N = 4096 at M = 1536, 384 tiles: 55.7 us with two
+// splits, 39.7 with none; 4096 -> 14336 at M = 512: 69 against 44.4 us).
 static int tiled_splits(int M, int N, int K) {
-    const int tiles = ((M + kTB - 1) / kTB) * (N / kTB);
+    const int64_t tiles = (int64_t)((M + kTB - 1) / kTB) * (N / kTB);
     const int G = K / kGroup;
     int s = 1;
-    while (tiles * s < 512 && G / (s * 2) >= 8) s *= 2;
+    while (G / (s * 2) >= 8 && (tiles * s * 2 <= 512 || (tiles * s < 512 && G / (s * 2) >= 32))) s *= 2;
     return s;
 }
 
