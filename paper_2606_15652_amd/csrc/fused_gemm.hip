@@ -1409,9 +1409,11 @@ static int decode_spw(int M, int N) {
 // 0: one workgroup per tile.
 static unsigned decode_grid(const void* kernel, size_t lds_bytes, int K, int64_t tiles) {
     int occ = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, 64 * kDecodeWaves, lds_bytes) != hipSuccess ||
-        occ < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, 64 * kDecodeWaves, lds_bytes) != hipSuccess) {
+        (void)hipGetLastError();    // a failed query must not surface as the launch's error
         occ = 1;
+    }
+    if (occ < 1) occ = 1;
     const int64_t slots = (int64_t)occ * kCUs;
     if (tiles <= slots || K / kGroup < kDecodeWaves) return 0;
     const int64_t per = (tiles + slots - 1) / slots;
