@@ -857,6 +857,8 @@ static int tiled_splits(int M, int N, int K) {
 // holding an item issues a fixed number of loads; a stage past the last item
 // issues none (loads at offsets past the resource, which read zeros, still
 // cost nearly as much as real ones: issuing them measured up to 20 % slower).
+// When the tiles outnumber a round of resident workgroups, each workgroup
+// takes several in turn (PT), with one item stream running through them.
 // --------------------------------------------------------------------------
 // Fused activation quantisation (FQ): at most kFusedMaxM rows and
 // kFusedCPT 16-element chunks per thread; the workgroup quantises the rows
@@ -1385,14 +1387,15 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
 constexpr int kSkinnyMaxM = 32;
 constexpr int kSkinnyAutoM = 32;   // AUTO picks the skinny kernel up to this M
 
-// Strips per decode workgroup: two when that still gives every CU a
-// workgroup (a workgroup's adjacent strips share DRAM pages and the block
+// Strips per decode tile from two rows on: two when that still gives every
+// CU a workgroup (a tile's adjacent strips share DRAM pages and the block
 // row's CSR entries), else one.  (Four measured no faster than two on the
-// 5120 -> 25600 layer at one token, slightly slower.)
+// 5120 -> 25600 layer at one token, slightly slower.)  At one row the callers
+// take one strip: there the tiles outnumber a round of workgroups on wide
+// layers, and smaller tiles balance the workgroups that take several.
 constexpr int kCUs = 256;
-static int decode_spw(int M, int N) {
+static int decode_spw(int N) {
     const int S = N / 16;
-    (void)M;
     if (S / 2 >= kCUs) return 2;
     return 1;
 }
@@ -1584,8 +1587,8 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
                            stream, a, 0, (float*)nullptr);
     } else if (variant == MQ_VARIANT_SKINNY) {
         // (one strip a tile at one row, as for fused quantisation)
-        if (a.M <= 16) launch_decode<1, RAW, false>(a, a.M == 1 ? 1 : decode_spw(a.M, a.N), 0, stream);
-        else launch_decode<2, RAW, false>(a, decode_spw(a.M, a.N), 0, stream);
+        if (a.M <= 16) launch_decode<1, RAW, false>(a, a.M == 1 ? 1 : decode_spw(a.N), 0, stream);
+        else launch_decode<2, RAW, false>(a, decode_spw(a.N), 0, stream);
     } else {
         const int64_t tiles = (int64_t)((a.M + kTB - 1) / kTB) * (a.N / kTB);
         if (tiles > 0x7fffffff) return MQ_ERR_UNSUPPORTED_SHAPE;
@@ -1711,11 +1714,11 @@ static mq_status launch_a8(GemmArgs a, hipStream_t stream) {
     const mq_status rs = operand_resources<RAW>(a, true);
     if (rs != MQ_OK) return rs;
     if (a.M <= 16) {
-        const int spw = decode_spw(a.M, a.N);
+        const int spw = decode_spw(a.N);
         if (spw == 2) launch_stream<1, 2, 1, 1, RAW, false, true>(a, 0, stream);
         else launch_stream<1, 1, 1, 1, RAW, false, true>(a, 0, stream);
     } else if (a.M <= 32) {
-        if (decode_spw(a.M, a.N) >= 2) launch_stream<2, 2, 1, 1, RAW, false, true>(a, 0, stream);
+        if (decode_spw(a.N) >= 2) launch_stream<2, 2, 1, 1, RAW, false, true>(a, 0, stream);
         else launch_stream<2, 1, 1, 1, RAW, false, true>(a, 0, stream);
     } else {
         const int64_t t64 = (int64_t)((a.M + 63) / 64) * (a.N / 64);
@@ -1807,7 +1810,7 @@ static mq_status linear_impl(int M, int N, int K, const void* X, int ldx,
         // one strip a tile at one row: more, smaller tiles balance the grid
         // of workgroups that take several (5120 -> 25600: 19.9 -> 19.1 us;
         // at four rows two strips measured faster)
-        launch_decode<1, false, true>(a, M == 1 ? 1 : decode_spw(M, N), (size_t)M * (K / 2), stream);
+        launch_decode<1, false, true>(a, M == 1 ? 1 : decode_spw(N), (size_t)M * (K / 2), stream);
         return mq_host::launch_status();
     }
     // quantise into the workspace, then the fused GEMM
