@@ -132,6 +132,19 @@ mq_status mq_quantize_act(const void* X, int M, int K, int ldx,
 size_t mq_fused_gemm_workspace_size(int M, int N, int K);
 
 /*
+ * The kernel family mq_fused_gemm (AUTO) takes for an M x N x K layer, from
+ * the shape alone (host logic; no device call, callable without a GPU):
+ *   *variant : an mq_variant value (MQ_VARIANT_SKINNY, _TILED, _TILED_LARGE
+ *              or _MEDIUM);
+ *   *splits  : K splits of the 128 x 128 tiled kernel (whose partial sums go
+ *              through the workspace), 1 for the other families.
+ * MQ_ERR_INVALID_ARG for null outputs or M outside [1, 2^24],
+ * MQ_ERR_UNSUPPORTED_SHAPE for N, K that mq_fused_gemm does not accept
+ * (multiples of 128, K <= 2^20, N <= 2^24).
+ */
+mq_status mq_fused_gemm_plan(int M, int N, int K, int* variant, int* splits);
+
+/*
  * Fused dense + sparse-residual W4A4 GEMM (Section 3 Eq. (4) with Eq. (2)'s
  * scale factorisation per group; Section 4.2 "Kernel Fusion" and
  * "Overlapped pipeline"):

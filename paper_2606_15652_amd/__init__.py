@@ -29,6 +29,7 @@ _SIG = {
     "mq_version": (_I, []),
     "mq_quantize_act": (_I, [_P, _I, _I, _I, _P, _P, _P]),
     "mq_fused_gemm_workspace_size": (C.c_size_t, [_I, _I, _I]),
+    "mq_fused_gemm_plan": (_I, [_I, _I, _I, _P, _P]),
     "mq_fused_gemm": (_I, [_I, _I, _I, _P, _P, _P, _P, _P, _P, _I, _P, _P, _P, _I, _P,
                           C.c_size_t, _P]),
     "mq_linear_workspace_size": (C.c_size_t, [_I, _I, _I]),
@@ -198,6 +199,15 @@ def _res_ptrs(pw: PackedWeight):
     if pw.nnzb == 0:
         return None, None, None, None
     return _ptr(pw.rowptr), _ptr(pw.kb), _ptr(pw.Rq), _ptr(pw.s_r)
+
+
+def plan(M: int, N: int, K: int):
+    """(kernel family name, K splits) that the AUTO variant takes for an
+    M x N x K layer (host logic only; no device needed)."""
+    v, sp = C.c_int(0), C.c_int(0)
+    _check("mq_fused_gemm_plan", load().mq_fused_gemm_plan(M, N, K, C.byref(v), C.byref(sp)))
+    name = {code: n for n, code in VARIANTS.items()}[v.value]
+    return name, sp.value
 
 
 def fused_gemm(Xq, s_x, pw: PackedWeight, out=None, variant: str = "auto", stream=None,

@@ -1558,6 +1558,18 @@ static mq_status operand_resources(GemmArgs& a, bool a8 = false) {
     return MQ_OK;
 }
 
+// The kernel family a launch takes: AUTO by shape, and the explicit choices
+// that do not apply to the shape mapped to the tiled kernel.
+static mq_variant resolve_variant(mq_variant variant, int M, int N, int K) {
+    if (variant == MQ_VARIANT_AUTO)
+        variant = M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY
+                  : large_tiles_fit(M, N) ? MQ_VARIANT_TILED_LARGE
+                  : medium_preferred(M, N, K) ? MQ_VARIANT_MEDIUM : MQ_VARIANT_TILED;
+    if (variant == MQ_VARIANT_SKINNY && M > kSkinnyMaxM) variant = MQ_VARIANT_TILED;
+    if (variant == MQ_VARIANT_TILED_LARGE && N % 256 != 0) variant = MQ_VARIANT_TILED;
+    return variant;
+}
+
 template <bool RAW>
 static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspace, size_t ws_bytes,
                         hipStream_t stream) {
@@ -1565,12 +1577,7 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
     const mq_status rs = operand_resources<RAW>(a);
     if (rs != MQ_OK) return rs;
     a.y16 = (!RAW && a.Y && mq_host::aligned(a.Y, 16)) ? 1 : 0;
-    if (variant == MQ_VARIANT_AUTO)
-        variant = a.M <= kSkinnyAutoM ? MQ_VARIANT_SKINNY
-                  : large_tiles_fit(a.M, a.N) ? MQ_VARIANT_TILED_LARGE
-                  : medium_preferred(a.M, a.N, a.K) ? MQ_VARIANT_MEDIUM : MQ_VARIANT_TILED;
-    if (variant == MQ_VARIANT_SKINNY && a.M > kSkinnyMaxM) variant = MQ_VARIANT_TILED;
-    if (variant == MQ_VARIANT_TILED_LARGE && a.N % 256 != 0) variant = MQ_VARIANT_TILED;
+    variant = resolve_variant(variant, a.M, a.N, a.K);
     if (variant == MQ_VARIANT_MEDIUM) {
         // one workgroup per CU (its ring takes most of the LDS): 64-row tiles
         // when they alone give every CU one, else 32-row ones
@@ -1648,6 +1655,15 @@ extern "C" size_t mq_fused_gemm_workspace_size(int M, int N, int K) {
     if (M <= 0 || !mq_host::shape_ok(N, K)) return 0;
     const int splits = tiled_splits(M, N, K);
     return splits > 1 ? (size_t)splits * M * N * sizeof(float) : 0;
+}
+
+extern "C" mq_status mq_fused_gemm_plan(int M, int N, int K, int* variant, int* splits) {
+    if (!variant || !splits || M < 1 || M > (1 << 24)) return MQ_ERR_INVALID_ARG;
+    if (!mq_host::shape_ok(N, K)) return MQ_ERR_UNSUPPORTED_SHAPE;
+    const mq_variant v = resolve_variant(MQ_VARIANT_AUTO, M, N, K);
+    *variant = (int)v;
+    *splits = v == MQ_VARIANT_TILED ? tiled_splits(M, N, K) : 1;
+    return MQ_OK;
 }
 
 extern "C" mq_status mq_fused_gemm_variant(mq_variant variant, int M, int N, int K,

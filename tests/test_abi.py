@@ -174,3 +174,36 @@ def test_a8_validation(lib):
     assert r(4, 256, 256, A, A, A, A, 1, A, None, A, None) == INVALID
     assert lib.mq_repack_act8(4, 256, A, 250, A, None, None) == SHAPE
     assert lib.mq_unpack_act8(4, 256, A + 8, A, 256, None) == MISALIGNED
+
+
+# AUTO's kernel choice (host logic, no device call): the families and split
+# counts the dispatch rules give on the benchmarked and family shapes
+PLANS = [
+    ((1, 4096, 4096), ("skinny", 1)), ((16, 4096, 4096), ("skinny", 1)), ((32, 4096, 4096), ("skinny", 1)),
+    ((33, 4096, 4096), ("medium", 1)), ((256, 4096, 4096), ("medium", 1)), ((512, 4096, 4096), ("medium", 1)),
+    ((1536, 4096, 4096), ("tiled", 1)), ((2048, 4096, 4096), ("tiled", 1)), ((4096, 4096, 4096), ("tiled_large", 1)),
+    ((512, 5120, 25600), ("tiled", 4)), ((1024, 4096, 14336), ("tiled", 2)), ((768, 5120, 5120), ("tiled", 2)),
+    ((2048, 1024, 5120), ("medium", 1)), ((2048, 5120, 5120), ("tiled_large", 1)), ((4096, 14336, 4096), ("tiled_large", 1)),
+    ((4096, 384, 4096), ("medium", 1)), ((4096, 384, 14336), ("tiled", 4)),
+]
+
+
+@pytest.mark.parametrize("shape,expect", PLANS, ids=[f"M{m}_N{n}_K{k}" for (m, n, k), _ in PLANS])
+def test_auto_plan(lib, shape, expect):
+    import paper_2606_15652_amd as mq
+    M, N, K = shape
+    assert mq.plan(M, N, K) == expect
+    fam, splits = expect
+    ws = lib.mq_fused_gemm_workspace_size(M, N, K)
+    if splits > 1:
+        assert ws >= splits * M * N * 4          # the partial sums fit the advertised workspace
+
+
+def test_auto_plan_validation(lib):
+    import ctypes as C
+    v, s = C.c_int(0), C.c_int(0)
+    assert lib.mq_fused_gemm_plan(0, 4096, 4096, C.byref(v), C.byref(s)) == INVALID
+    assert lib.mq_fused_gemm_plan(16, 4096, 4096, None, C.byref(s)) == INVALID
+    assert lib.mq_fused_gemm_plan(16, 4000, 4096, C.byref(v), C.byref(s)) == SHAPE
+    assert lib.mq_fused_gemm_plan(16, 4096, 100, C.byref(v), C.byref(s)) == SHAPE
+
