@@ -1410,15 +1410,34 @@ static int decode_spw(int N) {
 // and 16 rows: 18.55 -> 18.25 and 20.2 -> 19.6 us).  Every wave needs a group
 // of each tile (K >= 8 x 128) and a workgroup at most 64 tiles (one a lane);
 // 0: one workgroup per tile.
-static unsigned decode_grid(const void* kernel, size_t lds_bytes, int K, int64_t tiles) {
+// Resident workgroups per CU of a decode kernel with this much dynamic LDS
+// (the runtime's occupancy query, remembered per kernel and LDS size).
+static int decode_occupancy(const void* kernel, size_t lds_bytes) {
+    struct Entry {
+        const void* kernel;
+        size_t lds;
+        int occ;
+    };
+    static std::mutex mutex;
+    static Entry cache[64];
+    static int used = 0;
+    std::lock_guard<std::mutex> lock(mutex);
+    for (int i = 0; i < used; ++i)
+        if (cache[i].kernel == kernel && cache[i].lds == lds_bytes) return cache[i].occ;
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, 64 * kDecodeWaves, lds_bytes) != hipSuccess) {
         (void)hipGetLastError();    // a failed query must not surface as the launch's error
-        occ = 1;
+        return 1;
     }
     if (occ < 1) occ = 1;
-    const int64_t slots = (int64_t)occ * kCUs;
-    if (tiles <= slots || K / kGroup < kDecodeWaves) return 0;
+    if (used < 64) cache[used++] = Entry{kernel, lds_bytes, occ};
+    return occ;
+}
+
+static unsigned decode_grid(const void* kernel, size_t lds_bytes, int K, int64_t tiles) {
+    if (tiles <= kCUs || K / kGroup < kDecodeWaves) return 0;     // one round whatever the occupancy
+    const int64_t slots = (int64_t)decode_occupancy(kernel, lds_bytes) * kCUs;
+    if (tiles <= slots) return 0;
     const int64_t per = (tiles + slots - 1) / slots;
     if (per > 64) return (unsigned)(((tiles + 63) / 64 + 7) / 8 * 8);
     return (unsigned)slots;
