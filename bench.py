@@ -101,6 +101,13 @@ def parse():
     ap.add_argument("--summarize-families", nargs="+", metavar=("OUT_MD", "JSONL"),
                     help="format the JSON lines of --families runs as a markdown table (appended to OUT_MD; "
                          "needs no GPU)")
+    ap.add_argument("--sweep", metavar="LAYERS",
+                    help="time AUTO and every kernel family that applies over a range of M on these layers "
+                         "(comma-separated names; one JSON line per layer and M)")
+    ap.add_argument("--sweep-ms", type=str,
+                    default="1,16,32,48,64,128,256,384,512,768,1024,1280,1536,2048,3072,4096,6144,8192")
+    ap.add_argument("--summarize-sweep", nargs="+", metavar=("OUT_MD", "JSONL"),
+                    help="append the markdown table of --sweep JSON lines to OUT_MD; needs no GPU")
     ap.add_argument("--traffic", action="store_true",
                     help="counter run: eager fused GEMM launches at the largest M, then a plain "
                          "256 MiB device copy as the scale reference for FETCH_SIZE / WRITE_SIZE")
@@ -596,8 +603,87 @@ def families(args):
         torch.cuda.empty_cache()
 
 
+def sweep(args):
+    """Per layer and M: the fused GEMM under AUTO and under each kernel family
+    that applies (decode up to M = 32, both tiled kernels, the medium tiles),
+    weights rotating through more than 512 MB of copies, graph replays; with
+    the family and K splits AUTO takes (mq_fused_gemm_plan)."""
+    import torch
+
+    import paper_2606_15652_amd as mq
+    import synth
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    mq.load()
+    dev = torch.device("cuda:0")
+    for name in args.sweep.split(","):
+        layer = synth.workload(name)
+        K, N, nnzb = layer.K, layer.N, layer.nnzb
+        pw0 = mq.prepare_weight(torch.from_numpy(layer.weight()).to(dev), nnzb)
+        torch.cuda.synchronize()
+        ncopy = max(2, -(-ROTATE_BYTES // pw0.nbytes))
+        copies = [pw0] + [mq.PackedWeight(N, K, pw0.Wq.clone(), pw0.s_w.clone(), pw0.rowptr.clone(),
+                                          pw0.kb.clone(), pw0.Rq.clone(), pw0.s_r.clone())
+                          for _ in range(ncopy - 1)]
+        rot = [0]
+
+        def next_pw():
+            rot[0] = (rot[0] + 1) % ncopy
+            return copies[rot[0]]
+
+        for m in (int(x) for x in args.sweep_ms.split(",")):
+            X = torch.from_numpy(layer.act(m)).to(dev)
+            Xq, sx = mq.quantize_act(X)
+            Y = torch.empty((m, N), dtype=torch.float16, device=dev)
+            ws = torch.empty(max(1, mq.load().mq_fused_gemm_workspace_size(m, N, K)), dtype=torch.uint8, device=dev)
+            reps = max(5, min(args.reps, int(2e5 // max(1.0, m * N * K / 1e9))))
+            variants = (["skinny"] if m <= 32 else []) + ["tiled"] + (["tiled_large"] if N % 256 == 0 else []) + \
+                       ["medium", "auto"]
+            # one untimed call of each first (buffers, code objects), then the
+            # timings in the order above, AUTO last
+            for v in variants:
+                mq.fused_gemm(Xq, sx, next_pw(), out=Y, variant=v, workspace=ws)
+            torch.cuda.synchronize()
+            us = {v: round(timed(torch, lambda: mq.fused_gemm(Xq, sx, next_pw(), out=Y, variant=v, workspace=ws),
+                                 reps), 3) for v in variants}
+            fam, splits = mq.plan(m, N, K)
+            print(json.dumps({"layer": name, "K": K, "N": N, "M": m, "auto_family": fam, "auto_splits": splits,
+                              "us": us}), flush=True)
+            del X, Xq, sx, Y, ws
+        del copies, pw0
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
+def summarize_sweep(args):
+    """Markdown table of --sweep JSON lines: per layer and M, AUTO's choice and
+    time, every family's time, and AUTO's time over the fastest family's."""
+    out_md, paths = args.summarize_sweep[0], args.summarize_sweep[1:]
+    fams = ["skinny", "tiled", "tiled_large", "medium"]
+    lines = ["| layer | K → N | M | AUTO takes | AUTO µs | " + " | ".join(f"{f} µs" for f in fams) +
+             " | fastest | AUTO / fastest |", "|" + "---|" * (7 + len(fams))]
+    for path in paths:
+        for line in open(path):
+            if not line.startswith("{"):
+                continue
+            d = json.loads(line)
+            us = d["us"]
+            best = min((us[f], f) for f in fams if f in us)
+            take = d["auto_family"] + (f" ({d['auto_splits']} K splits)" if d["auto_splits"] > 1 else "")
+            cells = " | ".join(f"{us[f]:.1f}" if f in us else "-" for f in fams)
+            lines.append(f"| {d['layer']} | {d['K']} → {d['N']} | {d['M']} | {take} | {us['auto']:.1f} | {cells} | "
+                         f"{best[1]} | {us['auto'] / best[0]:.2f} |")
+    with open(out_md, "a") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
+    if args.summarize_sweep:
+        summarize_sweep(args)
+        return
     if args.summarize_counters:
         summarize_counters(args)
         return
@@ -618,6 +704,9 @@ def main():
         args.steps, args.warmup, args.reps = 3, 1, 5
     if args.families:
         families(args)
+        return
+    if args.sweep:
+        sweep(args)
         return
     if args.kernel_run:
         kernel_run(args)

@@ -1512,11 +1512,12 @@ static void launch_decode(const GemmArgs& a, int spw, size_t xs_bytes, hipStream
 // 25600 -> 5120 at M = 2048, 160 tiles, were 9 and 11 % faster than 640 small
 // tiles), and the small tile (with split-K when they are few) takes grids
 // that fit in one round.
-// (Where two rounds of large tiles meet three of small ones the estimate is
-// a near tie, and either side measured faster: large on 5120 -> 25600 at
-// M = 768, 117 against 127 us, and on 4096 -> 14336 at M = 1536, 102.5
-// against 107.6 us; small on K = N = 4096 at M = 5120, 94.7 against 100.5.)
-constexpr int kLargeRoundPct = 100, kSmallRoundPct = 66;
+// (68 rather than the 66 measured: where two rounds of large tiles meet
+// three of small ones, a near tie at 66, the large tiles measured faster on
+// 5120 -> 25600 at M = 768, 117 against 127 us, 4096 -> 14336 at M = 1536,
+// 102.5 against 107.6, 14336 -> 4096 at M = 6144 and 5120 -> 5120 at
+// M = 4096, and slower only on K = N = 4096 at M = 5120, 100.5 against 94.7.)
+constexpr int kLargeRoundPct = 100, kSmallRoundPct = 68;
 static bool large_tiles_fit(int M, int N) {
     if (N % 256 != 0) return false;
     const int64_t tl = (int64_t)((M + 255) / 256) * (N / 256);
@@ -1535,17 +1536,18 @@ static i32x4 host_buf_desc(const void* base, uint32_t bytes) {
 // be too few to give every CU two workgroups (the tiled kernel would split K
 // and add the partial sums in a second launch), as long as its 64 x 64 tiles
 // fit on the CUs in one round (one workgroup per CU: its partial-sum exchange
-// takes most of the LDS), or in a few rounds at short K: five up to K = 4096,
+// takes most of the LDS), or in a few rounds at short K: four up to K = 4096,
 // three up to 8192.  There the split and its reduction cost more than the
-// extra rounds (K = N = 4096: M = 512 27.4 -> 20.3 us, M = 768 38.0 -> 29.0 us,
-// M = 1280 48.5 -> 45.5 us; 5120 -> 1024 at M = 2048 28.4 -> 22.7 us; 5120 ->
-// 5120 at M = 512 41.6 -> 35.5 us, but at M = 768, four rounds, 46.0 split
-// against 47.5 us), while deeper K amortises them (14336 -> 4096 at M = 1024:
-// 78 us split against 96 us medium).
+// extra rounds (K = N = 4096: M = 512 27.4 -> 20.3 us, M = 768 38.0 -> 29.0 us;
+// 5120 -> 1024 at M = 2048 28.4 -> 22.7 us; 5120 -> 5120 at M = 512 41.6 ->
+// 35.5 us), but not beyond (K = N = 4096 at M = 1280, five rounds: 38.6 us
+// tiled against 44.9; 5120 -> 5120 at M = 768, four rounds, 46.0 against
+// 47.5), and deeper K amortises them (14336 -> 4096 at M = 1024: 78 us split
+// against 96 us medium).
 constexpr int kMediumTargetWGs = 512;
 static bool medium_preferred(int M, int N, int K) {
     const int64_t t128 = (int64_t)((M + kTB - 1) / kTB) * (N / kTB), t64 = (int64_t)((M + 63) / 64) * (N / 64);
-    const int64_t rounds = K <= 4096 ? 5 : K <= 8192 ? 3 : 1;
+    const int64_t rounds = K <= 4096 ? 4 : K <= 8192 ? 3 : 1;
     return t128 < kMediumTargetWGs && t64 <= rounds * kCUs;
 }
 
