@@ -1537,7 +1537,8 @@ static i32x4 host_buf_desc(const void* base, uint32_t bytes) {
 // and add the partial sums in a second launch), as long as its 64 x 64 tiles
 // fit on the CUs in one round (one workgroup per CU: its partial-sum exchange
 // takes most of the LDS), or in a few rounds at short K: four up to K = 4096,
-// three up to 8192.  There the split and its reduction cost more than the
+// three and a half up to 8192 (5120 -> 25600 at M = 128, 3.1 rounds: 46.1 us
+// against 56.2 split).  There the split and its reduction cost more than the
 // extra rounds (K = N = 4096: M = 512 27.4 -> 20.3 us, M = 768 38.0 -> 29.0 us;
 // 5120 -> 1024 at M = 2048 28.4 -> 22.7 us; 5120 -> 5120 at M = 512 41.6 ->
 // 35.5 us), but not beyond (K = N = 4096 at M = 1280, five rounds: 38.6 us
@@ -1547,8 +1548,9 @@ static i32x4 host_buf_desc(const void* base, uint32_t bytes) {
 constexpr int kMediumTargetWGs = 512;
 static bool medium_preferred(int M, int N, int K) {
     const int64_t t128 = (int64_t)((M + kTB - 1) / kTB) * (N / kTB), t64 = (int64_t)((M + 63) / 64) * (N / 64);
-    const int64_t rounds = K <= 4096 ? 4 : K <= 8192 ? 3 : 1;
-    return t128 < kMediumTargetWGs && t64 <= rounds * kCUs;
+    // (in half rounds)
+    const int64_t half_rounds = K <= 4096 ? 8 : K <= 8192 ? 7 : 2;
+    return t128 < kMediumTargetWGs && 2 * t64 <= half_rounds * kCUs;
 }
 
 // Byte sizes of the operands and buffer resources spanning each of them.

@@ -187,6 +187,7 @@ PLANS = [
     ((4096, 384, 4096), ("medium", 1)), ((4096, 384, 14336), ("tiled", 4)),
     ((1024, 4096, 4096), ("medium", 1)), ((1280, 4096, 4096), ("tiled", 1)), ((4096, 5120, 5120), ("tiled_large", 1)),
     ((6144, 4096, 14336), ("tiled_large", 1)), ((768, 25600, 5120), ("tiled_large", 1)),
+    ((128, 25600, 5120), ("medium", 1)),
 ]
 
 
