@@ -1387,17 +1387,22 @@ __global__ __launch_bounds__(64 * kDecodeWaves) void gemm_stream_kernel(GemmArgs
 constexpr int kSkinnyMaxM = 32;
 constexpr int kSkinnyAutoM = 32;   // AUTO picks the skinny kernel up to this M
 
-// Strips per decode tile from two rows on: two when that still gives every
-// CU a workgroup (a tile's adjacent strips share DRAM pages and the block
-// row's CSR entries), else one.  (Four measured no faster than two on the
-// 5120 -> 25600 layer at one token, slightly slower.)  At one row the callers
-// take one strip: there the tiles outnumber a round of workgroups on wide
-// layers, and smaller tiles balance the workgroups that take several.
+// Strips per decode tile: two when that still gives every CU a workgroup (a
+// tile's adjacent strips share DRAM pages and the block row's CSR entries),
+// else one.  (Four measured no faster than two on the 5120 -> 25600 layer at
+// one token, slightly slower.)
 constexpr int kCUs = 256;
 static int decode_spw(int N) {
     const int S = N / 16;
     if (S / 2 >= kCUs) return 2;
     return 1;
+}
+// at one row: two strips only while their tiles still fit in one round of
+// two workgroups a CU (4096 -> 14336: 11.0 -> 9.6 us); on wider layers one
+// strip, so that the workgroups that take several tiles stay balanced
+// (8192 -> 28672: 28.5 -> 27.3 us)
+static int decode_spw_one_row(int N) {
+    return N / 32 <= 2 * kCUs ? decode_spw(N) : 1;
 }
 
 // Decode grids (fused quantisation or staged activations): one workgroup per
@@ -1616,8 +1621,7 @@ static mq_status launch(mq_variant variant, const GemmArgs& args, void* workspac
         hipLaunchKernelGGL((gemm_tiled_kernel<8, 4, RAW, false>), dim3((unsigned)tiles), dim3(TS::kThreads), 0,
                            stream, a, 0, (float*)nullptr);
     } else if (variant == MQ_VARIANT_SKINNY) {
-        // (one strip a tile at one row, as for fused quantisation)
-        if (a.M <= 16) launch_decode<1, RAW, false>(a, a.M == 1 ? 1 : decode_spw(a.N), 0, stream);
+        if (a.M <= 16) launch_decode<1, RAW, false>(a, a.M == 1 ? decode_spw_one_row(a.N) : decode_spw(a.N), 0, stream);
         else launch_decode<2, RAW, false>(a, decode_spw(a.N), 0, stream);
     } else {
         const int64_t tiles = (int64_t)((a.M + kTB - 1) / kTB) * (a.N / kTB);
@@ -1846,10 +1850,9 @@ static mq_status linear_impl(int M, int N, int K, const void* X, int ldx,
         a.nnzb = nnzb;
         st = operand_resources<false>(a);
         if (st != MQ_OK) return st;
-        // one strip a tile at one row: more, smaller tiles balance the grid
-        // of workgroups that take several (5120 -> 25600: 19.9 -> 19.1 us;
-        // at four rows two strips measured faster)
-        launch_decode<1, false, true>(a, M == 1 ? 1 : decode_spw(N), (size_t)M * (K / 2), stream);
+        // (at four rows two strips measured faster than one on the wide
+        // layers, where one row takes one: 5120 -> 25600 19.9 -> 19.1 us)
+        launch_decode<1, false, true>(a, M == 1 ? decode_spw_one_row(N) : decode_spw(N), (size_t)M * (K / 2), stream);
         return mq_host::launch_status();
     }
     // quantise into the workspace, then the fused GEMM
